@@ -1,0 +1,359 @@
+#!/usr/bin/env python3
+"""Benchmark: the fused Layered SGD aggregate + update on one MI355X.
+
+One step is one fused lsgd_step launch over the whole workload: N = G*W worker
+gradients read, parameters and momentum read and written, R replicas written
+(Yu et al., arXiv 1906.05936, Alg. 3: local Reduce and divide, Allreduce over
+communicators, Broadcast, update). Inputs are synthetic and seeded (module
+`workloads`), already resident in HBM when the timed region starts; gradients
+are generated once before it.
+
+Prints ONE JSON line. `value` is achieved GB/s: the step's algorithmic bytes
+(N*n*s_g + 16n + R*n*s_r) divided by the average launch duration over the
+timed region (HIP events on the stream the kernel runs on). The roofline peak
+is MI355X's published 8 TB/s. `cpu_baseline` times the CPU oracle on a bounded
+sample of the same workload on this host (one thread).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--replicas R] [--no-cpu-baseline]
+       python bench.py --derive-traffic --fetch-csv F --write-csv W [--workload NAME]
+"""
+import argparse
+import ctypes
+import glob
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused LSGD aggregate+update: achieved HBM GB/s and steps/s, 1 MI355X"
+PEAK_HBM_GBPS = 8000.0                     # MI355X HBM3E, published peak
+PROFILES = os.path.join(ROOT, "profiles")
+CALIB_ELEMS = 1 << 28                      # 1 GiB of fp32 for the counter calibration kernel
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="resnet50_flat")
+    ap.add_argument("--replicas", type=int, default=-1, help="replicas written per step (default N)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget")
+    ap.add_argument("--no-r0", action="store_true", help="skip the secondary R=0 measurement")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also launch a plain 1 GiB negate-copy kernel (counter calibration)")
+    ap.add_argument("--derive-traffic", action="store_true")
+    ap.add_argument("--fetch-csv")
+    ap.add_argument("--write-csv")
+    return ap.parse_args(argv)
+
+
+# ---------------------------------------------------------------- workload setup
+
+class Setup:
+    """Device buffers of one workload and a zero-overhead step callable."""
+
+    def __init__(self, wl, R, dev):
+        import torch
+        import paper_1906_05936_amd as lsgd
+        import workloads
+        from paper_1906_05936_amd._lib import lib, ptr_array, int32_array, check
+
+        self.wl, self.R = wl, R
+        N, G = wl.n_workers, wl.groups
+        self.gow = workloads.contiguous_groups(G, wl.workers_per_group)
+        rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
+        stream = torch.cuda.current_stream(dev)
+        flat_p = workloads.init_params(wl, dev)
+        scratch = torch.empty(wl.n, device=dev) if wl.grad_dtype == "bf16" else None
+        if wl.tensor_sizes:
+            sizes = wl.tensor_sizes
+            self.params = workloads.split_tensors(flat_p, sizes)
+            del flat_p
+            self.mom = [torch.zeros_like(x) for x in self.params]
+            self.grads = []
+            tmp = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
+            for w in range(N):
+                workloads.fill_worker_grad(wl, 0, w, tmp, scratch)
+                self.grads.append(workloads.split_tensors(tmp, sizes))
+            del tmp
+            self.reps = [[torch.empty(s, device=dev, dtype=rtd) for s in sizes] for _ in range(R)]
+            self.plan = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps)
+            h = self.plan._handle
+            fn = lib.lsgd_step_plan
+            hyper = (ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd))
+            s = ctypes.c_void_p(stream.cuda_stream)
+
+            def step():
+                check(fn(h, *hyper, s))
+        else:
+            self.plan = None
+            self.params = [flat_p]
+            self.mom = [torch.zeros_like(flat_p)]
+            self.grads = []
+            for w in range(N):
+                g = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
+                workloads.fill_worker_grad(wl, 0, w, g, scratch)
+                self.grads.append([g])
+            self.reps = [[torch.empty(wl.n, device=dev, dtype=rtd)] for _ in range(R)]
+            fn = lib.lsgd_step
+            args = (self.params[0].data_ptr(), self.mom[0].data_ptr(),
+                    ptr_array([g[0].data_ptr() for g in self.grads]),
+                    1 if wl.grad_dtype == "bf16" else 0, N, int32_array(self.gow), G, wl.n,
+                    ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd),
+                    ptr_array([r[0].data_ptr() for r in self.reps]), R,
+                    1 if rtd == torch.bfloat16 else 0, ctypes.c_void_p(stream.cuda_stream))
+
+            def step():
+                check(fn(*args))
+        del scratch
+        self.step = step
+        self.stream = stream
+
+    def close(self):
+        if self.plan is not None:
+            self.plan.close()
+
+
+def time_steps(setup, steps, warmup):
+    """Average ms per step over `steps` back-to-back launches, HIP events on the
+    launch stream, synchronized on both sides."""
+    import torch
+    for _ in range(warmup):
+        setup.step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(setup.stream)
+    for _ in range(steps):
+        setup.step()
+    t1.record(setup.stream)
+    t1.synchronize()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def copy_ceiling(dev, calibrate):
+    """GB/s of a plain device copy (2 GiB read + 2 GiB written): a measured
+    ceiling to read the kernel's fraction against."""
+    import torch
+    n = 1 << 29
+    src = torch.ones(n, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    t1.synchronize()
+    gbps = 2 * n * 4 * reps / (t0.elapsed_time(t1) * 1e-3) / 1e9
+    if calibrate:
+        # plain negate-copy of a known size: its FETCH_SIZE / WRITE_SIZE counters
+        # calibrate the counters of the step kernel
+        a = src[:CALIB_ELEMS]
+        b = dst[:CALIB_ELEMS]
+        for _ in range(3):
+            torch.neg(a, out=b)
+        torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
+# ---------------------------------------------------------------- CPU baseline
+
+def cpu_baseline(setup, seconds):
+    """The oracle (plain C, one thread) on the first elements of the same inputs,
+    repeated until `seconds` have passed; scaled to GB/s and steps/s."""
+    import numpy as np
+    import torch
+    import oracle
+
+    wl, R = setup.wl, setup.R
+    S = min(wl.n, 1 << 20)
+
+    def head(tensors):
+        parts, got = [], 0
+        for t in tensors:
+            take = min(t.numel(), S - got)
+            parts.append(t[:take])
+            got += take
+            if got == S:
+                break
+        x = torch.cat(parts).cpu()
+        if x.dtype == torch.bfloat16:
+            return x.view(torch.int16).numpy().view(np.uint16).copy()
+        return x.numpy().copy()
+
+    p = head(setup.params)
+    m = head(setup.mom)
+    grads = [head(g) for g in setup.grads]
+    rdt = oracle.BF16 if wl.replica_dtype == "bf16" else oracle.F32
+    reps = [np.zeros(S, np.uint16 if rdt == oracle.BF16 else np.float32) for _ in range(R)]
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.lsgd_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, reps, rdt)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    elem_per_s = S * steps / el
+    per_elem = wl.algorithmic_bytes(R) / wl.n
+    return {"value": round(elem_per_s * per_elem / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "steps_per_s": round(elem_per_s / wl.n, 6),
+            "sample": "first %d of %d elements, all %d worker gradients and %d replicas, "
+                      "%d oracle steps in %.1f s on one host thread" % (S, wl.n, wl.n_workers, R,
+                                                                          steps, el)}
+
+
+# ---------------------------------------------------------------- counters
+
+def _read_counters(path):
+    import csv
+    rows = []
+    for f in sorted(glob.glob(path)) if any(c in path for c in "*?[") else [path]:
+        with open(f, newline="") as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def _per_dispatch_kib(rows, counter, match):
+    vals = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter or match not in r.get("Kernel_Name", ""):
+            continue
+        d = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        vals[d] = vals.get(d, 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise SystemExit("no %s rows for kernels matching %r" % (counter, match))
+    return sum(vals.values()) / len(vals), len(vals)
+
+
+def kernel_match(wl):
+    if wl.tensor_sizes:
+        return "step_plan_kernel"
+    return "step_flat_ct" if (wl.groups in (1, 2, 4, 8, 16) and
+                              wl.workers_per_group in (1, 2, 4, 8, 16)) else "step_flat_rt"
+
+
+def derive_traffic(args):
+    """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the step kernel, each scaled
+    by what the same counter reads for the plain 1 GiB negate-copy (4 bytes read
+    and 4 written per element) launched by --calibrate-copy."""
+    import workloads
+    from paper_1906_05936_amd import build as libbuild
+    wl = workloads.WORKLOADS[args.workload]
+    R = wl.n_workers if args.replicas < 0 else args.replicas
+    fetch_rows = _read_counters(args.fetch_csv)
+    write_rows = _read_counters(args.write_csv)
+    kname = kernel_match(wl)
+    f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
+    w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
+    f_c, _ = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", "neg")
+    w_c, _ = _per_dispatch_kib(write_rows, "WRITE_SIZE", "neg")
+    known = CALIB_ELEMS * 4 / 1024.0
+    f_scale, w_scale = known / f_c, known / w_c
+    fetch_b = f_k * f_scale * 1024
+    write_b = w_k * w_scale * 1024
+    alg = wl.algorithmic_bytes(R)
+    out = {"workload": wl.name, "replicas": R, "kernel": kname, "source_digest": libbuild.source_digest(),
+           "fetch_kib_per_dispatch": f_k, "write_kib_per_dispatch": w_k, "dispatches": [nf, nw],
+           "copy_fetch_kib": f_c, "copy_write_kib": w_c, "copy_known_kib": known,
+           "fetch_scale": f_scale, "write_scale": w_scale,
+           "traffic_bytes": fetch_b + write_b, "read_bytes": fetch_b, "write_bytes": write_b,
+           "algorithmic_bytes": alg, "traffic_over_algorithmic": (fetch_b + write_b) / alg}
+    os.makedirs(PROFILES, exist_ok=True)
+    path = os.path.join(PROFILES, "traffic_%s_R%d.json" % (wl.name, R))
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
+def stored_traffic(wl, R):
+    from paper_1906_05936_amd import build as libbuild
+    path = os.path.join(PROFILES, "traffic_%s_R%d.json" % (wl.name, R))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_digest") != libbuild.source_digest():
+        return None          # the kernels changed since the counters were taken
+    return t["traffic_bytes"]
+
+
+# ---------------------------------------------------------------- main
+
+def main(argv=None):
+    args = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world > 1:
+        print("bench.py measures one GPU: every worker gradient of the workload sits in that "
+              "GPU's HBM (one GPU's share of the aggregation); runs on %d GPUs are not part of "
+              "this build." % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    if args.derive_traffic:
+        derive_traffic(args)
+        return
+    import torch
+    import workloads
+
+    wl = workloads.WORKLOADS[args.workload]
+    R = wl.n_workers if args.replicas < 0 else args.replicas
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print("bench: %s n=%d G=%d W=%d %s R=%d" % (wl.name, wl.n, wl.groups, wl.workers_per_group,
+                                               wl.grad_dtype, R), file=sys.stderr, flush=True)
+    ceiling = copy_ceiling(dev, args.calibrate_copy)
+    setup = Setup(wl, R, dev)
+    ms = time_steps(setup, args.steps, args.warmup)
+    alg = wl.algorithmic_bytes(R)
+    gbps = alg / (ms * 1e-3) / 1e9
+    traffic = stored_traffic(wl, R)
+    result = {
+        "metric": METRIC, "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n": wl.n, "groups": wl.groups,
+                   "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
+                   "replicas": R, "replica_dtype": wl.replica_dtype,
+                   "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1},
+        "steps_per_s": round(1e3 / ms, 2),
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes": alg,
+                     "kernel": kernel_match(wl)},
+        "copy_ceiling_GBps": round(ceiling, 1),
+    }
+    if R != 0 and not args.no_r0:
+        setup.close()
+        del setup
+        torch.cuda.empty_cache()
+        setup = Setup(wl, 0, dev)
+        ms0 = time_steps(setup, args.steps, args.warmup)
+        alg0 = wl.algorithmic_bytes(0)
+        result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
+                        "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),
+                        "frac": round(alg0 / (ms0 * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+        if not args.no_cpu_baseline:      # the baseline's replica count follows the headline
+            setup.R = R
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
+    setup.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

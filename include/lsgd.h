@@ -1,0 +1,186 @@
+/*
+ * lsgd.h - C ABI of liblsgd.so: the Layered SGD gradient aggregation and
+ * momentum-SGD update on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: K. Yu, T. Flynn, S. Yoo, N. D'Imperio, "Layered SGD: A Decentralized
+ * and Synchronous SGD Algorithm for Scalable Deep Neural Network Training",
+ * arXiv 1906.05936. N = G*W workers each hold a gradient of the flat parameter
+ * vector w (Sec. 3, Alg. 2, "Delta w^i"). The workers are partitioned into G
+ * equal subgroups (Alg. 3 require line: worker index i, node index j of G nodes;
+ * Sec. 3: equal-cardinality partition). Per element, with PW the fixed pairwise
+ * sum described below:
+ *
+ *   group mean   m_j  = PW(g_{members[j][0]}, ..., g_{members[j][W-1]}) / W
+ *                       (Alg. 3: Reduce to the communicator and divide; Sec. 4.1 item 1)
+ *   global mean  gbar = PW(m_0, ..., m_{G-1}) / G
+ *                       (Alg. 3: Allreduce over communicators; Sec. 4.1 item 2)
+ *   update       d = gbar + weight_decay*w;  v = momentum_coef*v + d;  w = w - lr*v
+ *                       (Alg. 3 update step, the epsilon-step of Alg. 1/2, with the
+ *                        momentum and weight decay of Sec. 5.3)
+ *   copy-out     replica_r = w   (or w rounded to bfloat16, nearest-even)
+ *                       (Alg. 3: Broadcast to the workers from the communicator)
+ *
+ * PW(x[0..k)) = x[0] if k == 1, else PW(x[0..h)) + PW(x[h..k)) with h the largest
+ * power of two below k. Members of a group are taken in ascending worker id and
+ * groups in ascending group id. All arithmetic is binary32, each operation
+ * rounded to nearest-even, no fused multiply-add, subnormals kept; bf16
+ * gradients widen to binary32 exactly. Results are therefore deterministic and
+ * independent of launch shape. With W and G powers of two the two-level mean
+ * equals the flat mean over all N workers bit for bit (Sec. 4.2: Algorithms 2
+ * and 3 reach the same parameters).
+ *
+ * Conventions shared by every call:
+ *  - Memory. Every buffer argument is caller-owned device memory on the current
+ *    HIP device. Pointer ARRAYS (grads, replicas, group_means) are host arrays of
+ *    device pointers, read during the call only. The library keeps no pointer
+ *    after a call returns, except inside a plan.
+ *  - Streams. `stream` is a hipStream_t (NULL = the null stream). Calls validate,
+ *    enqueue on `stream` and return without synchronizing; outputs are ready when
+ *    the stream reaches that point.
+ *  - Validation happens before anything is enqueued. On any error nothing is
+ *    launched and no output is touched. n == 0 is a no-op that returns LSGD_OK
+ *    after the counts, dtypes and membership are validated (pointers may then
+ *    be NULL).
+ *  - Alignment. Every buffer must be 16-byte aligned (LSGD_ERR_ALIGN).
+ *  - Aliasing. Written buffers may not overlap each other or any read buffer
+ *    (LSGD_ERR_ALIAS). Read buffers may overlap each other (several workers may
+ *    pass the same gradient buffer).
+ *  - Non-finite values are not checked; NaN and Inf propagate.
+ *  - Thread safety. Calls on distinct streams and buffers may run concurrently.
+ *    lsgd_last_error() is per thread.
+ */
+#ifndef LSGD_H
+#define LSGD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define LSGD_API __attribute__((visibility("default")))
+#else
+#define LSGD_API
+#endif
+
+typedef enum lsgd_status {
+    LSGD_OK = 0,
+    LSGD_ERR_NULL = 1,   /* a required pointer (or pointer-array entry) is NULL        */
+    LSGD_ERR_SIZE = 2,   /* n < 0, or a count < 1 (< 0 for replicas) or above its max  */
+    LSGD_ERR_GROUPS = 3, /* group id out of [0,G), G does not divide N, unequal groups */
+    LSGD_ERR_ALIGN = 4,  /* a buffer is not 16-byte aligned                            */
+    LSGD_ERR_DTYPE = 5,  /* dtype is not one of lsgd_dtype                             */
+    LSGD_ERR_HIP = 6,    /* the HIP runtime reported an error; see lsgd_last_error()   */
+    LSGD_ERR_ALIAS = 7   /* a written buffer overlaps another buffer of the call       */
+} lsgd_status;
+
+typedef enum lsgd_dtype {
+    LSGD_F32 = 0,  /* IEEE binary32                                        */
+    LSGD_BF16 = 1  /* bfloat16: the upper 16 bits of a binary32, as uint16 */
+} lsgd_dtype;
+
+/* Planless calls carry their pointer tables in the kernel arguments, so every
+ * call accepts at most this many workers (hence groups) and replicas; plans
+ * keep the same limits. */
+#define LSGD_MAX_WORKERS 128
+#define LSGD_MAX_REPLICAS 128
+
+/* Static, never-NULL text for a status. */
+LSGD_API const char* lsgd_status_string(lsgd_status status);
+
+/* Detail of the last failing call made by this thread ("" if none). The
+ * string stays valid until the next failing call on this thread. */
+LSGD_API const char* lsgd_last_error(void);
+
+/*
+ * The local layer alone (Alg. 3, Reduce to the communicator and divide):
+ *   group_means[j][i] = PW over the W members of group j of grads[w][i], / W.
+ * grads          [n_workers] device pointers, each n elements of dtype gdt.
+ * group_of_worker[n_workers] host int32, the group of each worker, in [0, n_groups).
+ * group_means    [n_groups] device pointers, each n binary32 elements (written).
+ * 1 <= n_workers <= LSGD_MAX_WORKERS; n_groups divides n_workers and every group
+ * has exactly n_workers/n_groups members.
+ */
+LSGD_API lsgd_status lsgd_group_mean(const void* const* grads, lsgd_dtype gdt,
+                                     int32_t n_workers, const int32_t* group_of_worker,
+                                     int32_t n_groups, int64_t n,
+                                     float* const* group_means, void* stream);
+
+/*
+ * The global layer alone (Alg. 3, Allreduce over communicators), as a mean:
+ *   grad_mean[i] = PW(group_means[0][i], ..., group_means[n_groups-1][i]) / n_groups.
+ * group_means [n_groups] device pointers to n binary32 each; grad_mean n binary32
+ * (written). 1 <= n_groups <= LSGD_MAX_WORKERS.
+ */
+LSGD_API lsgd_status lsgd_global_mean(const float* const* group_means, int32_t n_groups,
+                                      int64_t n, float* grad_mean, void* stream);
+
+/*
+ * The update and copy-out alone (Alg. 3 update step and Broadcast; momentum and
+ * weight decay of Sec. 5.3), in place on params and momentum (n binary32 each):
+ *   d = grad_mean + weight_decay*params; momentum = momentum_coef*momentum + d;
+ *   params = params - lr*momentum; replicas[r] = params (dtype rdt).
+ * replicas: host array of n_replicas device pointers (may be NULL when
+ * n_replicas == 0), each n elements of dtype rdt. 0 <= n_replicas <= LSGD_MAX_REPLICAS.
+ * A fresh momentum buffer is zero-filled by the caller.
+ */
+LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* grad_mean,
+                                   int64_t n, float lr, float momentum_coef,
+                                   float weight_decay, void* const* replicas,
+                                   int32_t n_replicas, lsgd_dtype rdt, void* stream);
+
+/*
+ * One fused Layered SGD step: group means, global mean, update and copy-out in
+ * one pass over memory. Reads every gradient, parameter and momentum element
+ * once; writes parameters, momentum and the replicas once. Arguments as for the
+ * three calls above. The results are bit-identical to lsgd_group_mean, then
+ * lsgd_global_mean, then lsgd_sgd_step.
+ */
+LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
+                               lsgd_dtype gdt, int32_t n_workers,
+                               const int32_t* group_of_worker, int32_t n_groups, int64_t n,
+                               float lr, float momentum_coef, float weight_decay,
+                               void* const* replicas, int32_t n_replicas, lsgd_dtype rdt,
+                               void* stream);
+
+/*
+ * Multi-tensor plan: the fused step over a model's list of parameter tensors
+ * (e.g. the 161 tensors of ResNet-50, the model of Sec. 5.3) in ONE kernel
+ * launch. The plan copies a chunk table and a pointer table to device memory
+ * once; lsgd_step_plan then launches one kernel. Small tensors are bucketed so
+ * that one workgroup covers several of them.
+ *   numel     [n_tensors] host int64, elements of each tensor (>= 0).
+ *   params, momentum [n_tensors] device pointers (binary32).
+ *   grads     [n_workers * n_tensors] device pointers, worker-major:
+ *             grads[w * n_tensors + t] is worker w's gradient of tensor t.
+ *   replicas  [n_replicas * n_tensors] device pointers, replica-major, or NULL
+ *             when n_replicas == 0.
+ * The plan holds the pointers: the tensors must stay allocated, unmoved, while
+ * the plan is used. Counts: n_tensors >= 1, 1 <= n_workers <= LSGD_MAX_WORKERS,
+ * 0 <= n_replicas <= LSGD_MAX_REPLICAS. The plan is bound to the device current
+ * at creation.
+ * lsgd_plan_create allocates device memory (LSGD_ERR_HIP if that fails) and
+ * synchronizes the null stream once; lsgd_step_plan allocates nothing.
+ */
+typedef struct lsgd_plan lsgd_plan;
+
+LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const int64_t* numel,
+                                      float* const* params, float* const* momentum,
+                                      const void* const* grads, lsgd_dtype gdt,
+                                      int32_t n_workers, const int32_t* group_of_worker,
+                                      int32_t n_groups, void* const* replicas,
+                                      int32_t n_replicas, lsgd_dtype rdt);
+
+LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
+                                    float weight_decay, void* stream);
+
+/* Frees the plan's device tables. NULL-safe. The caller synchronizes every
+ * stream that ran lsgd_step_plan with this plan first. */
+LSGD_API void lsgd_plan_destroy(lsgd_plan* plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSGD_H */

@@ -1,0 +1,12 @@
+"""Layered SGD (Yu et al., arXiv 1906.05936) gradient aggregation and update on
+AMD Instinct MI355X.
+
+The computation lives in liblsgd.so (hand-written HIP for gfx950) behind the C
+ABI of include/lsgd.h; this package is its Python binding. Importing it fails
+loudly if the library has not been built: there is no fallback path.
+"""
+from ._lib import (BF16, F32, LIB_PATH, MAX_REPLICAS, MAX_WORKERS, LsgdError, Plan, global_mean,
+                   group_mean, sgd_step, step)
+
+__all__ = ["BF16", "F32", "LIB_PATH", "MAX_REPLICAS", "MAX_WORKERS", "LsgdError", "Plan",
+           "global_mean", "group_mean", "sgd_step", "step"]

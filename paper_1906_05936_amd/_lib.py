@@ -1,0 +1,264 @@
+"""ctypes binding of liblsgd.so. Argument marshalling only: every step of the
+method runs in the library's HIP kernels. torch supplies device memory and the
+stream; nothing here computes on tensor values.
+
+The C ABI is declared in include/lsgd.h; the Python names mirror it:
+``group_mean`` -> lsgd_group_mean, ``global_mean`` -> lsgd_global_mean,
+``sgd_step`` -> lsgd_sgd_step, ``step`` -> lsgd_step, ``Plan`` ->
+lsgd_plan_create / lsgd_step_plan / lsgd_plan_destroy.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblsgd.so")
+
+F32 = 0
+BF16 = 1
+MAX_WORKERS = 128
+MAX_REPLICAS = 128
+
+STATUS_NAMES = {0: "LSGD_OK", 1: "LSGD_ERR_NULL", 2: "LSGD_ERR_SIZE", 3: "LSGD_ERR_GROUPS",
+                4: "LSGD_ERR_ALIGN", 5: "LSGD_ERR_DTYPE", 6: "LSGD_ERR_HIP", 7: "LSGD_ERR_ALIAS"}
+
+EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_group_mean", "lsgd_global_mean",
+           "lsgd_sgd_step", "lsgd_step", "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy")
+
+
+class LsgdError(RuntimeError):
+    """A non-OK lsgd_status, with the library's detail text."""
+
+    def __init__(self, status, detail):
+        self.status = status
+        self.name = STATUS_NAMES.get(status, str(status))
+        super().__init__("%s: %s" % (self.name, detail))
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("liblsgd.so is not built (expected at %s); run "
+                          "`python -c 'import __graft_entry__ as g; g.build()'` first" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    c_int = ctypes.c_int
+    lib.lsgd_status_string.argtypes, lib.lsgd_status_string.restype = [c_int], ctypes.c_char_p
+    lib.lsgd_last_error.argtypes, lib.lsgd_last_error.restype = [], ctypes.c_char_p
+    lib.lsgd_group_mean.argtypes = [P, c_int, i32, P, i32, i64, P, P]
+    lib.lsgd_global_mean.argtypes = [P, i32, i64, P, P]
+    lib.lsgd_sgd_step.argtypes = [P, P, P, i64, f32, f32, f32, P, i32, c_int, P]
+    lib.lsgd_step.argtypes = [P, P, P, c_int, i32, P, i32, i64, f32, f32, f32, P, i32, c_int, P]
+    lib.lsgd_plan_create.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, c_int, i32, P, i32, P, i32,
+                                     c_int]
+    lib.lsgd_step_plan.argtypes = [P, f32, f32, f32, P]
+    lib.lsgd_plan_destroy.argtypes, lib.lsgd_plan_destroy.restype = [P], None
+    for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
+                 "lsgd_plan_create", "lsgd_step_plan"):
+        getattr(lib, name).restype = c_int
+    return lib
+
+
+lib = _load()
+
+
+def check(status):
+    """Raise LsgdError for a non-OK status returned by the library."""
+    if status != 0:
+        raise LsgdError(status, lib.lsgd_last_error().decode(errors="replace"))
+
+
+def ptr_array(values):
+    """Host array of pointers (ints) for a pointer-array argument."""
+    arr = (ctypes.c_void_p * max(1, len(values)))()
+    for k, v in enumerate(values):
+        arr[k] = v
+    return arr
+
+
+def int32_array(values):
+    arr = (ctypes.c_int32 * max(1, len(values)))()
+    for k, v in enumerate(values):
+        arr[k] = int(v)
+    return arr
+
+
+def int64_array(values):
+    arr = (ctypes.c_int64 * max(1, len(values)))()
+    for k, v in enumerate(values):
+        arr[k] = int(v)
+    return arr
+
+
+def _dtype_code(t, what):
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError("%s must be float32 or bfloat16, got %s" % (what, t.dtype))
+
+
+def _common_dtype(tensors, what):
+    codes = {_dtype_code(t, what) for t in tensors}
+    if len(codes) > 1:
+        raise TypeError("all %s must share one dtype" % what)
+    return codes.pop() if codes else F32
+
+
+def _dev_tensor(t, what, dtype=None, numel=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % what)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor, got device %s" % (what, t.device))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (what, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (what, dtype, t.dtype))
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (what, t.numel(), numel))
+    return t
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def step(params, momentum, grads, group_of_worker, n_groups, lr, momentum_coef, weight_decay,
+         replicas=(), stream=None):
+    """lsgd_step: one fused Layered SGD step, in place on params and momentum.
+
+    params, momentum: float32 GPU tensors of n elements. grads: N tensors of n
+    elements (all float32 or all bfloat16). group_of_worker: N ints in
+    [0, n_groups). replicas: R tensors of n elements (all float32 or all
+    bfloat16). Enqueued on ``stream`` (default: the current stream).
+    """
+    n = params.numel()
+    dev = params.device
+    _dev_tensor(params, "params", torch.float32)
+    _dev_tensor(momentum, "momentum", torch.float32, n, dev)
+    for g in grads:
+        _dev_tensor(g, "grad", None, n, dev)
+    for r in replicas:
+        _dev_tensor(r, "replica", None, n, dev)
+    gdt = _common_dtype(grads, "grads")
+    rdt = _common_dtype(replicas, "replicas")
+    with torch.cuda.device(dev):
+        st = lib.lsgd_step(params.data_ptr(), momentum.data_ptr(),
+                           ptr_array([g.data_ptr() for g in grads]), gdt, len(grads),
+                           int32_array(group_of_worker), n_groups, n, lr, momentum_coef,
+                           weight_decay, ptr_array([r.data_ptr() for r in replicas]),
+                           len(replicas), rdt, _stream(stream, dev))
+    check(st)
+
+
+def group_mean(grads, group_of_worker, n_groups, out, stream=None):
+    """lsgd_group_mean: out[j] = mean over the members of group j (float32 tensors)."""
+    if not grads:
+        raise ValueError("grads is empty")
+    n = grads[0].numel()
+    dev = grads[0].device
+    for g in grads:
+        _dev_tensor(g, "grad", None, n, dev)
+    for o in out:
+        _dev_tensor(o, "group mean", torch.float32, n, dev)
+    if len(out) != n_groups:
+        raise ValueError("need %d output tensors, got %d" % (n_groups, len(out)))
+    gdt = _common_dtype(grads, "grads")
+    with torch.cuda.device(dev):
+        st = lib.lsgd_group_mean(ptr_array([g.data_ptr() for g in grads]), gdt, len(grads),
+                                 int32_array(group_of_worker), n_groups, n,
+                                 ptr_array([o.data_ptr() for o in out]), _stream(stream, dev))
+    check(st)
+
+
+def global_mean(group_means, out, stream=None):
+    """lsgd_global_mean: out = mean of the float32 group-mean tensors."""
+    n = out.numel()
+    dev = out.device
+    _dev_tensor(out, "grad mean", torch.float32)
+    for m in group_means:
+        _dev_tensor(m, "group mean", torch.float32, n, dev)
+    with torch.cuda.device(dev):
+        st = lib.lsgd_global_mean(ptr_array([m.data_ptr() for m in group_means]), len(group_means),
+                                  n, out.data_ptr(), _stream(stream, dev))
+    check(st)
+
+
+def sgd_step(params, momentum, grad_mean, lr, momentum_coef, weight_decay, replicas=(), stream=None):
+    """lsgd_sgd_step: update and copy-out from a precomputed mean gradient."""
+    n = params.numel()
+    dev = params.device
+    _dev_tensor(params, "params", torch.float32)
+    _dev_tensor(momentum, "momentum", torch.float32, n, dev)
+    _dev_tensor(grad_mean, "grad mean", torch.float32, n, dev)
+    for r in replicas:
+        _dev_tensor(r, "replica", None, n, dev)
+    rdt = _common_dtype(replicas, "replicas")
+    with torch.cuda.device(dev):
+        st = lib.lsgd_sgd_step(params.data_ptr(), momentum.data_ptr(), grad_mean.data_ptr(), n, lr,
+                               momentum_coef, weight_decay,
+                               ptr_array([r.data_ptr() for r in replicas]), len(replicas), rdt,
+                               _stream(stream, dev))
+    check(st)
+
+
+class Plan:
+    """lsgd_plan_*: the fused step over a list of parameter tensors, one launch.
+
+    params, momentum: T float32 tensors. grads: N lists (one per worker) of T
+    tensors, worker-major. replicas: R lists of T tensors. The plan keeps
+    references to every tensor so that none is freed while it is in use.
+    """
+
+    def __init__(self, params, momentum, grads, group_of_worker, n_groups, replicas=()):
+        T = len(params)
+        if len(momentum) != T or any(len(g) != T for g in grads) or any(len(r) != T for r in replicas):
+            raise ValueError("every tensor list must hold one tensor per parameter")
+        dev = params[0].device if T else None
+        numel = [p.numel() for p in params]
+        for t in range(T):
+            _dev_tensor(params[t], "params[%d]" % t, torch.float32, None, dev)
+            _dev_tensor(momentum[t], "momentum[%d]" % t, torch.float32, numel[t], dev)
+            for w, gl in enumerate(grads):
+                _dev_tensor(gl[t], "grads[%d][%d]" % (w, t), None, numel[t], dev)
+            for r, rl in enumerate(replicas):
+                _dev_tensor(rl[t], "replicas[%d][%d]" % (r, t), None, numel[t], dev)
+        gdt = _common_dtype([g for gl in grads for g in gl], "grads")
+        rdt = _common_dtype([r for rl in replicas for r in rl], "replicas")
+        self.device = dev
+        self._keep = (list(params), list(momentum), [list(g) for g in grads],
+                      [list(r) for r in replicas])
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(dev):
+            st = lib.lsgd_plan_create(
+                ctypes.byref(handle), T, int64_array(numel),
+                ptr_array([p.data_ptr() for p in params]),
+                ptr_array([m.data_ptr() for m in momentum]),
+                ptr_array([g.data_ptr() for gl in grads for g in gl]), gdt, len(grads),
+                int32_array(group_of_worker), n_groups,
+                ptr_array([r.data_ptr() for rl in replicas for r in rl]), len(replicas), rdt)
+        check(st)
+        self._handle = handle
+
+    def step(self, lr, momentum_coef, weight_decay, stream=None):
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        with torch.cuda.device(self.device):
+            check(lib.lsgd_step_plan(self._handle, lr, momentum_coef, weight_decay,
+                                     _stream(stream, self.device)))
+
+    def close(self):
+        if getattr(self, "_handle", None) is not None:
+            torch.cuda.synchronize(self.device)
+            lib.lsgd_plan_destroy(self._handle)
+            self._handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,74 @@
+"""Builds liblsgd.so (HIP, gfx950) in-tree next to this file.
+
+Every translation unit is compiled with:
+  -ffp-contract=off       no a*b+c contraction into fused multiply-add: each
+                          operation of the update is rounded on its own;
+  -Xclang -target-feature -Xclang -packed-fp32-ops
+                          no packed binary32 instructions (v_pk_*_f32);
+  -fvisibility=hidden     only the LSGD_API (extern "C") symbols are exported.
+"""
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD_DIR = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "liblsgd.so")
+SOURCES = ["lsgd_common.hip", "lsgd_flat.hip", "lsgd_plan.hip"]
+ARCH = "gfx950"
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CFLAGS = [
+    "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
+    "-fvisibility=hidden", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-command-line-argument", "-I" + INCLUDE, "-I" + CSRC,
+]
+
+
+def _compile(src, verbose):
+    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC] + CFLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    if verbose:
+        print(" ".join(cmd), file=sys.stderr)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, r.stdout, r.stderr))
+    return obj
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    jobs = min(len(SOURCES), max(1, min(16, os.cpu_count() or 1)))
+    with ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
+    if verbose:
+        print(" ".join(cmd), file=sys.stderr)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def source_digest() -> str:
+    """SHA-256 over the kernel sources, the public header and the build flags:
+    identifies the kernels a stored profile was taken from."""
+    import hashlib
+    h = hashlib.sha256()
+    h.update(" ".join(CFLAGS).replace(ROOT, "").encode())
+    files = sorted(os.listdir(CSRC))
+    for name in files:
+        if name.endswith((".hip", ".hpp")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    with open(os.path.join(INCLUDE, "lsgd.h"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,142 @@
+// Host helpers of liblsgd: error reporting, membership validation, aliasing
+// checks and launch sizing.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <algorithm>
+#include <atomic>
+#include <mutex>
+
+#include "lsgd_host.hpp"
+#include "lsgd_kernels.hpp"
+
+namespace lsgd {
+
+namespace {
+thread_local std::string t_last_error;
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+
+// Workgroups per compute unit for grid-stride launches. LSGD_BLOCKS_PER_CU
+// overrides it (read once); 0 means one unit per thread, no grid-stride.
+int blocks_per_cu() {
+    static const int v = [] {
+        const char* e = getenv("LSGD_BLOCKS_PER_CU");
+        if (e && *e) {
+            int x = atoi(e);
+            if (x >= 0) return x;
+        }
+        return 8;
+    }();
+    return v;
+}
+}  // namespace
+
+lsgd_status fail(lsgd_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_last_error = buf;
+    return st;
+}
+
+lsgd_status check_launch(const char* what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(LSGD_ERR_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+    return LSGD_OK;
+}
+
+lsgd_status member_order(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
+                         std::vector<int32_t>& order) {
+    if (n_workers < 1 || n_workers > kMaxWorkers)
+        return fail(LSGD_ERR_SIZE, "n_workers=%d outside [1, %d]", n_workers, kMaxWorkers);
+    if (n_groups < 1) return fail(LSGD_ERR_SIZE, "n_groups=%d < 1", n_groups);
+    if (!group_of_worker) return fail(LSGD_ERR_NULL, "group_of_worker is NULL");
+    if (n_workers % n_groups != 0)
+        return fail(LSGD_ERR_GROUPS, "n_groups=%d does not divide n_workers=%d", n_groups, n_workers);
+    const int32_t W = n_workers / n_groups;
+    std::vector<int32_t> fill(n_groups, 0);
+    order.assign(n_workers, -1);
+    for (int32_t i = 0; i < n_workers; ++i) {
+        const int32_t j = group_of_worker[i];
+        if (j < 0 || j >= n_groups)
+            return fail(LSGD_ERR_GROUPS, "group_of_worker[%d]=%d outside [0, %d)", i, j, n_groups);
+        if (fill[j] == W)
+            return fail(LSGD_ERR_GROUPS, "group %d has more than W=%d members", j, W);
+        order[static_cast<size_t>(j) * W + fill[j]++] = i;  // i ascends, so rows ascend
+    }
+    for (int32_t j = 0; j < n_groups; ++j)
+        if (fill[j] != W) return fail(LSGD_ERR_GROUPS, "group %d has %d members, expected %d", j, fill[j], W);
+    return LSGD_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+lsgd_status check_overlap(std::vector<Range>& ranges) {
+    ranges.erase(std::remove_if(ranges.begin(), ranges.end(),
+                                [](const Range& r) { return r.end <= r.begin; }),
+                 ranges.end());
+    std::sort(ranges.begin(), ranges.end(),
+              [](const Range& a, const Range& b) { return a.begin < b.begin; });
+    uintptr_t max_end_any = 0, max_end_written = 0;
+    const char* last_any = "";
+    const char* last_written = "";
+    for (const Range& r : ranges) {
+        if (r.written && r.begin < max_end_any)
+            return fail(LSGD_ERR_ALIAS, "written buffer %s overlaps %s", r.what, last_any);
+        if (!r.written && r.begin < max_end_written)
+            return fail(LSGD_ERR_ALIAS, "buffer %s overlaps written buffer %s", r.what, last_written);
+        if (r.end > max_end_any) { max_end_any = r.end; last_any = r.what; }
+        if (r.written && r.end > max_end_written) { max_end_written = r.end; last_written = r.what; }
+    }
+    return LSGD_OK;
+}
+
+int device_cus() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int c = g_cus[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0)
+        c = 256;
+    g_cus[dev].store(c, std::memory_order_relaxed);
+    return c;
+}
+
+unsigned grid_blocks(int64_t units) {
+    int64_t need = (units + kBlock - 1) / kBlock;
+    if (need < 1) need = 1;
+    const int bpc = blocks_per_cu();
+    if (bpc > 0) {
+        const int64_t cap = static_cast<int64_t>(device_cus()) * bpc;
+        if (need > cap) need = cap;
+    }
+    if (need > 0x7fffffff) need = 0x7fffffff;
+    return static_cast<unsigned>(need);
+}
+
+}  // namespace lsgd
+
+extern "C" {
+
+LSGD_API const char* lsgd_status_string(lsgd_status status) {
+    switch (status) {
+        case LSGD_OK: return "LSGD_OK";
+        case LSGD_ERR_NULL: return "LSGD_ERR_NULL: a required pointer is NULL";
+        case LSGD_ERR_SIZE: return "LSGD_ERR_SIZE: a size or count is out of range";
+        case LSGD_ERR_GROUPS: return "LSGD_ERR_GROUPS: invalid subgroup membership";
+        case LSGD_ERR_ALIGN: return "LSGD_ERR_ALIGN: a buffer is not 16-byte aligned";
+        case LSGD_ERR_DTYPE: return "LSGD_ERR_DTYPE: unsupported dtype";
+        case LSGD_ERR_HIP: return "LSGD_ERR_HIP: the HIP runtime reported an error";
+        case LSGD_ERR_ALIAS: return "LSGD_ERR_ALIAS: a written buffer overlaps another buffer";
+    }
+    return "unknown lsgd_status";
+}
+
+LSGD_API const char* lsgd_last_error(void) { return lsgd::t_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,233 @@
+// Planless entry points of liblsgd: lsgd_group_mean, lsgd_global_mean,
+// lsgd_sgd_step and the fused lsgd_step over one flat parameter vector.
+#include <string.h>
+
+#include "lsgd_host.hpp"
+#include "lsgd_kernels.hpp"
+
+namespace lsgd {
+namespace {
+
+using FlatKernel = void (*)(StepArgs);
+
+// Compile-time (W, G) kernels for power-of-two counts up to 16 each (and
+// N <= 128); every other grouping takes the runtime-count kernel. Both give
+// the same bits.
+template <typename GT, int W>
+FlatKernel pick_flat_g(int G) {
+    switch (G) {
+        case 1: return step_flat_ct<GT, W, 1>;
+        case 2: return step_flat_ct<GT, W, 2>;
+        case 4: return step_flat_ct<GT, W, 4>;
+        case 8: return step_flat_ct<GT, W, 8>;
+        case 16:
+            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16>;
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+template <typename GT>
+FlatKernel pick_flat(int W, int G) {
+    FlatKernel k = nullptr;
+    switch (W) {
+        case 1: k = pick_flat_g<GT, 1>(G); break;
+        case 2: k = pick_flat_g<GT, 2>(G); break;
+        case 4: k = pick_flat_g<GT, 4>(G); break;
+        case 8: k = pick_flat_g<GT, 8>(G); break;
+        case 16: k = pick_flat_g<GT, 16>(G); break;
+    }
+    return k ? k : step_flat_rt<GT>;
+}
+
+size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
+
+bool valid_dtype(lsgd_dtype d) { return d == LSGD_F32 || d == LSGD_BF16; }
+
+Range range_of(const void* p, int64_t n, size_t esize, bool written, const char* what) {
+    uintptr_t b = reinterpret_cast<uintptr_t>(p);
+    return Range{b, b + static_cast<uintptr_t>(n) * esize, written, what};
+}
+
+// Checks the replica list: count, dtype, non-NULL, alignment; appends ranges.
+lsgd_status check_replicas(void* const* replicas, int32_t n_replicas, lsgd_dtype rdt, int64_t n,
+                           bool check_ptrs, std::vector<Range>& ranges) {
+    if (n_replicas < 0 || n_replicas > kMaxReplicas)
+        return fail(LSGD_ERR_SIZE, "n_replicas=%d outside [0, %d]", n_replicas, kMaxReplicas);
+    if (!valid_dtype(rdt)) return fail(LSGD_ERR_DTYPE, "replica dtype %d", static_cast<int>(rdt));
+    if (!check_ptrs) return LSGD_OK;
+    if (n_replicas > 0 && !replicas) return fail(LSGD_ERR_NULL, "replicas is NULL with n_replicas=%d", n_replicas);
+    for (int32_t r = 0; r < n_replicas; ++r) {
+        if (!replicas[r]) return fail(LSGD_ERR_NULL, "replicas[%d] is NULL", r);
+        if (!aligned16(replicas[r])) return fail(LSGD_ERR_ALIGN, "replicas[%d] is not 16-byte aligned", r);
+        ranges.push_back(range_of(replicas[r], n, dtype_size(rdt), true, "replica"));
+    }
+    return LSGD_OK;
+}
+
+lsgd_status check_update_buffers(float* params, float* momentum, int64_t n, std::vector<Range>& ranges) {
+    if (!params) return fail(LSGD_ERR_NULL, "params is NULL");
+    if (!momentum) return fail(LSGD_ERR_NULL, "momentum is NULL");
+    if (!aligned16(params)) return fail(LSGD_ERR_ALIGN, "params is not 16-byte aligned");
+    if (!aligned16(momentum)) return fail(LSGD_ERR_ALIGN, "momentum is not 16-byte aligned");
+    ranges.push_back(range_of(params, n, 4, true, "params"));
+    ranges.push_back(range_of(momentum, n, 4, true, "momentum"));
+    return LSGD_OK;
+}
+
+// Gradient pointers in member order (entry j*W + k) with their ranges.
+lsgd_status check_grads(const void* const* grads, lsgd_dtype gdt, const std::vector<int32_t>& order,
+                        int64_t n, bool check_ptrs, const void** out, std::vector<Range>& ranges) {
+    if (!valid_dtype(gdt)) return fail(LSGD_ERR_DTYPE, "gradient dtype %d", static_cast<int>(gdt));
+    if (!check_ptrs) return LSGD_OK;
+    if (!grads) return fail(LSGD_ERR_NULL, "grads is NULL");
+    for (size_t k = 0; k < order.size(); ++k) {
+        const void* g = grads[order[k]];
+        if (!g) return fail(LSGD_ERR_NULL, "grads[%d] is NULL", order[k]);
+        if (!aligned16(g)) return fail(LSGD_ERR_ALIGN, "grads[%d] is not 16-byte aligned", order[k]);
+        out[k] = g;
+        ranges.push_back(range_of(g, n, dtype_size(gdt), false, "grad"));
+    }
+    return LSGD_OK;
+}
+
+}  // namespace
+}  // namespace lsgd
+
+using namespace lsgd;
+
+extern "C" {
+
+LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
+                               lsgd_dtype gdt, int32_t n_workers, const int32_t* group_of_worker,
+                               int32_t n_groups, int64_t n, float lr, float momentum_coef,
+                               float weight_decay, void* const* replicas, int32_t n_replicas,
+                               lsgd_dtype rdt, void* stream) {
+    if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
+    std::vector<int32_t> order;
+    lsgd_status st = member_order(n_workers, group_of_worker, n_groups, order);
+    if (st != LSGD_OK) return st;
+    const bool live = n > 0;
+    StepArgs a;
+    memset(&a, 0, sizeof a);
+    std::vector<Range> ranges;
+    if ((st = check_grads(grads, gdt, order, n, live, a.grads, ranges)) != LSGD_OK) return st;
+    if ((st = check_replicas(replicas, n_replicas, rdt, n, live, ranges)) != LSGD_OK) return st;
+    if (!live) return LSGD_OK;
+    if ((st = check_update_buffers(params, momentum, n, ranges)) != LSGD_OK) return st;
+    if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+
+    a.p = params;
+    a.m = momentum;
+    a.n = n;
+    a.h = Hyper{lr, momentum_coef, weight_decay};
+    a.n_workers = n_workers;
+    a.n_groups = n_groups;
+    a.W = n_workers / n_groups;
+    a.n_replicas = n_replicas;
+    a.rdt = static_cast<int32_t>(rdt);
+    for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
+
+    const int vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
+    const unsigned blocks = grid_blocks(n / vec);
+    FlatKernel k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    hipLaunchKernelGGL(k, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_step");
+}
+
+LSGD_API lsgd_status lsgd_group_mean(const void* const* grads, lsgd_dtype gdt, int32_t n_workers,
+                                     const int32_t* group_of_worker, int32_t n_groups, int64_t n,
+                                     float* const* group_means, void* stream) {
+    if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
+    std::vector<int32_t> order;
+    lsgd_status st = member_order(n_workers, group_of_worker, n_groups, order);
+    if (st != LSGD_OK) return st;
+    const bool live = n > 0;
+    MeanArgs a;
+    memset(&a, 0, sizeof a);
+    std::vector<Range> ranges;
+    if ((st = check_grads(grads, gdt, order, n, live, a.in, ranges)) != LSGD_OK) return st;
+    if (!live) return LSGD_OK;
+    if (!group_means) return fail(LSGD_ERR_NULL, "group_means is NULL");
+    for (int32_t j = 0; j < n_groups; ++j) {
+        if (!group_means[j]) return fail(LSGD_ERR_NULL, "group_means[%d] is NULL", j);
+        if (!aligned16(group_means[j])) return fail(LSGD_ERR_ALIGN, "group_means[%d] is not 16-byte aligned", j);
+        ranges.push_back(range_of(group_means[j], n, 4, true, "group_mean"));
+        a.out[j] = group_means[j];
+    }
+    if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+    a.n = n;
+    a.n_workers = n_workers;
+    a.n_groups = n_groups;
+    a.W = n_workers / n_groups;
+    const int vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
+    const unsigned blocks = grid_blocks(n / vec);
+    if (gdt == LSGD_BF16)
+        hipLaunchKernelGGL(group_mean_kernel<uint16_t>, dim3(blocks), dim3(kBlock), 0,
+                           static_cast<hipStream_t>(stream), a);
+    else
+        hipLaunchKernelGGL(group_mean_kernel<float>, dim3(blocks), dim3(kBlock), 0,
+                           static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_group_mean");
+}
+
+LSGD_API lsgd_status lsgd_global_mean(const float* const* group_means, int32_t n_groups, int64_t n,
+                                      float* grad_mean, void* stream) {
+    if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
+    if (n_groups < 1 || n_groups > kMaxWorkers)
+        return fail(LSGD_ERR_SIZE, "n_groups=%d outside [1, %d]", n_groups, kMaxWorkers);
+    if (n == 0) return LSGD_OK;
+    if (!group_means) return fail(LSGD_ERR_NULL, "group_means is NULL");
+    if (!grad_mean) return fail(LSGD_ERR_NULL, "grad_mean is NULL");
+    if (!aligned16(grad_mean)) return fail(LSGD_ERR_ALIGN, "grad_mean is not 16-byte aligned");
+    MeanArgs a;
+    memset(&a, 0, sizeof a);
+    std::vector<Range> ranges;
+    for (int32_t j = 0; j < n_groups; ++j) {
+        if (!group_means[j]) return fail(LSGD_ERR_NULL, "group_means[%d] is NULL", j);
+        if (!aligned16(group_means[j])) return fail(LSGD_ERR_ALIGN, "group_means[%d] is not 16-byte aligned", j);
+        ranges.push_back(range_of(group_means[j], n, 4, false, "group_mean"));
+        a.in[j] = group_means[j];
+    }
+    ranges.push_back(range_of(grad_mean, n, 4, true, "grad_mean"));
+    lsgd_status st = check_overlap(ranges);
+    if (st != LSGD_OK) return st;
+    a.out[0] = grad_mean;
+    a.n = n;
+    a.n_groups = n_groups;
+    hipLaunchKernelGGL(global_mean_kernel, dim3(grid_blocks(n / 4)), dim3(kBlock), 0,
+                       static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_global_mean");
+}
+
+LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* grad_mean, int64_t n,
+                                   float lr, float momentum_coef, float weight_decay,
+                                   void* const* replicas, int32_t n_replicas, lsgd_dtype rdt,
+                                   void* stream) {
+    if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
+    const bool live = n > 0;
+    std::vector<Range> ranges;
+    lsgd_status st = check_replicas(replicas, n_replicas, rdt, n, live, ranges);
+    if (st != LSGD_OK) return st;
+    if (!live) return LSGD_OK;
+    if ((st = check_update_buffers(params, momentum, n, ranges)) != LSGD_OK) return st;
+    if (!grad_mean) return fail(LSGD_ERR_NULL, "grad_mean is NULL");
+    if (!aligned16(grad_mean)) return fail(LSGD_ERR_ALIGN, "grad_mean is not 16-byte aligned");
+    ranges.push_back(range_of(grad_mean, n, 4, false, "grad_mean"));
+    if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+    StepArgs a;
+    memset(&a, 0, sizeof a);
+    a.p = params;
+    a.m = momentum;
+    a.gbar = grad_mean;
+    a.n = n;
+    a.h = Hyper{lr, momentum_coef, weight_decay};
+    a.n_replicas = n_replicas;
+    a.rdt = static_cast<int32_t>(rdt);
+    for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
+    hipLaunchKernelGGL(sgd_kernel, dim3(grid_blocks(n / 4)), dim3(kBlock), 0,
+                       static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_sgd_step");
+}
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Host-side helpers shared by the translation units of liblsgd: error text,
+// argument validation, the membership-to-member-order map and launch sizing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "lsgd.h"
+
+namespace lsgd {
+
+// Records the detail of a failing call for lsgd_last_error() and returns `st`.
+lsgd_status fail(lsgd_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+// hipGetLastError() after a launch, mapped to LSGD_ERR_HIP with its text.
+lsgd_status check_launch(const char* what);
+
+// Subgroup indexing: validates the worker->group map (every id in [0, G), G | N,
+// every group of exactly W = N/G members) and returns the member order, G rows
+// of W worker ids, each row ascending. Returns LSGD_OK or LSGD_ERR_GROUPS/SIZE.
+lsgd_status member_order(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
+                         std::vector<int32_t>& order);
+
+bool aligned16(const void* p);
+
+// A byte range [begin, end) of one buffer argument; `written` for outputs.
+struct Range {
+    uintptr_t begin, end;
+    bool written;
+    const char* what;
+};
+
+// LSGD_ERR_ALIAS if a written range overlaps any other range (empty ranges
+// never overlap). Sort-and-sweep, O(k log k).
+lsgd_status check_overlap(std::vector<Range>& ranges);
+
+// Blocks for a grid-stride launch over `units` 16-byte units on the current
+// device: min(ceil(units / kBlock), compute units * blocks-per-CU).
+unsigned grid_blocks(int64_t units);
+
+// Compute units of the current device (cached per device).
+int device_cus();
+
+inline bool is_pow2_le16(int x) { return x == 1 || x == 2 || x == 4 || x == 8 || x == 16; }
+
+}  // namespace lsgd

@@ -1,0 +1,529 @@
+// Device code of liblsgd: the Layered SGD aggregation and update for gfx950.
+//
+// Every step is elementwise along the parameter vector, so the kernels stream
+// HBM: each lane owns one 16-byte "unit" of the gradient layout (4 binary32 or
+// 8 bfloat16 elements), loads all N worker units of it with 128-bit nontemporal
+// loads, reduces them in registers in the fixed pairwise order, applies the
+// update and writes parameters, momentum and replicas with 128-bit stores.
+// No element is touched by two lanes, so there are no atomics, no LDS and no
+// cross-lane reductions: a lane's result depends only on its own inputs.
+//
+// Rounding contract (matches the header): binary32, one rounding per written
+// operation, no contraction into fused multiply-add.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#pragma clang fp contract(off)
+
+namespace lsgd {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kMaxWorkers = 128;   // == LSGD_MAX_WORKERS
+constexpr int kMaxReplicas = 128;  // == LSGD_MAX_REPLICAS
+constexpr int kBlock = 256;        // threads per workgroup (4 wave64)
+constexpr int kAccLevels = 8;      // runtime pairwise accumulator: counts up to 255
+
+enum : int { kF32 = 0, kBF16 = 1 };
+
+// Elements per 16-byte gradient unit. bf16 is carried as its uint16 bits.
+template <typename GT> struct Unit;
+template <> struct Unit<float> { static constexpr int VEC = 4; };
+template <> struct Unit<uint16_t> { static constexpr int VEC = 8; };
+
+// Largest power of two strictly below k (k >= 2): the split point of the
+// pairwise sum PW(x[0..k)) = PW(x[0..h)) + PW(x[h..k)).
+__host__ __device__ constexpr int pw_split(int k) {
+    int h = 1;
+    while (h * 2 < k) h *= 2;
+    return h;
+}
+
+// ---------------------------------------------------------------- loads/stores
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// binary32 -> bfloat16 bits, nearest-even via the carry of a 0x7fff(+1 if odd)
+// bias; NaN is returned as a quiet NaN of the same sign.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// One gradient unit of a worker, widened to binary32. TAIL units (the ragged end
+// of a tensor, cnt < VEC) read element by element and zero-fill the rest.
+template <typename GT, bool TAIL>
+__device__ __forceinline__ void load_grad(const void* g, int64_t e0, int cnt,
+                                          float (&x)[Unit<GT>::VEC]) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const GT* p = static_cast<const GT*>(g) + e0;
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            if constexpr (sizeof(GT) == 4) x[v] = v < cnt ? reinterpret_cast<const float*>(p)[v] : 0.f;
+            else x[v] = v < cnt ? bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(p)[v]) : 0.f;
+        }
+    } else if constexpr (sizeof(GT) == 4) {
+        f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+        x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    } else {
+        u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            x[2 * q] = __uint_as_float(t[q] << 16);
+            x[2 * q + 1] = __uint_as_float(t[q] & 0xffff0000u);
+        }
+    }
+}
+
+// VEC binary32 values at p + e0 (VEC is 4 or 8: one or two 128-bit accesses).
+template <int VEC, bool TAIL>
+__device__ __forceinline__ void load_f32(const float* p, int64_t e0, int cnt, float (&x)[VEC]) {
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) x[v] = v < cnt ? p[e0 + v] : 0.f;
+    } else {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + e0) + q);
+            x[4 * q] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
+        }
+    }
+}
+
+template <int VEC, bool TAIL>
+__device__ __forceinline__ void store_f32(float* p, int64_t e0, int cnt, const float (&x)[VEC]) {
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            if (v < cnt) p[e0 + v] = x[v];
+    } else {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            f32x4 t = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+            __builtin_nontemporal_store(t, reinterpret_cast<f32x4*>(p + e0) + q);
+        }
+    }
+}
+
+// A replica unit: binary32 copy, or nearest-even bfloat16 (VEC*2 bytes: 8 or 16).
+template <int VEC, bool TAIL>
+__device__ __forceinline__ void store_replica(void* r, int rdt, int64_t e0, int cnt,
+                                              const float (&x)[VEC]) {
+    if (rdt == kF32) {
+        store_f32<VEC, TAIL>(static_cast<float*>(r), e0, cnt, x);
+        return;
+    }
+    uint16_t* h = static_cast<uint16_t*>(r) + e0;
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            if (v < cnt) h[v] = static_cast<uint16_t>(f32_to_bf16_bits(x[v]));
+    } else if constexpr (VEC == 4) {
+        u32x2 t = {f32_to_bf16_bits(x[0]) | (f32_to_bf16_bits(x[1]) << 16),
+                   f32_to_bf16_bits(x[2]) | (f32_to_bf16_bits(x[3]) << 16)};
+        __builtin_nontemporal_store(t, reinterpret_cast<u32x2*>(h));
+    } else {
+        u32x4 t;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            t[q] = f32_to_bf16_bits(x[2 * q]) | (f32_to_bf16_bits(x[2 * q + 1]) << 16);
+        __builtin_nontemporal_store(t, reinterpret_cast<u32x4*>(h));
+    }
+}
+
+// ------------------------------------------------------------- pairwise sums
+
+// Compile-time pairwise tree over leaves LO .. LO+CNT-1: leaf(k, x) produces the
+// k-th term; the tree is PW with the largest-power-of-two split.
+template <int LO, int CNT, int VEC, typename Leaf>
+__device__ __forceinline__ void pw_tree(const Leaf& leaf, float (&out)[VEC]) {
+    if constexpr (CNT == 1) {
+        leaf(LO, out);
+    } else {
+        constexpr int H = pw_split(CNT);
+        float a[VEC], b[VEC];
+        pw_tree<LO, H, VEC>(leaf, a);
+        pw_tree<LO + H, CNT - H, VEC>(leaf, b);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) out[v] = a[v] + b[v];
+    }
+}
+
+// Runtime-count pairwise accumulator (a binary counter of partial sums). After
+// k pushes, slot[l] holds the sum of an aligned block of 2^l terms for every set
+// bit l of k; the largest block holds the earliest terms. result() folds the
+// blocks from the smallest up, each time adding the earlier (larger) block on
+// the left: exactly PW(x[0..k)) with the largest-power-of-two split.
+// Every slot is updated by a select, never by a conditional store, so that the
+// compiler cannot merge the per-level stores into one variable-index store
+// (which would move the slots to scratch memory). `levels` (uniform, <= LEVELS)
+// bounds the levels a push visits: pushes beyond 2^levels - 1 terms are not
+// supported.
+template <int VEC, int LEVELS = kAccLevels>
+struct PwAcc {
+    float slot[LEVELS][VEC];
+    uint32_t count = 0;
+
+    __device__ __forceinline__ void push(float (&x)[VEC], int levels = LEVELS) {
+        bool carrying = true;
+#pragma unroll
+        for (int l = 0; l < LEVELS; ++l) {
+            if (l < levels) {
+                const bool full = (count >> l) & 1u;
+                const bool merge = carrying && full;
+                const bool park = carrying && !full;
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    const float merged = slot[l][v] + x[v];
+                    slot[l][v] = park ? x[v] : slot[l][v];
+                    x[v] = merge ? merged : x[v];
+                }
+                carrying = merge;
+            }
+        }
+        ++count;
+    }
+
+    __device__ __forceinline__ void result(float (&out)[VEC], int levels = LEVELS) const {
+        bool have = false;
+#pragma unroll
+        for (int l = 0; l < LEVELS; ++l) {
+            if (l < levels && ((count >> l) & 1u)) {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) out[v] = have ? slot[l][v] + out[v] : slot[l][v];
+                have = true;
+            }
+        }
+    }
+};
+
+__host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
+
+// Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
+__device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
+
+// Runtime-count pairwise sum of `cnt` terms, loading up to 8 terms ahead so
+// that several 128-bit loads are in flight before they are folded in.
+template <int VEC, typename Load>
+__device__ __forceinline__ void pw_runtime(int cnt, const Load& load, float (&out)[VEC]) {
+    PwAcc<VEC> acc;
+    const int levels = acc_levels(cnt);
+    for (int k0 = 0; k0 < cnt; k0 += 8) {
+        float x[8][VEC];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (k0 + q < cnt) load(k0 + q, x[q]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (k0 + q < cnt) acc.push(x[q], levels);
+    }
+    acc.result(out, levels);
+}
+
+// ------------------------------------------------------------- the update
+
+struct Hyper {
+    float lr, mu, wd;
+};
+
+// Alg. 3 update with heavy-ball momentum and L2 weight decay, each operation
+// rounded separately: d = gbar + wd*p; m = mu*m + d; p = p - lr*m.
+template <int VEC>
+__device__ __forceinline__ void sgd_update(const Hyper& h, const float (&gbar)[VEC],
+                                           float (&p)[VEC], float (&m)[VEC]) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        float d = gbar[v] + h.wd * p[v];
+        m[v] = h.mu * m[v] + d;
+        p[v] = p[v] - h.lr * m[v];
+    }
+}
+
+// ------------------------------------------------------------- pointer sources
+
+// Kernel arguments of the planless calls. Pointer tables travel by value
+// (kernarg segment, read with scalar loads). grads[] is in member order:
+// entry j*W + k is the k-th member (ascending worker id) of group j.
+struct StepArgs {
+    float* p;
+    float* m;
+    const float* gbar;  // lsgd_sgd_step only
+    int64_t n;
+    Hyper h;
+    int32_t n_workers, n_groups, W;
+    int32_t n_replicas, rdt;
+    const void* grads[kMaxWorkers];
+    void* replicas[kMaxReplicas];
+};
+
+// Group-mean outputs of lsgd_group_mean / inputs of lsgd_global_mean.
+struct MeanArgs {
+    int64_t n;
+    int32_t n_workers, n_groups, W;
+    const void* in[kMaxWorkers];
+    float* out[kMaxWorkers];
+};
+
+// ------------------------------------------------------------- per-unit bodies
+
+// Widened gradient values one lane may hold at once before the compiler's load
+// hoisting starts to cost occupancy: 16 fp32 units or 8 bf16 units.
+constexpr int kUnrollFloats = 64;
+
+// Fused step on one unit, compile-time W and G (powers of two).
+// Small N: the whole two-level tree is unrolled and every load is issued up
+// front. Large N: groups are streamed GU at a time (GU*W units in flight per
+// lane) and folded into a pairwise accumulator over groups, which yields the
+// same PW order.
+template <typename GT, int W, int G, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    auto group_leaf = [&](int j, float (&gm)[VEC]) {
+        auto member_leaf = [&](int k, float (&x)[VEC]) {
+            load_grad<GT, TAIL>(s.grad(j * W + k), e0, cnt, x);
+        };
+        float sum[VEC];
+        pw_tree<0, W, VEC>(member_leaf, sum);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) gm[v] = sum[v] / static_cast<float>(W);
+    };
+    float tot[VEC], gbar[VEC];
+    if constexpr (W * G * VEC <= kUnrollFloats) {
+        pw_tree<0, G, VEC>(group_leaf, tot);
+    } else {
+        constexpr int GU0 = kUnrollFloats / (W * VEC);
+        constexpr int GU = GU0 < 1 ? 1 : (GU0 > G ? G : GU0);
+        PwAcc<VEC, ilog2(G) + 1> groups;
+#pragma unroll 1
+        for (int j0 = 0; j0 < G; j0 += GU) {
+            float gm[GU][VEC];
+#pragma unroll
+            for (int q = 0; q < GU; ++q) group_leaf(j0 + q, gm[q]);
+#pragma unroll
+            for (int q = 0; q < GU; ++q) groups.push(gm[q]);
+        }
+        groups.result(tot);
+    }
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) gbar[v] = tot[v] / static_cast<float>(G);
+
+    float p[VEC], m[VEC];
+    load_f32<VEC, TAIL>(s.p(), e0, cnt, p);
+    load_f32<VEC, TAIL>(s.m(), e0, cnt, m);
+    sgd_update<VEC>(s.hyper(), gbar, p, m);
+    store_f32<VEC, TAIL>(s.p(), e0, cnt, p);
+    store_f32<VEC, TAIL>(s.m(), e0, cnt, m);
+    const int R = s.n_replicas();
+    const int rdt = s.rdt();
+    for (int r = 0; r < R; ++r) store_replica<VEC, TAIL>(s.replica(r), rdt, e0, cnt, p);
+}
+
+// Fused step on one unit, runtime W and G (any equal-size grouping).
+template <typename GT, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_unit_rt(const Src& s, int W, int G, int64_t e0, int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const float wf = static_cast<float>(W), gf = static_cast<float>(G);
+    PwAcc<VEC> groups;
+    const int glevels = acc_levels(G);
+    for (int j = 0; j < G; ++j) {
+        float gm[VEC];
+        pw_runtime<VEC>(W, [&](int k, float (&x)[VEC]) {
+            load_grad<GT, TAIL>(s.grad(j * W + k), e0, cnt, x);
+        }, gm);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) gm[v] = gm[v] / wf;
+        groups.push(gm, glevels);
+    }
+    float gbar[VEC];
+    groups.result(gbar, glevels);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
+
+    float p[VEC], m[VEC];
+    load_f32<VEC, TAIL>(s.p(), e0, cnt, p);
+    load_f32<VEC, TAIL>(s.m(), e0, cnt, m);
+    sgd_update<VEC>(s.hyper(), gbar, p, m);
+    store_f32<VEC, TAIL>(s.p(), e0, cnt, p);
+    store_f32<VEC, TAIL>(s.m(), e0, cnt, m);
+    const int R = s.n_replicas();
+    const int rdt = s.rdt();
+    for (int r = 0; r < R; ++r) store_replica<VEC, TAIL>(s.replica(r), rdt, e0, cnt, p);
+}
+
+// Pointer source for the planless fused step: everything from StepArgs.
+struct FlatSrc {
+    const StepArgs& a;
+    __device__ const void* grad(int k) const { return a.grads[k]; }
+    __device__ float* p() const { return a.p; }
+    __device__ float* m() const { return a.m; }
+    __device__ void* replica(int r) const { return a.replicas[r]; }
+    __device__ int n_replicas() const { return a.n_replicas; }
+    __device__ int rdt() const { return a.rdt; }
+    __device__ Hyper hyper() const { return a.h; }
+};
+
+// ------------------------------------------------------------- flat kernels
+
+// Grid-stride loop over the full units of a flat vector; the ragged tail
+// (n % VEC elements) is handled by thread 0 of block 0 after its loop.
+template <typename GT, int W, int G>
+__global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const FlatSrc s{a};
+    const int64_t full = a.n / VEC;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
+        fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
+    const int rem = static_cast<int>(a.n - full * VEC);
+    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0)
+        fused_unit_ct<GT, W, G, true>(s, full * VEC, rem);
+}
+
+template <typename GT>
+__global__ __launch_bounds__(kBlock) void step_flat_rt(StepArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const FlatSrc s{a};
+    const int64_t full = a.n / VEC;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
+        fused_unit_rt<GT, false>(s, a.W, a.n_groups, u * VEC, VEC);
+    const int rem = static_cast<int>(a.n - full * VEC);
+    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0)
+        fused_unit_rt<GT, true>(s, a.W, a.n_groups, full * VEC, rem);
+}
+
+// lsgd_group_mean: every group's mean of its W members, for one unit.
+template <typename GT, bool TAIL>
+__device__ __forceinline__ void group_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const float wf = static_cast<float>(a.W);
+    for (int j = 0; j < a.n_groups; ++j) {
+        float gm[VEC];
+        pw_runtime<VEC>(a.W, [&](int k, float (&x)[VEC]) {
+            load_grad<GT, TAIL>(a.in[j * a.W + k], e0, cnt, x);
+        }, gm);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) gm[v] = gm[v] / wf;
+        store_f32<VEC, TAIL>(a.out[j], e0, cnt, gm);
+    }
+}
+
+template <typename GT>
+__global__ __launch_bounds__(kBlock) void group_mean_kernel(MeanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int64_t full = a.n / VEC;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
+        group_mean_unit<GT, false>(a, u * VEC, VEC);
+    const int rem = static_cast<int>(a.n - full * VEC);
+    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) group_mean_unit<GT, true>(a, full * VEC, rem);
+}
+
+// lsgd_global_mean: PW over the G group means, / G, for one 4-element unit.
+template <bool TAIL>
+__device__ __forceinline__ void global_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
+    float s[4];
+    pw_runtime<4>(a.n_groups, [&](int j, float (&x)[4]) {
+        load_f32<4, TAIL>(static_cast<const float*>(a.in[j]), e0, cnt, x);
+    }, s);
+    const float gf = static_cast<float>(a.n_groups);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) s[v] = s[v] / gf;
+    store_f32<4, TAIL>(a.out[0], e0, cnt, s);
+}
+
+static __global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) {
+    const int64_t full = a.n / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
+        global_mean_unit<false>(a, u * 4, 4);
+    const int rem = static_cast<int>(a.n - full * 4);
+    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) global_mean_unit<true>(a, full * 4, rem);
+}
+
+// lsgd_sgd_step: update and copy-out from a precomputed mean gradient.
+template <bool TAIL>
+__device__ __forceinline__ void sgd_unit(const StepArgs& a, int64_t e0, int cnt) {
+    float g[4], p[4], m[4];
+    load_f32<4, TAIL>(a.gbar, e0, cnt, g);
+    load_f32<4, TAIL>(a.p, e0, cnt, p);
+    load_f32<4, TAIL>(a.m, e0, cnt, m);
+    sgd_update<4>(a.h, g, p, m);
+    store_f32<4, TAIL>(a.p, e0, cnt, p);
+    store_f32<4, TAIL>(a.m, e0, cnt, m);
+    for (int r = 0; r < a.n_replicas; ++r) store_replica<4, TAIL>(a.replicas[r], a.rdt, e0, cnt, p);
+}
+
+static __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
+    const int64_t full = a.n / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
+        sgd_unit<false>(a, u * 4, 4);
+    const int rem = static_cast<int>(a.n - full * 4);
+    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) sgd_unit<true>(a, full * 4, rem);
+}
+
+// ------------------------------------------------------------- multi-tensor plan
+
+// One piece of one tensor: elements [start, start+len). Pieces start at
+// multiples of the unit size; only a tensor's last piece can end ragged.
+struct PlanChunk {
+    int32_t tensor;
+    int32_t pad_;
+    int64_t start;
+    int64_t len;
+};
+
+// Per tensor the device pointer table holds `stride` entries:
+// [p, m, grads in member order (N), replicas (R)].
+struct PlanArgs {
+    const PlanChunk* chunks;
+    const int32_t* bucket_begin;  // [n_buckets + 1]: workgroup b runs chunks [begin[b], begin[b+1])
+    void* const* ptrs;
+    int32_t stride, n_workers, n_groups, W;
+    int32_t n_replicas, rdt;
+    Hyper h;
+};
+
+struct PlanSrc {
+    void* const* t;  // this tensor's row of the pointer table
+    const PlanArgs& a;
+    __device__ const void* grad(int k) const { return t[2 + k]; }
+    __device__ float* p() const { return static_cast<float*>(t[0]); }
+    __device__ float* m() const { return static_cast<float*>(t[1]); }
+    __device__ void* replica(int r) const { return t[2 + a.n_workers + r]; }
+    __device__ int n_replicas() const { return a.n_replicas; }
+    __device__ int rdt() const { return a.rdt; }
+    __device__ Hyper hyper() const { return a.h; }
+};
+
+// One workgroup per bucket; a bucket is a run of chunks (one large piece, or
+// several small tensors). Chunk and pointer-table reads are uniform per
+// workgroup.
+template <typename GT, int W, int G>
+__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int32_t c_end = a.bucket_begin[blockIdx.x + 1];
+    for (int32_t c = a.bucket_begin[blockIdx.x]; c < c_end; ++c) {
+        const PlanChunk ch = a.chunks[c];
+        const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a};
+        const int64_t full = ch.len / VEC;
+        for (int64_t u = threadIdx.x; u < full; u += kBlock) {
+            if constexpr (W > 0) fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
+            else fused_unit_rt<GT, false>(s, a.W, a.n_groups, ch.start + u * VEC, VEC);
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            if constexpr (W > 0) fused_unit_ct<GT, W, G, true>(s, ch.start + full * VEC, rem);
+            else fused_unit_rt<GT, true>(s, a.W, a.n_groups, ch.start + full * VEC, rem);
+        }
+    }
+}
+
+}  // namespace lsgd

@@ -1,0 +1,210 @@
+// Multi-tensor plans of liblsgd: the fused step over a list of parameter
+// tensors (a model's per-layer tensors) in one kernel launch.
+//
+// lsgd_plan_create cuts every tensor into pieces of at most kPiece elements
+// (starting at multiples of the 16-byte unit), then packs consecutive pieces
+// into buckets of at most kPiece elements: a large tensor yields one bucket per
+// piece, while runs of small tensors (ResNet-50's 64..4096-element batch-norm
+// and bias vectors) share a bucket. One workgroup runs one bucket.
+#include <string.h>
+
+#include <algorithm>
+
+#include "lsgd_host.hpp"
+#include "lsgd_kernels.hpp"
+
+struct lsgd_plan {
+    int device;
+    int32_t n_tensors, n_workers, n_groups, W, n_replicas;
+    lsgd_dtype gdt, rdt;
+    int32_t n_buckets, n_chunks, stride;
+    lsgd::PlanChunk* d_chunks;
+    int32_t* d_bucket_begin;
+    void** d_ptrs;
+};
+
+namespace lsgd {
+namespace {
+
+// Elements per piece and per bucket: 8 units of 16 bytes per thread for
+// binary32 gradients.
+constexpr int64_t kPiece = 8192;
+constexpr int64_t kUnitAlign = 8;  // piece starts are multiples of 8 elements (16 B of bf16)
+
+using PlanKernel = void (*)(PlanArgs);
+
+template <typename GT, int W>
+PlanKernel pick_plan_g(int G) {
+    switch (G) {
+        case 1: return step_plan_kernel<GT, W, 1>;
+        case 2: return step_plan_kernel<GT, W, 2>;
+        case 4: return step_plan_kernel<GT, W, 4>;
+        case 8: return step_plan_kernel<GT, W, 8>;
+        case 16:
+            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16>;
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+template <typename GT>
+PlanKernel pick_plan(int W, int G) {
+    PlanKernel k = nullptr;
+    switch (W) {
+        case 1: k = pick_plan_g<GT, 1>(G); break;
+        case 2: k = pick_plan_g<GT, 2>(G); break;
+        case 4: k = pick_plan_g<GT, 4>(G); break;
+        case 8: k = pick_plan_g<GT, 8>(G); break;
+        case 16: k = pick_plan_g<GT, 16>(G); break;
+    }
+    return k ? k : step_plan_kernel<GT, 0, 0>;
+}
+
+void free_plan(lsgd_plan* p) {
+    if (!p) return;
+    if (p->d_chunks) (void)hipFree(p->d_chunks);
+    if (p->d_bucket_begin) (void)hipFree(p->d_bucket_begin);
+    if (p->d_ptrs) (void)hipFree(p->d_ptrs);
+    delete p;
+}
+
+}  // namespace
+}  // namespace lsgd
+
+using namespace lsgd;
+
+extern "C" {
+
+LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const int64_t* numel,
+                                      float* const* params, float* const* momentum,
+                                      const void* const* grads, lsgd_dtype gdt, int32_t n_workers,
+                                      const int32_t* group_of_worker, int32_t n_groups,
+                                      void* const* replicas, int32_t n_replicas, lsgd_dtype rdt) {
+    if (!out) return fail(LSGD_ERR_NULL, "out is NULL");
+    *out = nullptr;
+    if (n_tensors < 1) return fail(LSGD_ERR_SIZE, "n_tensors=%d < 1", n_tensors);
+    if (!numel) return fail(LSGD_ERR_NULL, "numel is NULL");
+    std::vector<int32_t> order;
+    lsgd_status st = member_order(n_workers, group_of_worker, n_groups, order);
+    if (st != LSGD_OK) return st;
+    if (gdt != LSGD_F32 && gdt != LSGD_BF16) return fail(LSGD_ERR_DTYPE, "gradient dtype %d", (int)gdt);
+    if (rdt != LSGD_F32 && rdt != LSGD_BF16) return fail(LSGD_ERR_DTYPE, "replica dtype %d", (int)rdt);
+    if (n_replicas < 0 || n_replicas > kMaxReplicas)
+        return fail(LSGD_ERR_SIZE, "n_replicas=%d outside [0, %d]", n_replicas, kMaxReplicas);
+    if (!params || !momentum || !grads) return fail(LSGD_ERR_NULL, "params, momentum or grads is NULL");
+    if (n_replicas > 0 && !replicas) return fail(LSGD_ERR_NULL, "replicas is NULL with n_replicas=%d", n_replicas);
+
+    const size_t gsz = gdt == LSGD_BF16 ? 2 : 4, rsz = rdt == LSGD_BF16 ? 2 : 4;
+    const int32_t stride = 2 + n_workers + n_replicas;
+    std::vector<void*> table(static_cast<size_t>(n_tensors) * stride, nullptr);
+    std::vector<Range> ranges;
+    std::vector<PlanChunk> chunks;
+    std::vector<int32_t> bucket_begin;
+    int64_t bucket_fill = kPiece;  // forces a new bucket at the first piece
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        const int64_t ne = numel[t];
+        if (ne < 0) return fail(LSGD_ERR_SIZE, "numel[%d]=%lld < 0", t, static_cast<long long>(ne));
+        if (ne == 0) continue;
+        void** row = &table[static_cast<size_t>(t) * stride];
+        auto add = [&](void* p, size_t esz, bool written, const char* what, int idx) -> lsgd_status {
+            if (!p) return fail(LSGD_ERR_NULL, "%s[%d] of tensor %d is NULL", what, idx, t);
+            if (!aligned16(p)) return fail(LSGD_ERR_ALIGN, "%s[%d] of tensor %d is not 16-byte aligned", what, idx, t);
+            const uintptr_t b = reinterpret_cast<uintptr_t>(p);
+            ranges.push_back(Range{b, b + static_cast<uintptr_t>(ne) * esz, written, what});
+            return LSGD_OK;
+        };
+        if ((st = add(params[t], 4, true, "params", t)) != LSGD_OK) return st;
+        if ((st = add(momentum[t], 4, true, "momentum", t)) != LSGD_OK) return st;
+        row[0] = params[t];
+        row[1] = momentum[t];
+        for (int32_t k = 0; k < n_workers; ++k) {
+            const int32_t w = order[k];
+            void* g = const_cast<void*>(grads[static_cast<size_t>(w) * n_tensors + t]);
+            if ((st = add(g, gsz, false, "grads", w)) != LSGD_OK) return st;
+            row[2 + k] = g;
+        }
+        for (int32_t r = 0; r < n_replicas; ++r) {
+            void* rp = replicas[static_cast<size_t>(r) * n_tensors + t];
+            if ((st = add(rp, rsz, true, "replicas", r)) != LSGD_OK) return st;
+            row[2 + n_workers + r] = rp;
+        }
+        for (int64_t s0 = 0; s0 < ne; s0 += kPiece) {
+            const int64_t len = std::min(kPiece, ne - s0);
+            if (bucket_fill + len > kPiece) {
+                bucket_begin.push_back(static_cast<int32_t>(chunks.size()));
+                bucket_fill = 0;
+            }
+            // every piece but a tensor's last has len == kPiece (a multiple of kUnitAlign)
+            static_assert(kPiece % kUnitAlign == 0, "pieces must start on unit boundaries");
+            chunks.push_back(PlanChunk{t, 0, s0, len});
+            bucket_fill += len;
+        }
+    }
+    if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+    if (chunks.size() > 0x7fffffff) return fail(LSGD_ERR_SIZE, "too many pieces");
+    bucket_begin.push_back(static_cast<int32_t>(chunks.size()));
+
+    lsgd_plan* p = new lsgd_plan;
+    memset(p, 0, sizeof *p);
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return fail(LSGD_ERR_HIP, "hipGetDevice failed");
+    }
+    p->n_tensors = n_tensors;
+    p->n_workers = n_workers;
+    p->n_groups = n_groups;
+    p->W = n_workers / n_groups;
+    p->n_replicas = n_replicas;
+    p->gdt = gdt;
+    p->rdt = rdt;
+    p->n_chunks = static_cast<int32_t>(chunks.size());
+    p->n_buckets = static_cast<int32_t>(bucket_begin.size()) - 1;
+    p->stride = stride;
+    hipError_t e = hipSuccess;
+    const size_t chunk_bytes = std::max<size_t>(1, chunks.size()) * sizeof(PlanChunk);
+    const size_t bucket_bytes = bucket_begin.size() * sizeof(int32_t);
+    const size_t table_bytes = table.size() * sizeof(void*);
+    if (e == hipSuccess) e = hipMalloc(&p->d_chunks, chunk_bytes);
+    if (e == hipSuccess) e = hipMalloc(&p->d_bucket_begin, bucket_bytes);
+    if (e == hipSuccess) e = hipMalloc(&p->d_ptrs, table_bytes);
+    if (e == hipSuccess && !chunks.empty())
+        e = hipMemcpy(p->d_chunks, chunks.data(), chunks.size() * sizeof(PlanChunk), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_bucket_begin, bucket_begin.data(), bucket_bytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(p->d_ptrs, table.data(), table_bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        free_plan(p);
+        return fail(LSGD_ERR_HIP, "lsgd_plan_create: %s", hipGetErrorString(e));
+    }
+    *out = p;
+    return LSGD_OK;
+}
+
+LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
+                                    float weight_decay, void* stream) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    if (plan->n_buckets == 0) return LSGD_OK;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+        return fail(LSGD_ERR_HIP, "plan was created on device %d, current device is %d", plan->device, dev);
+    PlanArgs a;
+    memset(&a, 0, sizeof a);
+    a.chunks = plan->d_chunks;
+    a.bucket_begin = plan->d_bucket_begin;
+    a.ptrs = plan->d_ptrs;
+    a.stride = plan->stride;
+    a.n_workers = plan->n_workers;
+    a.n_groups = plan->n_groups;
+    a.W = plan->W;
+    a.n_replicas = plan->n_replicas;
+    a.rdt = static_cast<int32_t>(plan->rdt);
+    a.h = Hyper{lr, momentum_coef, weight_decay};
+    PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups)
+                                          : pick_plan<float>(plan->W, plan->n_groups);
+    hipLaunchKernelGGL(k, dim3(plan->n_buckets), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_step_plan");
+}
+
+LSGD_API void lsgd_plan_destroy(lsgd_plan* plan) { free_plan(plan); }
+
+}  // extern "C"

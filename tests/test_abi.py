@@ -1,0 +1,197 @@
+"""The C ABI of liblsgd.so without a GPU: the library loads, exports every entry
+point include/lsgd.h declares, and rejects invalid arguments with the
+documented status before anything is launched (every call here fails
+validation, so no HIP work is ever enqueued).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lsgd.h")
+
+import torch
+
+# These tests hand the library fake device addresses that must never be
+# dereferenced. Each case fails validation before any launch; as a second
+# line of defence the module only runs where no GPU is visible (counting
+# devices does not initialise one).
+pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                                reason="fake-pointer validation tests run only without a GPU")
+
+L = pytest.importorskip("paper_1906_05936_amd._lib")
+lib = L.lib
+pa, i32a, i64a = L.ptr_array, L.int32_array, L.int64_array
+
+OK, NULL, SIZE, GROUPS, ALIGN, DTYPE, HIP, ALIAS = range(8)
+A = 1 << 20   # fake, 16-byte aligned "device" addresses: never dereferenced
+MB = 1 << 20
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"LSGD_API\s+[\w\s\*]+?\b(lsgd_\w+)\s*\(", text)
+
+
+def test_header_declares_the_boundary():
+    names = set(declared_functions())
+    assert {"lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
+            "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
+            "lsgd_status_string", "lsgd_last_error"} == names
+    assert set(L.EXPORTS) == names
+
+
+def test_library_exports_every_declared_symbol():
+    raw = ctypes.CDLL(L.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(raw, name), name
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define LSGD_MAX_WORKERS (\d+)", text).group(1)) == L.MAX_WORKERS
+    assert int(re.search(r"#define LSGD_MAX_REPLICAS (\d+)", text).group(1)) == L.MAX_REPLICAS
+    for code, name in L.STATUS_NAMES.items():
+        assert re.search(r"%s = %d" % (name, code), text), name
+
+
+def test_status_strings():
+    for code, name in L.STATUS_NAMES.items():
+        assert lib.lsgd_status_string(code).decode().startswith(name)
+    assert lib.lsgd_status_string(99) is not None
+
+
+def step(params=A, mom=A + 100 * MB, grads=None, gdt=0, gow=(0, 0, 1, 1), G=2, n=1000,
+         replicas=None, R=0, rdt=0):
+    if grads is None:
+        grads = [A + (k + 2) * 100 * MB for k in range(len(gow))]
+    return lib.lsgd_step(params, mom, pa(grads) if grads != "null" else None, gdt, len(gow),
+                         i32a(gow), G, n, 0.1, 0.9, 1e-4,
+                         pa(replicas) if replicas is not None else None, R, rdt, None)
+
+
+def last():
+    return lib.lsgd_last_error().decode()
+
+
+def test_step_validation_errors():
+    assert step(n=-1) == SIZE
+    assert step(gow=(0, 0, 1), G=2) == GROUPS and "divide" in last()
+    assert step(gow=(0, 0, 0, 1), G=2) == GROUPS
+    assert step(gow=(0, 1, 2, 2), G=2) == GROUPS
+    assert step(gow=(0, -1, 1, 1), G=2) == GROUPS
+    assert step(G=0) == SIZE
+    assert step(gow=tuple(range(129)), G=129) == SIZE          # more than LSGD_MAX_WORKERS
+    assert step(gow=()) == SIZE
+    assert step(grads="null") == NULL
+    assert step(grads=[A, 0, A, A]) == NULL
+    assert step(params=0) == NULL
+    assert step(mom=0) == NULL
+    assert step(gdt=7) == DTYPE
+    assert step(rdt=3, R=1, replicas=[A + 900 * MB]) == DTYPE
+    assert step(R=-1) == SIZE
+    assert step(R=129, replicas=[A] * 129) == SIZE
+    assert step(R=2, replicas=None) == NULL
+    assert step(R=2, replicas=[A + 900 * MB, 0]) == NULL
+    assert step(params=A + 4) == ALIGN
+    assert step(grads=[A + 200 * MB, A + 300 * MB + 8, A, A]) == ALIGN
+    assert step(R=1, replicas=[A + 900 * MB + 2]) == ALIGN
+
+
+def test_step_aliasing_errors():
+    # a replica overlapping the parameters, the momentum overlapping a gradient
+    assert step(R=1, replicas=[A + 16]) == ALIAS
+    assert step(mom=A + 200 * MB + 64) == ALIAS
+    assert step(params=A, mom=A) == ALIAS
+    assert step(R=2, replicas=[A + 900 * MB, A + 900 * MB]) == ALIAS
+
+
+def test_n_zero_is_a_validated_noop():
+    assert step(n=0, params=0, mom=0, grads=[0, 0, 0, 0]) == OK
+    assert step(n=0, gow=(0, 0, 0, 1)) == GROUPS          # membership still validated
+    assert step(n=0, gdt=9) == DTYPE
+
+
+def test_group_mean_validation():
+    gr = [A + k * 100 * MB for k in range(4)]
+    outs = [A + 500 * MB, A + 600 * MB]
+    f = lambda grads=gr, gow=(0, 1, 0, 1), G=2, n=100, out=outs, gdt=0: lib.lsgd_group_mean(
+        pa(grads), gdt, len(gow), i32a(gow), G, n, pa(out) if out is not None else None, None)
+    assert f(n=-5) == SIZE
+    assert f(gow=(0, 1, 1, 1)) == GROUPS
+    assert f(out=None) == NULL
+    assert f(out=[A + 500 * MB, 0]) == NULL
+    assert f(out=[A + 500 * MB + 4, A + 600 * MB]) == ALIGN
+    assert f(out=[A + 128, A + 600 * MB]) == ALIAS            # output inside grads[0]
+    assert f(gdt=2) == DTYPE
+    assert f(n=0, out=None) == OK
+
+
+def test_global_mean_validation():
+    ins = [A, A + 100 * MB]
+    f = lambda ins=ins, G=2, n=100, out=A + 500 * MB: lib.lsgd_global_mean(
+        pa(ins), G, n, out, None)
+    assert f(G=0) == SIZE
+    assert f(G=200, ins=[A] * 200) == SIZE
+    assert f(n=-1) == SIZE
+    assert f(out=0) == NULL
+    assert f(out=A + 500 * MB + 8) == ALIGN
+    assert f(ins=[A, 0]) == NULL
+    assert f(out=A + 100 * MB) == ALIAS
+    assert f(n=0, out=0) == OK
+
+
+def test_sgd_step_validation():
+    f = lambda p=A, m=A + 100 * MB, g=A + 200 * MB, n=100, reps=None, R=0, rdt=0: lib.lsgd_sgd_step(
+        p, m, g, n, 0.1, 0.9, 1e-4, pa(reps) if reps is not None else None, R, rdt, None)
+    assert f(n=-1) == SIZE
+    assert f(p=0) == NULL
+    assert f(g=0) == NULL
+    assert f(g=A + 200 * MB + 4) == ALIGN
+    assert f(m=A) == ALIAS
+    assert f(g=A + 192) == ALIAS
+    assert f(reps=[A + 300 * MB], R=1, rdt=5) == DTYPE
+    assert f(reps=[A + 100 * MB + 16], R=1) == ALIAS
+    assert f(n=0, p=0, m=0, g=0) == OK
+
+
+def plan_create(numel=(100, 64), G=2, gow=(0, 0, 1, 1), R=0, gdt=0, rdt=0, params=None,
+                mom=None, grads=None, replicas=None):
+    T = len(numel)
+    params = params if params is not None else [A + t * MB for t in range(T)]
+    mom = mom if mom is not None else [A + (100 + t) * MB for t in range(T)]
+    grads = grads if grads is not None else [A + (200 + k) * MB for k in range(T * len(gow))]
+    handle = ctypes.c_void_p()
+    st = lib.lsgd_plan_create(ctypes.byref(handle), T, i64a(numel), pa(params), pa(mom),
+                              pa(grads), gdt, len(gow), i32a(gow), G,
+                              pa(replicas) if replicas is not None else None, R, rdt)
+    assert handle.value is None   # nothing is created on failure
+    return st
+
+
+def test_plan_validation_errors():
+    assert plan_create(numel=()) == SIZE
+    assert plan_create(numel=(100, -1)) == SIZE
+    assert plan_create(gow=(0, 0, 0, 1)) == GROUPS
+    assert plan_create(gdt=4) == DTYPE
+    assert plan_create(R=1, replicas=None) == NULL
+    assert plan_create(R=200, replicas=[A] * 400) == SIZE
+    assert plan_create(params=[A, 0]) == NULL
+    assert plan_create(params=[A, A + 8]) == ALIGN
+    assert plan_create(mom=[A + 100 * MB, A + 16]) == ALIAS          # momentum[1] inside params[0]
+    assert plan_create(R=1, replicas=[A + 900 * MB, A + 900 * MB]) == ALIAS
+    h = ctypes.c_void_p()
+    assert lib.lsgd_plan_create(None, 1, i64a([1]), pa([A]), pa([A]), pa([A]), 0, 1, i32a([0]), 1,
+                                None, 0, 0) == NULL
+    assert lib.lsgd_step_plan(None, 0.1, 0.9, 1e-4, None) == NULL
+    lib.lsgd_plan_destroy(None)   # NULL-safe
+    del h
+
+
+def test_package_fails_loudly_without_library(tmp_path, monkeypatch):
+    """The binding raises when liblsgd.so is absent: there is no fallback path."""
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        L._load()

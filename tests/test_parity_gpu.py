@@ -1,0 +1,393 @@
+"""GPU parity: liblsgd (HIP, through its C ABI) against the CPU oracle on the
+same seeded inputs.
+
+Bar: parameters, momentum, group means and mean gradient bit-exact (the kernels
+and the oracle use the same pairwise order and the same binary32 operations);
+the contract tolerance |gpu - ref| <= 1e-6*|ref| + 1e-6*rms(ref) is asserted
+as well. Replicas and all indexing are bit-exact.
+
+Sizes: small shapes that span several workgroups and end ragged (compared
+element by element), and the five workloads at full size in the launch
+configuration the benchmark times (sampled elements, which the oracle computes
+one by one; every element is independent of the others).
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.device_count() > 0:
+    import paper_1906_05936_amd as lsgd
+else:  # collected but skipped on machines without a GPU
+    lsgd = None
+
+DEV = torch.device("cuda:0")
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+# ---------------------------------------------------------------- helpers
+
+def to_dev(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def to_host(t):
+    t = t.detach()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def rand_host(rng, n, std, dtype):
+    x = (rng.standard_normal(n) * std).astype(np.float32)
+    return oracle.f32_to_bf16(x) if dtype == "bf16" else x
+
+
+def assert_close(gpu, ref, what):
+    """Bitwise equality, and the contract tolerance for binary32 results."""
+    assert gpu.shape == ref.shape, what
+    if gpu.dtype == np.float32:
+        nan = np.isnan(ref)
+        assert np.array_equal(np.isnan(gpu), nan), what
+        fin = np.isfinite(ref)
+        assert np.array_equal(gpu[~fin & ~nan], ref[~fin & ~nan]), what   # infinities
+        rms = float(np.sqrt(np.mean(ref[fin].astype(np.float64) ** 2))) if fin.any() else 0.0
+        err = np.abs(gpu[fin].astype(np.float64) - ref[fin])
+        tol = 1e-6 * np.abs(ref[fin]) + 1e-6 * rms
+        assert np.all(err <= tol), "%s: max err %g" % (what, err.max() if err.size else 0)
+        mism = np.count_nonzero(gpu[~nan].view(np.uint32) != ref[~nan].view(np.uint32))
+        assert mism == 0, "%s: %d of %d elements differ in bits" % (what, mism, ref.size)
+    else:
+        assert np.array_equal(gpu, ref), what
+
+
+def groups_for(G, W, layout, seed=0):
+    if layout == "contiguous":
+        return workloads.contiguous_groups(G, W)
+    return workloads.shuffled_groups(G, W, seed)
+
+
+# ---------------------------------------------------------------- flat fused step
+
+STEP_CASES = [
+    # G, W, gdt, n, R, rdt, layout
+    (2, 2, "f32", 1_000_003, 4, "f32", "shuffled"),
+    (4, 4, "f32", 65_541, 16, "f32", "contiguous"),
+    (4, 4, "f32", 3, 1, "f32", "contiguous"),
+    (16, 8, "f32", 20_001, 128, "f32", "shuffled"),
+    (8, 8, "bf16", 40_007, 64, "bf16", "shuffled"),
+    (8, 8, "bf16", 7, 2, "f32", "contiguous"),
+    (2, 16, "bf16", 33_333, 3, "bf16", "shuffled"),
+    (16, 4, "f32", 12_345, 0, "f32", "shuffled"),
+    (1, 16, "f32", 12_289, 0, "f32", "contiguous"),
+    (16, 1, "f32", 4_099, 1, "bf16", "contiguous"),
+    (1, 1, "f32", 1, 1, "f32", "contiguous"),
+    (3, 5, "f32", 10_007, 2, "bf16", "shuffled"),
+    (5, 3, "bf16", 9_999, 0, "f32", "shuffled"),
+    (7, 1, "f32", 5_000, 1, "f32", "contiguous"),
+    (1, 100, "f32", 777, 0, "f32", "contiguous"),
+    (128, 1, "bf16", 513, 1, "f32", "shuffled"),
+    (6, 7, "bf16", 2_050, 42, "bf16", "shuffled"),
+]
+
+
+@pytest.mark.parametrize("G,W,gdt,n,R,rdt,layout", STEP_CASES)
+def test_fused_step_matches_oracle(G, W, gdt, n, R, rdt, layout):
+    log("case G=%d W=%d gdt=%s n=%d R=%d rdt=%s %s" % (G, W, gdt, n, R, rdt, layout))
+    rng = np.random.default_rng(G * 7919 + W * 31 + n)
+    N = G * W
+    gow = groups_for(G, W, layout, seed=n)
+    p_ref = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m_ref = np.zeros(n, np.float32)
+    p, m = to_dev(p_ref), to_dev(m_ref)
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    reps = [torch.full((n,), float("nan"), device=DEV, dtype=rtd) for _ in range(R)]
+    for step in range(3):
+        host_grads = [rand_host(rng, n, 1e-2, gdt) for _ in range(N)]
+        grads = [to_dev(g) for g in host_grads]
+        lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
+        ref_reps = [np.zeros(n, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+        oracle.lsgd_step(p_ref, m_ref, host_grads, gow, G, 0.1, 0.9, 1e-4, ref_reps,
+                         oracle.BF16 if rdt == "bf16" else oracle.F32)
+        torch.cuda.synchronize()
+        assert_close(to_host(p), p_ref, "params step %d" % step)
+        assert_close(to_host(m), m_ref, "momentum step %d" % step)
+        for r in range(R):
+            assert np.array_equal(to_host(reps[r]), ref_reps[r]), "replica %d step %d" % (r, step)
+
+
+def test_fused_step_empty_and_errors():
+    p = torch.zeros(0, device=DEV)
+    lsgd.step(p, torch.zeros(0, device=DEV), [torch.zeros(0, device=DEV)] * 2, [0, 1], 2, 0.1, 0.9, 0.0)
+    base = torch.zeros(1025, device=DEV)
+    p, m = base[1:], torch.zeros(1024, device=DEV)          # p is 4 bytes off 16-byte alignment
+    g = [torch.zeros(1024, device=DEV) for _ in range(2)]
+    with pytest.raises(lsgd.LsgdError) as e:
+        lsgd.step(p, m, g, [0, 1], 2, 0.1, 0.9, 0.0)
+    assert e.value.name == "LSGD_ERR_ALIGN"
+    with pytest.raises(lsgd.LsgdError) as e:
+        lsgd.step(m, m, g, [0, 1], 2, 0.1, 0.9, 0.0)
+    assert e.value.name == "LSGD_ERR_ALIAS"
+    with pytest.raises(TypeError):
+        lsgd.step(m.clone(), m, [g[0], g[1].bfloat16()], [0, 1], 2, 0.1, 0.9, 0.0)
+
+
+def test_non_finite_values_propagate_like_the_oracle():
+    n = 1024
+    g = np.full(n, 1e-3, np.float32)
+    g[:6] = [np.nan, np.inf, -np.inf, 3e38, -3e38, 1e-45]
+    grads_h = [g, g.copy(), g[::-1].copy(), g.copy()]
+    p_ref = np.ones(n, np.float32)
+    m_ref = np.zeros(n, np.float32)
+    p, m = to_dev(p_ref), to_dev(m_ref)
+    lsgd.step(p, m, [to_dev(x) for x in grads_h], [0, 0, 1, 1], 2, 0.1, 0.9, 1e-4)
+    oracle.lsgd_step(p_ref, m_ref, grads_h, [0, 0, 1, 1], 2, 0.1, 0.9, 1e-4)
+    assert_close(to_host(p), p_ref, "params")
+    assert_close(to_host(m), m_ref, "momentum")
+
+
+def test_fixed_point_on_gpu():
+    """Identical worker gradients: the mean is the gradient itself, bitwise."""
+    for G, W, gdt in [(4, 4, "f32"), (8, 8, "bf16"), (16, 8, "f32")]:
+        rng = np.random.default_rng(G + W)
+        gh = rand_host(rng, 50_003, 1e-2, gdt)
+        g = to_dev(gh)
+        outs = [torch.empty(50_003, device=DEV) for _ in range(G)]
+        lsgd.group_mean([g] * (G * W), workloads.contiguous_groups(G, W), G, outs)
+        gbar = torch.empty(50_003, device=DEV)
+        lsgd.global_mean(outs, gbar)
+        want = oracle.bf16_to_f32(gh) if gdt == "bf16" else gh
+        assert to_host(gbar).tobytes() == want.tobytes()
+
+
+# ---------------------------------------------------------------- unfused calls
+
+@pytest.mark.parametrize("G,W,gdt,n,R,rdt", [(4, 4, "f32", 100_003, 2, "f32"),
+                                             (8, 8, "bf16", 20_001, 1, "bf16"),
+                                             (3, 5, "f32", 7_777, 0, "f32"),
+                                             (1, 1, "bf16", 5, 1, "f32")])
+def test_unfused_calls_match_oracle_and_fused(G, W, gdt, n, R, rdt):
+    log("unfused G=%d W=%d %s n=%d" % (G, W, gdt, n))
+    rng = np.random.default_rng(n)
+    N = G * W
+    gow = groups_for(G, W, "shuffled", seed=3)
+    gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(N)]
+    grads = [to_dev(x) for x in gh]
+    gm = [torch.empty(n, device=DEV) for _ in range(G)]
+    lsgd.group_mean(grads, gow, G, gm)
+    gm_ref = oracle.group_means(gh, gow, G)
+    for j in range(G):
+        assert_close(to_host(gm[j]), gm_ref[j], "group mean %d" % j)
+    gbar = torch.empty(n, device=DEV)
+    lsgd.global_mean(gm, gbar)
+    gbar_ref = oracle.global_mean(gm_ref)
+    assert_close(to_host(gbar), gbar_ref, "mean gradient")
+
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 0.01).astype(np.float32)
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    p, m = to_dev(p0), to_dev(m0)
+    reps = [torch.empty(n, device=DEV, dtype=rtd) for _ in range(R)]
+    lsgd.sgd_step(p, m, gbar, 0.1, 0.9, 1e-4, reps)
+    p_ref, m_ref = p0.copy(), m0.copy()
+    ref_reps = [np.zeros(n, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+    oracle.sgd_step(p_ref, m_ref, gbar_ref, 0.1, 0.9, 1e-4, ref_reps,
+                    oracle.BF16 if rdt == "bf16" else oracle.F32)
+    assert_close(to_host(p), p_ref, "params")
+    assert_close(to_host(m), m_ref, "momentum")
+    for r in range(R):
+        assert np.array_equal(to_host(reps[r]), ref_reps[r])
+
+    pf, mf = to_dev(p0), to_dev(m0)
+    lsgd.step(pf, mf, grads, gow, G, 0.1, 0.9, 1e-4)
+    assert torch.equal(pf, p) and torch.equal(mf, m)   # fused == unfused, bitwise
+
+
+# ---------------------------------------------------------------- multi-tensor plans
+
+PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_385]
+
+
+@pytest.mark.parametrize("G,W,gdt,R,rdt", [(4, 4, "f32", 16, "f32"), (2, 2, "f32", 0, "f32"),
+                                           (8, 8, "bf16", 3, "bf16"), (3, 5, "f32", 1, "bf16"),
+                                           (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32")])
+def test_plan_matches_oracle(G, W, gdt, R, rdt):
+    log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
+    rng = np.random.default_rng(G * 100 + W)
+    N = G * W
+    gow = groups_for(G, W, "shuffled", seed=G)
+    T = len(PLAN_SIZES)
+    ph = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in PLAN_SIZES]
+    mh = [np.zeros(s, np.float32) for s in PLAN_SIZES]
+    params = [to_dev(x) for x in ph]
+    mom = [to_dev(x) for x in mh]
+    gh = [[rand_host(rng, s, 1e-2, gdt) for s in PLAN_SIZES] for _ in range(N)]
+    grads = [[to_dev(x) for x in row] for row in gh]
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    reps = [[torch.empty(s, device=DEV, dtype=rtd) for s in PLAN_SIZES] for _ in range(R)]
+    plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+    for step in range(2):
+        if step:
+            gh = [[rand_host(rng, s, 1e-2, gdt) for s in PLAN_SIZES] for _ in range(N)]
+            for w in range(N):
+                for t in range(T):
+                    grads[w][t].copy_(to_dev(gh[w][t]))
+        plan.step(0.1, 0.9, 1e-4)
+        torch.cuda.synchronize()
+        for t in range(T):
+            rr = [np.zeros(PLAN_SIZES[t], np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+            oracle.lsgd_step(ph[t], mh[t], [gh[w][t] for w in range(N)], gow, G, 0.1, 0.9, 1e-4, rr,
+                             oracle.BF16 if rdt == "bf16" else oracle.F32)
+            assert_close(to_host(params[t]), ph[t], "params[%d] step %d" % (t, step))
+            assert_close(to_host(mom[t]), mh[t], "momentum[%d] step %d" % (t, step))
+            for r in range(R):
+                assert np.array_equal(to_host(reps[r][t]), rr[r]), (t, r)
+    plan.close()
+
+
+def test_plan_equals_flat_bitwise():
+    """Different launch shapes (plan buckets vs grid-stride flat kernel) give the
+    same bits: every element's result depends only on its own inputs."""
+    sizes = workloads.resnet50_param_sizes()[:40]
+    n = sum(sizes)
+    G, W = 4, 4
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(5)
+    flat_p = torch.randn(n, device=DEV, generator=gen) * 0.05
+    flat_g = [torch.randn(n, device=DEV, generator=gen) * 1e-2 for _ in range(G * W)]
+    params = workloads.split_tensors(flat_p, sizes)
+    mom = [torch.zeros_like(x) for x in params]
+    grads = [workloads.split_tensors(g, sizes) for g in flat_g]
+    flat_m = torch.zeros(n, device=DEV)
+    gow = workloads.contiguous_groups(G, W)
+    plan = lsgd.Plan(params, mom, grads, gow, G)
+    for _ in range(3):
+        plan.step(0.1, 0.9, 1e-4)
+        lsgd.step(flat_p, flat_m, flat_g, gow, G, 0.1, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat(params), flat_p) and torch.equal(torch.cat(mom), flat_m)
+    plan.close()
+
+
+def test_repeat_runs_are_bit_identical():
+    rng = np.random.default_rng(0)
+    n = 300_007
+    gh = [rand_host(rng, n, 1e-2, "f32") for _ in range(16)]
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    outs = []
+    for _ in range(2):
+        p, m = to_dev(p0), torch.zeros(n, device=DEV)
+        for _ in range(4):
+            lsgd.step(p, m, [to_dev(x) for x in gh], workloads.contiguous_groups(4, 4), 4, 0.1, 0.9, 1e-4)
+        outs.append((to_host(p), to_host(m)))
+    assert outs[0][0].tobytes() == outs[1][0].tobytes()
+    assert outs[0][1].tobytes() == outs[1][1].tobytes()
+
+
+def test_bf16_gradients_within_2e3_of_fp32_gradients():
+    """bf16 gradient storage against fp32 storage of the same fp32 draws: the
+    mean gradient agrees within 2e-3 normwise (64 workers, std 1e-3)."""
+    n, G, W = 1_000_000, 8, 8
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(77)
+    g32 = [torch.randn(n, device=DEV, generator=gen) * 1e-3 for _ in range(G * W)]
+    g16 = [g.bfloat16() for g in g32]
+    gow = workloads.contiguous_groups(G, W)
+    res = []
+    for gl in (g32, g16):
+        gm = [torch.empty(n, device=DEV) for _ in range(G)]
+        lsgd.group_mean(gl, gow, G, gm)
+        out = torch.empty(n, device=DEV)
+        lsgd.global_mean(gm, out)
+        res.append(out.double())
+    rel = (torch.linalg.vector_norm(res[1] - res[0]) / torch.linalg.vector_norm(res[0])).item()
+    log("bf16 vs fp32 gradient storage: normwise relative difference %.3e" % rel)
+    assert rel <= 2e-3
+
+
+# ---------------------------------------------------------------- full-size workloads
+
+@pytest.mark.parametrize("name", workloads.ORDER)
+def test_workload_full_size_sampled(name):
+    """Each workload at its full size and step count, R = N replicas, in the
+    benchmark's launch configuration. Inputs are regenerated every step; the
+    oracle follows the sampled elements (all of them for the tiny workload)."""
+    wl = workloads.WORKLOADS[name]
+    N, G, W = wl.n_workers, wl.groups, wl.workers_per_group
+    log("workload %s: n=%d G=%d W=%d %s steps=%d" % (name, wl.n, G, W, wl.grad_dtype, wl.steps))
+    gow = workloads.contiguous_groups(G, W)
+    rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
+    R = N
+    flat_p = workloads.init_params(wl, DEV)
+    if wl.tensor_sizes:
+        params = workloads.split_tensors(flat_p, wl.tensor_sizes)
+        del flat_p
+        mom = [torch.zeros_like(x) for x in params]
+        grads = [[torch.empty(s, device=DEV, dtype=wl.torch_grad_dtype) for s in wl.tensor_sizes]
+                 for _ in range(N)]
+        reps = [[torch.empty(s, device=DEV, dtype=rtd) for s in wl.tensor_sizes] for _ in range(R)]
+        plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+        offs = np.cumsum([0] + list(wl.tensor_sizes))
+    else:
+        params, mom = [flat_p], [torch.zeros_like(flat_p)]
+        grads = [[torch.empty(wl.n, device=DEV, dtype=wl.torch_grad_dtype)] for _ in range(N)]
+        reps = [[torch.empty(wl.n, device=DEV, dtype=rtd)] for _ in range(R)]
+        plan = None
+        offs = np.array([0, wl.n])
+    full = wl.n <= 1_000_000
+    idx = np.arange(wl.n) if full else workloads.sample_indices(wl.n, 4096, wl.seed)
+    if wl.tensor_sizes:   # also each tensor's first and last element
+        idx = np.unique(np.concatenate([idx, offs[:-1], offs[1:] - 1]))
+    # (tensor, local index) of every sampled element
+    tid = np.searchsorted(offs, idx, side="right") - 1
+    loc = idx - offs[tid]
+    sel = [(t, torch.from_numpy(loc[tid == t]).to(DEV)) for t in np.unique(tid)]
+
+    def gather(tensors):
+        return to_host(torch.cat([tensors[t].index_select(0, li) for t, li in sel]))
+
+    p_ref = gather(params)
+    m_ref = gather(mom)
+    scratch = torch.empty(max(wl.tensor_sizes or (wl.n,)), device=DEV) if wl.grad_dtype == "bf16" else None
+    flat_tmp = torch.empty(wl.n, device=DEV, dtype=wl.torch_grad_dtype) if wl.tensor_sizes else None
+    for step in range(wl.steps):
+        for w in range(N):
+            if wl.tensor_sizes:
+                workloads.fill_worker_grad(wl, step, w, flat_tmp)
+                for t, s in enumerate(wl.tensor_sizes):
+                    grads[w][t].copy_(flat_tmp[offs[t]:offs[t + 1]])
+            else:
+                workloads.fill_worker_grad(wl, step, w, grads[w][0], scratch)
+        g_ref = [gather(grads[w]) for w in range(N)]
+        if plan is not None:
+            plan.step(wl.lr, wl.mu, wl.wd)
+        else:
+            lsgd.step(params[0], mom[0], [g[0] for g in grads], gow, G, wl.lr, wl.mu, wl.wd,
+                      [r[0] for r in reps])
+        rr = [np.zeros(idx.size, np.uint16 if rtd == torch.bfloat16 else np.float32) for _ in range(R)]
+        oracle.lsgd_step(p_ref, m_ref, g_ref, gow, G, wl.lr, wl.mu, wl.wd, rr,
+                         oracle.BF16 if rtd == torch.bfloat16 else oracle.F32)
+        torch.cuda.synchronize()
+        assert_close(gather(params), p_ref, "%s params step %d" % (name, step))
+        assert_close(gather(mom), m_ref, "%s momentum step %d" % (name, step))
+        for r in (0, R // 2, R - 1):
+            assert np.array_equal(gather(reps[r]), rr[r]), "%s replica %d step %d" % (name, r, step)
+        if step % 10 == 0 or step == wl.steps - 1:
+            log("  %s step %d ok (%d sampled elements)" % (name, step, idx.size))
+    if plan is not None:
+        plan.close()
+    del params, mom, grads, reps
+    torch.cuda.empty_cache()
