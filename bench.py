@@ -33,7 +33,7 @@ if ROOT not in sys.path:
 METRIC = "fused LSGD aggregate+update: achieved HBM GB/s and steps/s, 1 MI355X"
 PEAK_HBM_GBPS = 8000.0                     # MI355X HBM3E, published peak
 PROFILES = os.path.join(ROOT, "profiles")
-CALIB_ELEMS = 1 << 28                      # 1 GiB of fp32 for the counter calibration kernel
+CALIB_ELEMS = 1 << 28                      # 1 GiB of fp32 for the counter calibration copy
 
 
 def parse_args(argv=None):
@@ -47,7 +47,7 @@ def parse_args(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget")
     ap.add_argument("--no-r0", action="store_true", help="skip the secondary R=0 measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
-                    help="also launch a plain 1 GiB negate-copy kernel (counter calibration)")
+                    help="also launch a plain 1 GiB copy kernel (counter calibration)")
     ap.add_argument("--derive-traffic", action="store_true")
     ap.add_argument("--fetch-csv")
     ap.add_argument("--write-csv")
@@ -140,30 +140,30 @@ def time_steps(setup, steps, warmup):
 
 
 def copy_ceiling(dev, calibrate):
-    """GB/s of a plain device copy (2 GiB read + 2 GiB written): a measured
-    ceiling to read the kernel's fraction against."""
+    """GB/s of lsgd_stream_copy over 2 GiB (2 GiB read + 2 GiB written): a
+    measured ceiling for a plain two-stream read+write pattern, to read the
+    step kernel's fraction against. With `calibrate`, three more copies of
+    exactly 1 GiB: a kernel of known traffic for the FETCH_SIZE / WRITE_SIZE
+    counters."""
     import torch
+    import paper_1906_05936_amd as lsgd
     n = 1 << 29
     src = torch.ones(n, device=dev)
     dst = torch.empty_like(src)
     for _ in range(2):
-        dst.copy_(src)
+        lsgd.stream_copy(dst, src)
     torch.cuda.synchronize()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     reps = 10
     t0.record()
     for _ in range(reps):
-        dst.copy_(src)
+        lsgd.stream_copy(dst, src)
     t1.record()
     t1.synchronize()
     gbps = 2 * n * 4 * reps / (t0.elapsed_time(t1) * 1e-3) / 1e9
     if calibrate:
-        # plain negate-copy of a known size: its FETCH_SIZE / WRITE_SIZE counters
-        # calibrate the counters of the step kernel
-        a = src[:CALIB_ELEMS]
-        b = dst[:CALIB_ELEMS]
         for _ in range(3):
-            torch.neg(a, out=b)
+            lsgd.stream_copy(dst[:CALIB_ELEMS], src[:CALIB_ELEMS])
         torch.cuda.synchronize()
     del src, dst
     torch.cuda.empty_cache()
@@ -241,6 +241,22 @@ def _per_dispatch_kib(rows, counter, match):
     return sum(vals.values()) / len(vals), len(vals)
 
 
+def _calib_kib(rows, counter):
+    """The counter for the 1 GiB calibration copies: the stream_copy_kernel
+    dispatches of that size (the 2 GiB ceiling copies are skipped)."""
+    vals = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter or "stream_copy_kernel" not in r.get("Kernel_Name", ""):
+            continue
+        if int(r.get("Grid_Size", 0)) > (CALIB_ELEMS // 4) * 3 // 2:   # a 2 GiB ceiling copy
+            continue
+        d = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        vals[d] = vals.get(d, 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise SystemExit("no %s rows for the 1 GiB calibration copy" % counter)
+    return sum(vals.values()) / len(vals), len(vals)
+
+
 def kernel_match(wl):
     if wl.tensor_sizes:
         return "step_plan_kernel"
@@ -250,8 +266,8 @@ def kernel_match(wl):
 
 def derive_traffic(args):
     """FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the step kernel, each scaled
-    by what the same counter reads for the plain 1 GiB negate-copy (4 bytes read
-    and 4 written per element) launched by --calibrate-copy."""
+    by what the same counter reads for the plain 1 GiB copy (1 GiB read and
+    1 GiB written) launched by --calibrate-copy."""
     import workloads
     from paper_1906_05936_amd import build as libbuild
     wl = workloads.WORKLOADS[args.workload]
@@ -261,8 +277,8 @@ def derive_traffic(args):
     kname = kernel_match(wl)
     f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
     w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
-    f_c, _ = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", "neg")
-    w_c, _ = _per_dispatch_kib(write_rows, "WRITE_SIZE", "neg")
+    f_c, _ = _calib_kib(fetch_rows, "FETCH_SIZE")
+    w_c, _ = _calib_kib(write_rows, "WRITE_SIZE")
     known = CALIB_ELEMS * 4 / 1024.0
     f_scale, w_scale = known / f_c, known / w_c
     fetch_b = f_k * f_scale * 1024

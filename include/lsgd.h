@@ -94,6 +94,28 @@ LSGD_API const char* lsgd_status_string(lsgd_status status);
 LSGD_API const char* lsgd_last_error(void);
 
 /*
+ * Launch shape of the planless kernels, process-wide (a tuning knob; results
+ * are bit-identical for every shape, because each element is computed by one
+ * lane from its own inputs in a fixed order). Plans launch one workgroup per
+ * bucket and ignore it.
+ *   xcd_chunk       0 = workgroups in hardware order; C > 0 = each of the eight
+ *                   XCDs runs C consecutive logical workgroups per turn (the grid
+ *                   is padded to a multiple of 8*C; not applied to grids smaller
+ *                   than 8*C). Range [0, 65536].
+ *   blocks_per_cu   0 = the grid covers the work; B > 0 = at most B workgroups per
+ *                   compute unit, grid-stride. Range [0, 4096].
+ *   units_per_lane  U: a workgroup walks U consecutive passes of 256 16-byte
+ *                   units of every buffer (planless calls). Range [1, 256].
+ * Defaults: xcd_chunk 256, blocks_per_cu 0, units_per_lane 1. Takes effect for
+ * launches made after the call returns. Errors: LSGD_ERR_SIZE (out of range),
+ * LSGD_ERR_NULL (get).
+ */
+LSGD_API lsgd_status lsgd_set_launch_shape(int32_t xcd_chunk, int32_t blocks_per_cu,
+                                           int32_t units_per_lane);
+LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_per_cu,
+                                           int32_t* units_per_lane);
+
+/*
  * The local layer alone (Alg. 3, Reduce to the communicator and divide):
  *   group_means[j][i] = PW over the W members of group j of grads[w][i], / W.
  * grads          [n_workers] device pointers, each n elements of dtype gdt.

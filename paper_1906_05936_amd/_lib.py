@@ -23,8 +23,10 @@ MAX_REPLICAS = 128
 STATUS_NAMES = {0: "LSGD_OK", 1: "LSGD_ERR_NULL", 2: "LSGD_ERR_SIZE", 3: "LSGD_ERR_GROUPS",
                 4: "LSGD_ERR_ALIGN", 5: "LSGD_ERR_DTYPE", 6: "LSGD_ERR_HIP", 7: "LSGD_ERR_ALIAS"}
 
-EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_group_mean", "lsgd_global_mean",
-           "lsgd_sgd_step", "lsgd_step", "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy")
+EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
+           "lsgd_get_launch_shape", "lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step",
+           "lsgd_step", "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
+           "lsgd_stream_copy")
 
 
 class LsgdError(RuntimeError):
@@ -45,6 +47,8 @@ def _load():
     c_int = ctypes.c_int
     lib.lsgd_status_string.argtypes, lib.lsgd_status_string.restype = [c_int], ctypes.c_char_p
     lib.lsgd_last_error.argtypes, lib.lsgd_last_error.restype = [], ctypes.c_char_p
+    lib.lsgd_set_launch_shape.argtypes = [i32, i32, i32]
+    lib.lsgd_get_launch_shape.argtypes = [ctypes.POINTER(i32)] * 3
     lib.lsgd_group_mean.argtypes = [P, c_int, i32, P, i32, i64, P, P]
     lib.lsgd_global_mean.argtypes = [P, i32, i64, P, P]
     lib.lsgd_sgd_step.argtypes = [P, P, P, i64, f32, f32, f32, P, i32, c_int, P]
@@ -53,8 +57,10 @@ def _load():
                                      c_int]
     lib.lsgd_step_plan.argtypes = [P, f32, f32, f32, P]
     lib.lsgd_plan_destroy.argtypes, lib.lsgd_plan_destroy.restype = [P], None
+    lib.lsgd_stream_copy.argtypes = [P, P, i64, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
-                 "lsgd_plan_create", "lsgd_step_plan"):
+                 "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
+                 "lsgd_get_launch_shape", "lsgd_stream_copy"):
         getattr(lib, name).restype = c_int
     return lib
 
@@ -125,6 +131,29 @@ def _stream(stream, device):
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream)
+
+
+def set_launch_shape(xcd_chunk, blocks_per_cu, units_per_lane=1):
+    """lsgd_set_launch_shape: process-wide launch shape (never changes results)."""
+    check(lib.lsgd_set_launch_shape(int(xcd_chunk), int(blocks_per_cu), int(units_per_lane)))
+
+
+def get_launch_shape():
+    """lsgd_get_launch_shape -> (xcd_chunk, blocks_per_cu, units_per_lane)."""
+    c, b, u = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    check(lib.lsgd_get_launch_shape(ctypes.byref(c), ctypes.byref(b), ctypes.byref(u)))
+    return c.value, b.value, u.value
+
+
+def stream_copy(dst, src, stream=None):
+    """lsgd_stream_copy (measurement utility): dst = src, byte for byte."""
+    _dev_tensor(dst, "dst")
+    _dev_tensor(src, "src", None, None, dst.device)
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("dst and src differ in size")
+    with torch.cuda.device(dst.device):
+        check(lib.lsgd_stream_copy(dst.data_ptr(), src.data_ptr(), nbytes, _stream(stream, dst.device)))
 
 
 def step(params, momentum, grads, group_of_worker, n_groups, lr, momentum_coef, weight_decay,

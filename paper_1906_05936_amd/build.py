@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblsgd.so")
-SOURCES = ["lsgd_common.hip", "lsgd_flat.hip", "lsgd_plan.hip"]
+SOURCES = ["lsgd_common.hip", "lsgd_flat.hip", "lsgd_plan.hip", "lsgd_bench.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -65,8 +65,9 @@ def source_digest() -> str:
         if name.endswith((".hip", ".hpp")):
             with open(os.path.join(CSRC, name), "rb") as f:
                 h.update(name.encode() + b"\0" + f.read())
-    with open(os.path.join(INCLUDE, "lsgd.h"), "rb") as f:
-        h.update(f.read())
+    for name in ("lsgd.h", "lsgd_bench.h"):
+        with open(os.path.join(INCLUDE, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 

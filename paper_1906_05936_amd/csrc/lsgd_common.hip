@@ -19,19 +19,10 @@ thread_local std::string t_last_error;
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];
 
-// Workgroups per compute unit for grid-stride launches. LSGD_BLOCKS_PER_CU
-// overrides it (read once); 0 means one unit per thread, no grid-stride.
-int blocks_per_cu() {
-    static const int v = [] {
-        const char* e = getenv("LSGD_BLOCKS_PER_CU");
-        if (e && *e) {
-            int x = atoi(e);
-            if (x >= 0) return x;
-        }
-        return 8;
-    }();
-    return v;
-}
+// Process-wide launch shape (lsgd_set_launch_shape). Results never depend on it.
+std::atomic<int32_t> g_xcd_chunk{kDefaultXcdChunk};
+std::atomic<int32_t> g_blocks_per_cu{kDefaultBlocksPerCu};
+std::atomic<int32_t> g_units_per_lane{kDefaultUnitsPerLane};
 }  // namespace
 
 lsgd_status fail(lsgd_status st, const char* fmt, ...) {
@@ -107,16 +98,41 @@ int device_cus() {
     return c;
 }
 
-unsigned grid_blocks(int64_t units) {
-    int64_t need = (units + kBlock - 1) / kBlock;
-    if (need < 1) need = 1;
-    const int bpc = blocks_per_cu();
+namespace {
+// `blocks` logical workgroups padded to a multiple of 8 * xcd_chunk (the chunk
+// is dropped for grids smaller than one full turn of the eight XCDs).
+LaunchShape pad_for_xcd_chunk(int64_t blocks) {
+    LaunchShape ls;
+    int64_t need = blocks < 1 ? 1 : blocks;
+    int64_t chunk = g_xcd_chunk.load(std::memory_order_relaxed);
+    if (chunk > 0 && need >= 8 * chunk && need <= 0x7fffffff - 8 * chunk) {
+        const int64_t group = 8 * chunk;
+        need = (need + group - 1) / group * group;
+    } else {
+        chunk = 0;
+    }
+    // The kernels grid-stride, so a capped grid still covers the work (the
+    // renumbering is off in that case, so it stays a bijection).
+    if (need > 0x7fffffff) need = 0x7fffffff;
+    ls.blocks = static_cast<unsigned>(need);
+    ls.xcd_chunk = static_cast<uint32_t>(chunk);
+    ls.upl = 1;
+    return ls;
+}
+}  // namespace
+
+LaunchShape launch_shape(int64_t units) {
+    const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);
+    const int64_t span = static_cast<int64_t>(kBlock) * upl;
+    int64_t need = (units + span - 1) / span;
+    const int32_t bpc = g_blocks_per_cu.load(std::memory_order_relaxed);
     if (bpc > 0) {
         const int64_t cap = static_cast<int64_t>(device_cus()) * bpc;
         if (need > cap) need = cap;
     }
-    if (need > 0x7fffffff) need = 0x7fffffff;
-    return static_cast<unsigned>(need);
+    LaunchShape ls = pad_for_xcd_chunk(need);
+    ls.upl = static_cast<uint32_t>(upl);
+    return ls;
 }
 
 }  // namespace lsgd
@@ -138,5 +154,29 @@ LSGD_API const char* lsgd_status_string(lsgd_status status) {
 }
 
 LSGD_API const char* lsgd_last_error(void) { return lsgd::t_last_error.c_str(); }
+
+LSGD_API lsgd_status lsgd_set_launch_shape(int32_t xcd_chunk, int32_t blocks_per_cu,
+                                           int32_t units_per_lane) {
+    if (xcd_chunk < 0 || xcd_chunk > 65536)
+        return lsgd::fail(LSGD_ERR_SIZE, "xcd_chunk=%d outside [0, 65536]", xcd_chunk);
+    if (blocks_per_cu < 0 || blocks_per_cu > 4096)
+        return lsgd::fail(LSGD_ERR_SIZE, "blocks_per_cu=%d outside [0, 4096]", blocks_per_cu);
+    if (units_per_lane < 1 || units_per_lane > 256)
+        return lsgd::fail(LSGD_ERR_SIZE, "units_per_lane=%d outside [1, 256]", units_per_lane);
+    lsgd::g_xcd_chunk.store(xcd_chunk, std::memory_order_relaxed);
+    lsgd::g_blocks_per_cu.store(blocks_per_cu, std::memory_order_relaxed);
+    lsgd::g_units_per_lane.store(units_per_lane, std::memory_order_relaxed);
+    return LSGD_OK;
+}
+
+LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_per_cu,
+                                           int32_t* units_per_lane) {
+    if (!xcd_chunk || !blocks_per_cu || !units_per_lane)
+        return lsgd::fail(LSGD_ERR_NULL, "output pointer is NULL");
+    *xcd_chunk = lsgd::g_xcd_chunk.load(std::memory_order_relaxed);
+    *blocks_per_cu = lsgd::g_blocks_per_cu.load(std::memory_order_relaxed);
+    *units_per_lane = lsgd::g_units_per_lane.load(std::memory_order_relaxed);
+    return LSGD_OK;
+}
 
 }  // extern "C"

@@ -128,10 +128,12 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
     a.rdt = static_cast<int32_t>(rdt);
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
-    const int vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    const unsigned blocks = grid_blocks(n / vec);
+    const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
+    const LaunchShape ls = launch_shape((n + vec - 1) / vec);
+    a.xcd_chunk = ls.xcd_chunk;
+    a.upl = ls.upl;
     FlatKernel k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
-    hipLaunchKernelGGL(k, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_step");
 }
 
@@ -160,13 +162,15 @@ LSGD_API lsgd_status lsgd_group_mean(const void* const* grads, lsgd_dtype gdt, i
     a.n_workers = n_workers;
     a.n_groups = n_groups;
     a.W = n_workers / n_groups;
-    const int vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    const unsigned blocks = grid_blocks(n / vec);
+    const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
+    const LaunchShape ls = launch_shape((n + vec - 1) / vec);
+    a.xcd_chunk = ls.xcd_chunk;
+    a.upl = ls.upl;
     if (gdt == LSGD_BF16)
-        hipLaunchKernelGGL(group_mean_kernel<uint16_t>, dim3(blocks), dim3(kBlock), 0,
+        hipLaunchKernelGGL(group_mean_kernel<uint16_t>, dim3(ls.blocks), dim3(kBlock), 0,
                            static_cast<hipStream_t>(stream), a);
     else
-        hipLaunchKernelGGL(group_mean_kernel<float>, dim3(blocks), dim3(kBlock), 0,
+        hipLaunchKernelGGL(group_mean_kernel<float>, dim3(ls.blocks), dim3(kBlock), 0,
                            static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_group_mean");
 }
@@ -195,7 +199,10 @@ LSGD_API lsgd_status lsgd_global_mean(const float* const* group_means, int32_t n
     a.out[0] = grad_mean;
     a.n = n;
     a.n_groups = n_groups;
-    hipLaunchKernelGGL(global_mean_kernel, dim3(grid_blocks(n / 4)), dim3(kBlock), 0,
+    const LaunchShape ls = launch_shape((n + 3) / 4);
+    a.xcd_chunk = ls.xcd_chunk;
+    a.upl = ls.upl;
+    hipLaunchKernelGGL(global_mean_kernel, dim3(ls.blocks), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_global_mean");
 }
@@ -225,7 +232,10 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     a.n_replicas = n_replicas;
     a.rdt = static_cast<int32_t>(rdt);
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
-    hipLaunchKernelGGL(sgd_kernel, dim3(grid_blocks(n / 4)), dim3(kBlock), 0,
+    const LaunchShape ls = launch_shape((n + 3) / 4);
+    a.xcd_chunk = ls.xcd_chunk;
+    a.upl = ls.upl;
+    hipLaunchKernelGGL(sgd_kernel, dim3(ls.blocks), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_sgd_step");
 }

@@ -37,9 +37,23 @@ struct Range {
 // never overlap). Sort-and-sweep, O(k log k).
 lsgd_status check_overlap(std::vector<Range>& ranges);
 
-// Blocks for a grid-stride launch over `units` 16-byte units on the current
-// device: min(ceil(units / kBlock), compute units * blocks-per-CU).
-unsigned grid_blocks(int64_t units);
+// Default launch shape of the planless kernels: XCD chunk of 256 workgroups
+// (each XCD walks 1 MB of every buffer per turn), one-shot grids, one unit per
+// lane per workgroup. Changed process-wide by lsgd_set_launch_shape.
+constexpr int32_t kDefaultXcdChunk = 256;
+constexpr int32_t kDefaultBlocksPerCu = 0;
+constexpr int32_t kDefaultUnitsPerLane = 1;
+
+struct LaunchShape {
+    unsigned blocks;     // grid size (padded to a multiple of 8 * xcd_chunk)
+    uint32_t xcd_chunk;  // 0 when the grid is too small to renumber
+    uint32_t upl;        // consecutive passes of kBlock units per logical block
+};
+
+// Grid for `units` work items: ceil(units / (kBlock * upl)) workgroups, capped
+// at compute units * blocks-per-CU when that is set (the kernels then
+// grid-stride), then padded for the XCD chunking.
+LaunchShape launch_shape(int64_t units);
 
 // Compute units of the current device (cached per device).
 int device_cus();

@@ -43,6 +43,38 @@ __host__ __device__ constexpr int pw_split(int k) {
     return h;
 }
 
+// Workgroups are dispatched to the eight XCDs round-robin by block index (block
+// b runs on XCD b % 8). With xcd_chunk = C > 0 the kernels renumber blocks so
+// that each XCD runs C consecutive logical blocks per turn: the chip-wide set of
+// active addresses stays one contiguous window per buffer, while each XCD walks
+// C * 4 KB runs of every buffer, which keeps fewer distinct pages live in that
+// XCD's address-translation caches. The host pads the grid to a multiple of
+// 8*C so that the renumbering is a bijection on [0, gridDim.x).
+__device__ __forceinline__ uint32_t logical_block(uint32_t b, uint32_t chunk) {
+    if (chunk == 0) return b;
+    const uint32_t x = b & 7u, i = b >> 3;
+    return ((i / chunk) * 8u + x) * chunk + (i % chunk);
+}
+
+// Runs body(u) for every unit u in [0, units). A logical block owns `upl`
+// consecutive passes of kBlock units (one unit per lane per pass), so each
+// workgroup walks upl * 4 KB of every buffer in address order; logical blocks
+// are taken in XCD-chunked order, grid-stride when the grid is smaller than
+// the work.
+template <typename Body>
+__device__ __forceinline__ void for_units(int64_t units, uint32_t chunk, uint32_t upl,
+                                          const Body& body) {
+    const int64_t span = static_cast<int64_t>(kBlock) * upl;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * span;
+    for (int64_t base = static_cast<int64_t>(logical_block(blockIdx.x, chunk)) * span; base < units;
+         base += stride) {
+        for (uint32_t q = 0; q < upl; ++q) {
+            const int64_t u = base + static_cast<int64_t>(q) * kBlock + threadIdx.x;
+            if (u < units) body(u);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- loads/stores
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
@@ -258,6 +290,7 @@ struct StepArgs {
     Hyper h;
     int32_t n_workers, n_groups, W;
     int32_t n_replicas, rdt;
+    uint32_t xcd_chunk, upl;
     const void* grads[kMaxWorkers];
     void* replicas[kMaxReplicas];
 };
@@ -266,6 +299,7 @@ struct StepArgs {
 struct MeanArgs {
     int64_t n;
     int32_t n_workers, n_groups, W;
+    uint32_t xcd_chunk, upl;
     const void* in[kMaxWorkers];
     float* out[kMaxWorkers];
 };
@@ -372,17 +406,18 @@ struct FlatSrc {
 
 // Grid-stride loop over the full units of a flat vector; the ragged tail
 // (n % VEC elements) is handled by thread 0 of block 0 after its loop.
+// The unit index space is [0, full] with unit `full` the ragged tail
+// (n % VEC elements, present only when that is nonzero).
 template <typename GT, int W, int G>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrc s{a};
     const int64_t full = a.n / VEC;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
-        fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
     const int rem = static_cast<int>(a.n - full * VEC);
-    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0)
-        fused_unit_ct<GT, W, G, true>(s, full * VEC, rem);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
+        else fused_unit_ct<GT, W, G, true>(s, u * VEC, rem);
+    });
 }
 
 template <typename GT>
@@ -390,12 +425,11 @@ __global__ __launch_bounds__(kBlock) void step_flat_rt(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrc s{a};
     const int64_t full = a.n / VEC;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
-        fused_unit_rt<GT, false>(s, a.W, a.n_groups, u * VEC, VEC);
     const int rem = static_cast<int>(a.n - full * VEC);
-    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0)
-        fused_unit_rt<GT, true>(s, a.W, a.n_groups, full * VEC, rem);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) fused_unit_rt<GT, false>(s, a.W, a.n_groups, u * VEC, VEC);
+        else fused_unit_rt<GT, true>(s, a.W, a.n_groups, u * VEC, rem);
+    });
 }
 
 // lsgd_group_mean: every group's mean of its W members, for one unit.
@@ -418,11 +452,11 @@ template <typename GT>
 __global__ __launch_bounds__(kBlock) void group_mean_kernel(MeanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const int64_t full = a.n / VEC;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
-        group_mean_unit<GT, false>(a, u * VEC, VEC);
     const int rem = static_cast<int>(a.n - full * VEC);
-    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) group_mean_unit<GT, true>(a, full * VEC, rem);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) group_mean_unit<GT, false>(a, u * VEC, VEC);
+        else group_mean_unit<GT, true>(a, u * VEC, rem);
+    });
 }
 
 // lsgd_global_mean: PW over the G group means, / G, for one 4-element unit.
@@ -440,11 +474,11 @@ __device__ __forceinline__ void global_mean_unit(const MeanArgs& a, int64_t e0, 
 
 static __global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) {
     const int64_t full = a.n / 4;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
-        global_mean_unit<false>(a, u * 4, 4);
     const int rem = static_cast<int>(a.n - full * 4);
-    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) global_mean_unit<true>(a, full * 4, rem);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) global_mean_unit<false>(a, u * 4, 4);
+        else global_mean_unit<true>(a, u * 4, rem);
+    });
 }
 
 // lsgd_sgd_step: update and copy-out from a precomputed mean gradient.
@@ -462,11 +496,11 @@ __device__ __forceinline__ void sgd_unit(const StepArgs& a, int64_t e0, int cnt)
 
 static __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
     const int64_t full = a.n / 4;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t u = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; u < full; u += stride)
-        sgd_unit<false>(a, u * 4, 4);
     const int rem = static_cast<int>(a.n - full * 4);
-    if (rem != 0 && blockIdx.x == 0 && threadIdx.x == 0) sgd_unit<true>(a, full * 4, rem);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) sgd_unit<false>(a, u * 4, 4);
+        else sgd_unit<true>(a, u * 4, rem);
+    });
 }
 
 // ------------------------------------------------------------- multi-tensor plan
@@ -488,6 +522,8 @@ struct PlanArgs {
     void* const* ptrs;
     int32_t stride, n_workers, n_groups, W;
     int32_t n_replicas, rdt;
+    int32_t n_buckets;
+    uint32_t xcd_chunk;
     Hyper h;
 };
 
@@ -503,14 +539,16 @@ struct PlanSrc {
     __device__ Hyper hyper() const { return a.h; }
 };
 
-// One workgroup per bucket; a bucket is a run of chunks (one large piece, or
-// several small tensors). Chunk and pointer-table reads are uniform per
-// workgroup.
+// One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
+// (one large piece, or several small tensors). Chunk and pointer-table reads
+// are uniform per workgroup.
 template <typename GT, int W, int G>
 __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const int32_t c_end = a.bucket_begin[blockIdx.x + 1];
-    for (int32_t c = a.bucket_begin[blockIdx.x]; c < c_end; ++c) {
+    const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
+    if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
+    const int32_t c_end = a.bucket_begin[b + 1];
+    for (int32_t c = a.bucket_begin[b]; c < c_end; ++c) {
         const PlanChunk ch = a.chunks[c];
         const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a};
         const int64_t full = ch.len / VEC;
@@ -524,6 +562,19 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
             else fused_unit_rt<GT, true>(s, a.W, a.n_groups, ch.start + full * VEC, rem);
         }
     }
+}
+
+}  // namespace lsgd
+
+namespace lsgd {
+
+// Plain streaming copy (measurement utility): one 16-byte unit per lane.
+static __global__ __launch_bounds__(kBlock) void stream_copy_kernel(u32x4* __restrict__ dst,
+                                                                    const u32x4* __restrict__ src,
+                                                                    int64_t units, uint32_t chunk) {
+    for_units(units, chunk, 1, [&](int64_t u) {
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
+    });
 }
 
 }  // namespace lsgd

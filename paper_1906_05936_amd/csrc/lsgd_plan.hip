@@ -199,6 +199,10 @@ LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momen
     a.n_replicas = plan->n_replicas;
     a.rdt = static_cast<int32_t>(plan->rdt);
     a.h = Hyper{lr, momentum_coef, weight_decay};
+    a.n_buckets = plan->n_buckets;
+    // One workgroup per bucket in hardware order: a bucket already walks up to
+    // 32 KB of each buffer, and measurements favoured no XCD renumbering here.
+    a.xcd_chunk = 0;
     PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups)
                                           : pick_plan<float>(plan->W, plan->n_groups);
     hipLaunchKernelGGL(k, dim3(plan->n_buckets), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);

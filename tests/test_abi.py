@@ -11,6 +11,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "lsgd.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 import torch
 
@@ -31,15 +33,18 @@ MB = 1 << 20
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    return re.findall(r"LSGD_API\s+[\w\s\*]+?\b(lsgd_\w+)\s*\(", text)
+    names = []
+    for h in HEADERS:
+        names += re.findall(r"LSGD_API\s+[\w\s\*]+?\b(lsgd_\w+)\s*\(", open(h).read())
+    return names
 
 
 def test_header_declares_the_boundary():
     names = set(declared_functions())
     assert {"lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
             "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
-            "lsgd_status_string", "lsgd_last_error"} == names
+            "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
+            "lsgd_get_launch_shape", "lsgd_stream_copy"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -195,3 +200,31 @@ def test_package_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         L._load()
+
+
+def test_launch_shape_setter():
+    c, b, u = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    get = lambda: lib.lsgd_get_launch_shape(ctypes.byref(c), ctypes.byref(b), ctypes.byref(u))
+    assert get() == OK
+    default = (c.value, b.value, u.value)
+    assert default == (256, 0, 1)
+    assert lib.lsgd_set_launch_shape(-1, 0, 1) == SIZE
+    assert lib.lsgd_set_launch_shape(0, 5000, 1) == SIZE
+    assert lib.lsgd_set_launch_shape(70000, 0, 1) == SIZE
+    assert lib.lsgd_set_launch_shape(0, 0, 0) == SIZE
+    assert lib.lsgd_set_launch_shape(0, 0, 300) == SIZE
+    assert lib.lsgd_get_launch_shape(None, ctypes.byref(b), ctypes.byref(u)) == NULL
+    assert lib.lsgd_set_launch_shape(4, 8, 2) == OK
+    get()
+    assert (c.value, b.value, u.value) == (4, 8, 2)
+    assert lib.lsgd_set_launch_shape(*default) == OK
+
+
+def test_stream_copy_validation():
+    f = lib.lsgd_stream_copy
+    assert f(A, A + 100 * MB, -16, None) == SIZE
+    assert f(A, A + 100 * MB, 100, None) == SIZE          # not a multiple of 16
+    assert f(0, 0, 0, None) == OK                          # no-op
+    assert f(0, A, 64, None) == NULL
+    assert f(A + 8, A + 100 * MB, 64, None) == ALIGN
+    assert f(A, A + 32, 64, None) == ALIAS

@@ -391,3 +391,45 @@ def test_workload_full_size_sampled(name):
         plan.close()
     del params, mom, grads, reps
     torch.cuda.empty_cache()
+
+
+def test_results_independent_of_launch_shape():
+    """Every launch shape (XCD chunking, grid-stride caps, units per lane) gives
+    the same bits: each element is computed by one lane from its own inputs."""
+    shapes = [(16, 0, 1), (0, 0, 1), (256, 0, 1), (0, 8, 1), (16, 0, 4), (4, 2, 8), (0, 1, 1),
+              (1, 0, 3)]
+    default = lsgd.get_launch_shape()
+    try:
+        for gdt, G, W, n in [("f32", 4, 4, 1_000_003), ("bf16", 8, 8, 400_009), ("f32", 3, 5, 77_777)]:
+            log("launch shapes %s G=%d W=%d n=%d" % (gdt, G, W, n))
+            rng = np.random.default_rng(n)
+            gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(G * W)]
+            grads = [to_dev(x) for x in gh]
+            p0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+            gow = groups_for(G, W, "shuffled", seed=1)
+            outs = []
+            for sh in shapes:
+                lsgd.set_launch_shape(*sh)
+                p, m = p0.clone(), torch.zeros(n, device=DEV)
+                reps = [torch.empty(n, device=DEV) for _ in range(2)]
+                for _ in range(2):
+                    lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
+                gm = [torch.empty(n, device=DEV) for _ in range(G)]
+                lsgd.group_mean(grads, gow, G, gm)
+                gbar = torch.empty(n, device=DEV)
+                lsgd.global_mean(gm, gbar)
+                outs.append((p, m, reps[1], gbar))
+            for sh, o in zip(shapes[1:], outs[1:]):
+                for a, b in zip(outs[0], o):
+                    assert torch.equal(a, b), sh
+    finally:
+        lsgd.set_launch_shape(*default)
+
+
+@pytest.mark.parametrize("nbytes", [16, 48, 4096 + 16, 1 << 20, (1 << 27) + 16 * 333])
+def test_stream_copy_is_exact(nbytes):
+    src = torch.randint(-2 ** 31, 2 ** 31 - 1, (nbytes // 4,), device=DEV, dtype=torch.int32)
+    dst = torch.zeros_like(src)
+    lsgd.stream_copy(dst, src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
