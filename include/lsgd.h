@@ -101,15 +101,19 @@ LSGD_API const char* lsgd_last_error(void);
  *   xcd_chunk       0 = workgroups in hardware order; C > 0 = each of the eight
  *                   XCDs runs C consecutive logical workgroups per turn (the grid
  *                   is padded to a multiple of 8*C; not applied to grids smaller
- *                   than 8*C). Range [0, 65536].
+ *                   than 8*C); LSGD_XCD_CHUNK_AUTO (-1) = the C that gives each
+ *                   XCD 512 KB of every buffer per turn. Range [-1, 65536].
  *   blocks_per_cu   0 = the grid covers the work; B > 0 = at most B workgroups per
  *                   compute unit, grid-stride. Range [0, 4096].
- *   units_per_lane  U: a workgroup walks U consecutive passes of 256 16-byte
- *                   units of every buffer (planless calls). Range [1, 256].
- * Defaults: xcd_chunk 256, blocks_per_cu 0, units_per_lane 1. Takes effect for
+ *   units_per_lane  P: a workgroup walks P consecutive passes of its lane tiles
+ *                   (256 lanes, each a tile of one or two 16-byte units) of
+ *                   every buffer. Range [1, 256].
+ * Defaults: xcd_chunk LSGD_XCD_CHUNK_AUTO, blocks_per_cu 0, units_per_lane 1.
+ * Takes effect for
  * launches made after the call returns. Errors: LSGD_ERR_SIZE (out of range),
  * LSGD_ERR_NULL (get).
  */
+#define LSGD_XCD_CHUNK_AUTO (-1)
 LSGD_API lsgd_status lsgd_set_launch_shape(int32_t xcd_chunk, int32_t blocks_per_cu,
                                            int32_t units_per_lane);
 LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_per_cu,

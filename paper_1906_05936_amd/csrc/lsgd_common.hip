@@ -100,11 +100,14 @@ int device_cus() {
 
 namespace {
 // `blocks` logical workgroups padded to a multiple of 8 * xcd_chunk (the chunk
-// is dropped for grids smaller than one full turn of the eight XCDs).
-LaunchShape pad_for_xcd_chunk(int64_t blocks) {
+// is dropped for grids smaller than one full turn of the eight XCDs). The
+// automatic chunk gives each XCD kAutoChunkBytes of every buffer per turn:
+// a workgroup pass covers kBlock lanes * tile units * 16 bytes.
+LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
     LaunchShape ls;
     int64_t need = blocks < 1 ? 1 : blocks;
     int64_t chunk = g_xcd_chunk.load(std::memory_order_relaxed);
+    if (chunk == kXcdChunkAuto) chunk = std::max<int64_t>(1, kAutoChunkBytes / block_bytes);
     if (chunk > 0 && need >= 8 * chunk && need <= 0x7fffffff - 8 * chunk) {
         const int64_t group = 8 * chunk;
         need = (need + group - 1) / group * group;
@@ -121,16 +124,16 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks) {
 }
 }  // namespace
 
-LaunchShape launch_shape(int64_t units) {
+LaunchShape launch_shape(int64_t units, int tile) {
     const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);
-    const int64_t span = static_cast<int64_t>(kBlock) * upl;
+    const int64_t span = static_cast<int64_t>(kBlock) * upl * (tile < 1 ? 1 : tile);
     int64_t need = (units + span - 1) / span;
     const int32_t bpc = g_blocks_per_cu.load(std::memory_order_relaxed);
     if (bpc > 0) {
         const int64_t cap = static_cast<int64_t>(device_cus()) * bpc;
         if (need > cap) need = cap;
     }
-    LaunchShape ls = pad_for_xcd_chunk(need);
+    LaunchShape ls = pad_for_xcd_chunk(need, static_cast<int64_t>(kBlock) * 16 * (tile < 1 ? 1 : tile) * upl);
     ls.upl = static_cast<uint32_t>(upl);
     return ls;
 }
@@ -157,8 +160,8 @@ LSGD_API const char* lsgd_last_error(void) { return lsgd::t_last_error.c_str(); 
 
 LSGD_API lsgd_status lsgd_set_launch_shape(int32_t xcd_chunk, int32_t blocks_per_cu,
                                            int32_t units_per_lane) {
-    if (xcd_chunk < 0 || xcd_chunk > 65536)
-        return lsgd::fail(LSGD_ERR_SIZE, "xcd_chunk=%d outside [0, 65536]", xcd_chunk);
+    if (xcd_chunk < lsgd::kXcdChunkAuto || xcd_chunk > 65536)
+        return lsgd::fail(LSGD_ERR_SIZE, "xcd_chunk=%d outside [-1, 65536]", xcd_chunk);
     if (blocks_per_cu < 0 || blocks_per_cu > 4096)
         return lsgd::fail(LSGD_ERR_SIZE, "blocks_per_cu=%d outside [0, 4096]", blocks_per_cu);
     if (units_per_lane < 1 || units_per_lane > 256)

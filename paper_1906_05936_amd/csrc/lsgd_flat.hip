@@ -10,25 +10,32 @@ namespace {
 
 using FlatKernel = void (*)(StepArgs);
 
+// A kernel and the number of units per lane tile it processes.
+struct FlatPick {
+    FlatKernel kernel;
+    int tile;
+};
+
 // Compile-time (W, G) kernels for power-of-two counts up to 16 each (and
 // N <= 128); every other grouping takes the runtime-count kernel. Both give
 // the same bits.
 template <typename GT, int W>
 FlatKernel pick_flat_g(int G) {
+    constexpr int U = TileUnits<GT>::U;
     switch (G) {
-        case 1: return step_flat_ct<GT, W, 1>;
-        case 2: return step_flat_ct<GT, W, 2>;
-        case 4: return step_flat_ct<GT, W, 4>;
-        case 8: return step_flat_ct<GT, W, 8>;
+        case 1: return step_flat_ct<GT, W, 1, U>;
+        case 2: return step_flat_ct<GT, W, 2, U>;
+        case 4: return step_flat_ct<GT, W, 4, U>;
+        case 8: return step_flat_ct<GT, W, 8, U>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16>;
+            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16, U>;
             else return nullptr;
     }
     return nullptr;
 }
 
 template <typename GT>
-FlatKernel pick_flat(int W, int G) {
+FlatPick pick_flat(int W, int G) {
     FlatKernel k = nullptr;
     switch (W) {
         case 1: k = pick_flat_g<GT, 1>(G); break;
@@ -37,7 +44,8 @@ FlatKernel pick_flat(int W, int G) {
         case 8: k = pick_flat_g<GT, 8>(G); break;
         case 16: k = pick_flat_g<GT, 16>(G); break;
     }
-    return k ? k : step_flat_rt<GT>;
+    if (k) return FlatPick{k, TileUnits<GT>::U};
+    return FlatPick{step_flat_rt<GT>, 1};
 }
 
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
@@ -129,11 +137,11 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    const LaunchShape ls = launch_shape((n + vec - 1) / vec);
+    const FlatPick k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    FlatKernel k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
-    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_step");
 }
 

@@ -37,10 +37,12 @@ struct Range {
 // never overlap). Sort-and-sweep, O(k log k).
 lsgd_status check_overlap(std::vector<Range>& ranges);
 
-// Default launch shape of the planless kernels: XCD chunk of 256 workgroups
-// (each XCD walks 1 MB of every buffer per turn), one-shot grids, one unit per
-// lane per workgroup. Changed process-wide by lsgd_set_launch_shape.
-constexpr int32_t kDefaultXcdChunk = 256;
+// Default launch shape of the planless kernels: automatic XCD chunk (each XCD
+// walks kAutoChunkBytes of every buffer per turn), one-shot grids, one pass per
+// workgroup. Changed process-wide by lsgd_set_launch_shape.
+constexpr int32_t kXcdChunkAuto = -1;
+constexpr int64_t kAutoChunkBytes = 512 * 1024;
+constexpr int32_t kDefaultXcdChunk = kXcdChunkAuto;
 constexpr int32_t kDefaultBlocksPerCu = 0;
 constexpr int32_t kDefaultUnitsPerLane = 1;
 
@@ -50,10 +52,11 @@ struct LaunchShape {
     uint32_t upl;        // consecutive passes of kBlock units per logical block
 };
 
-// Grid for `units` work items: ceil(units / (kBlock * upl)) workgroups, capped
-// at compute units * blocks-per-CU when that is set (the kernels then
-// grid-stride), then padded for the XCD chunking.
-LaunchShape launch_shape(int64_t units);
+// Grid for `units` 16-byte units processed in lane tiles of `tile` units:
+// ceil(units / (kBlock * tile * upl)) workgroups, capped at compute units *
+// blocks-per-CU when that is set (the kernels then grid-stride), then padded
+// for the XCD chunking.
+LaunchShape launch_shape(int64_t units, int tile = 1);
 
 // Compute units of the current device (cached per device).
 int device_cus();

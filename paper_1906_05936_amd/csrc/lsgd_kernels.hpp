@@ -75,6 +75,44 @@ __device__ __forceinline__ void for_units(int64_t units, uint32_t chunk, uint32_
     }
 }
 
+// Tiled variant of for_units: a lane's tile is U units kBlock apart (so every
+// wave instruction still covers 1 KB of one buffer), and a kernel visits each
+// buffer once per tile for all U units (stream-major), which keeps consecutive
+// instructions of a wave on the same pages and DRAM rows. tile(e0) gets the U
+// element offsets of a tile whose units are all complete; unit(u) handles the
+// units of the last, partial tile one by one (u < units_all).
+template <int U, int VEC, typename TileFn, typename UnitFn>
+__device__ __forceinline__ void for_tiles(int64_t units_full, int64_t units_all, uint32_t chunk,
+                                          uint32_t upl, const TileFn& tile, const UnitFn& unit) {
+    const int64_t tspan = static_cast<int64_t>(kBlock) * U;
+    const int64_t span = tspan * upl;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * span;
+    for (int64_t base = static_cast<int64_t>(logical_block(blockIdx.x, chunk)) * span; base < units_all;
+         base += stride) {
+        for (uint32_t pass = 0; pass < upl; ++pass) {
+            const int64_t t0 = base + static_cast<int64_t>(pass) * tspan + threadIdx.x;
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < units_full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                tile(e0);
+            } else {
+#pragma unroll
+                for (int q = 0; q < U; ++q) {
+                    const int64_t u = t0 + static_cast<int64_t>(q) * kBlock;
+                    if (u < units_all) unit(u);
+                }
+            }
+        }
+    }
+}
+
+// The q-th VEC-float slice of a tile array.
+template <int VEC, int T>
+__device__ __forceinline__ float (&slice(float (&x)[T], int q))[VEC] {
+    return *reinterpret_cast<float(*)[VEC]>(&x[q * VEC]);
+}
+
 // ---------------------------------------------------------------- loads/stores
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
@@ -306,37 +344,53 @@ struct MeanArgs {
 
 // ------------------------------------------------------------- per-unit bodies
 
-// Widened gradient values one lane may hold at once before the compiler's load
-// hoisting starts to cost occupancy: 16 fp32 units or 8 bf16 units.
-constexpr int kUnrollFloats = 64;
+// Units per lane tile in the compile-time fused kernels (measured: two fp32
+// units per lane, visited stream-major, beat one; bf16 tiles stay at one unit
+// to bound registers).
+template <typename GT> struct TileUnits;
+template <> struct TileUnits<float> { static constexpr int U = 2; };
+template <> struct TileUnits<uint16_t> { static constexpr int U = 1; };
 
-// Fused step on one unit, compile-time W and G (powers of two).
-// Small N: the whole two-level tree is unrolled and every load is issued up
-// front. Large N: groups are streamed GU at a time (GU*W units in flight per
-// lane) and folded into a pairwise accumulator over groups, which yields the
-// same PW order.
-template <typename GT, int W, int G, bool TAIL, typename Src>
-__device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt) {
+// Widened gradient values one lane may hold at once: up to kUnrollFloats the
+// whole two-level tree is unrolled with every load issued up front (32 fp32
+// units = a 4x4 grouping with two-unit tiles); above it groups stream through
+// in batches of about kStreamFloats, which bounds registers (and so keeps
+// occupancy) for the 64- and 128-worker groupings.
+constexpr int kUnrollFloats = 128;
+constexpr int kStreamFloats = 64;
+
+// Fused step on one tile of U units, compile-time W and G (powers of two).
+// Every array holds T = U*VEC floats: the tree is the same PW for each of them.
+// Small N*T: the whole two-level tree is unrolled and every load issued up
+// front. Large: groups are streamed GU at a time and folded into a pairwise
+// accumulator over groups, which yields the same PW order. TAIL (the ragged
+// end of a tensor, cnt < VEC elements) only with U = 1.
+template <typename GT, int W, int G, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[U], int cnt) {
+    static_assert(!TAIL || U == 1, "ragged units are processed one at a time");
     constexpr int VEC = Unit<GT>::VEC;
-    auto group_leaf = [&](int j, float (&gm)[VEC]) {
-        auto member_leaf = [&](int k, float (&x)[VEC]) {
-            load_grad<GT, TAIL>(s.grad(j * W + k), e0, cnt, x);
-        };
-        float sum[VEC];
-        pw_tree<0, W, VEC>(member_leaf, sum);
+    constexpr int T = U * VEC;
+    auto group_leaf = [&](int j, float (&gm)[T]) {
+        auto member_leaf = [&](int k, float (&x)[T]) {
+            const void* g = s.grad(j * W + k);
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) gm[v] = sum[v] / static_cast<float>(W);
+            for (int q = 0; q < U; ++q) load_grad<GT, TAIL>(g, e0[q], cnt, slice<VEC, T>(x, q));
+        };
+        float sum[T];
+        pw_tree<0, W, T>(member_leaf, sum);
+#pragma unroll
+        for (int v = 0; v < T; ++v) gm[v] = sum[v] / static_cast<float>(W);
     };
-    float tot[VEC], gbar[VEC];
-    if constexpr (W * G * VEC <= kUnrollFloats) {
-        pw_tree<0, G, VEC>(group_leaf, tot);
+    float tot[T], gbar[T];
+    if constexpr (W * G * T <= kUnrollFloats) {
+        pw_tree<0, G, T>(group_leaf, tot);
     } else {
-        constexpr int GU0 = kUnrollFloats / (W * VEC);
+        constexpr int GU0 = kStreamFloats / (W * T);
         constexpr int GU = GU0 < 1 ? 1 : (GU0 > G ? G : GU0);
-        PwAcc<VEC, ilog2(G) + 1> groups;
+        PwAcc<T, ilog2(G) + 1> groups;
 #pragma unroll 1
         for (int j0 = 0; j0 < G; j0 += GU) {
-            float gm[GU][VEC];
+            float gm[GU][T];
 #pragma unroll
             for (int q = 0; q < GU; ++q) group_leaf(j0 + q, gm[q]);
 #pragma unroll
@@ -345,17 +399,31 @@ __device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt)
         groups.result(tot);
     }
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) gbar[v] = tot[v] / static_cast<float>(G);
+    for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
 
-    float p[VEC], m[VEC];
-    load_f32<VEC, TAIL>(s.p(), e0, cnt, p);
-    load_f32<VEC, TAIL>(s.m(), e0, cnt, m);
-    sgd_update<VEC>(s.hyper(), gbar, p, m);
-    store_f32<VEC, TAIL>(s.p(), e0, cnt, p);
-    store_f32<VEC, TAIL>(s.m(), e0, cnt, m);
+    float p[T], m[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    sgd_update<T>(s.hyper(), gbar, p, m);
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
     const int R = s.n_replicas();
     const int rdt = s.rdt();
-    for (int r = 0; r < R; ++r) store_replica<VEC, TAIL>(s.replica(r), rdt, e0, cnt, p);
+    for (int r = 0; r < R; ++r) {
+        void* rp = s.replica(r);
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(p, q));
+    }
+}
+
+template <typename GT, int W, int G, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt) {
+    const int64_t e[1] = {e0};
+    fused_tile_ct<GT, W, G, 1, TAIL>(s, e, cnt);
 }
 
 // Fused step on one unit, runtime W and G (any equal-size grouping).
@@ -408,16 +476,19 @@ struct FlatSrc {
 // (n % VEC elements) is handled by thread 0 of block 0 after its loop.
 // The unit index space is [0, full] with unit `full` the ragged tail
 // (n % VEC elements, present only when that is nonzero).
-template <typename GT, int W, int G>
+template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrc s{a};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
-    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
-        else fused_unit_ct<GT, W, G, true>(s, u * VEC, rem);
-    });
+    for_tiles<U, VEC>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { fused_tile_ct<GT, W, G, U, false>(s, e0, VEC); },
+        [&](int64_t u) {
+            if (u < full) fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
+            else fused_unit_ct<GT, W, G, true>(s, u * VEC, rem);
+        });
 }
 
 template <typename GT>
@@ -542,7 +613,7 @@ struct PlanSrc {
 // One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
 // (one large piece, or several small tensors). Chunk and pointer-table reads
 // are uniform per workgroup.
-template <typename GT, int W, int G>
+template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
@@ -552,9 +623,22 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
         const PlanChunk ch = a.chunks[c];
         const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a};
         const int64_t full = ch.len / VEC;
-        for (int64_t u = threadIdx.x; u < full; u += kBlock) {
-            if constexpr (W > 0) fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
-            else fused_unit_rt<GT, false>(s, a.W, a.n_groups, ch.start + u * VEC, VEC);
+        if constexpr (W > 0) {
+            // tiles of U units kBlock apart, then the units of a partial last tile
+            for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+                if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                    int64_t e0[U];
+#pragma unroll
+                    for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                    fused_tile_ct<GT, W, G, U, false>(s, e0, VEC);
+                } else {
+                    for (int64_t u = t0; u < full; u += kBlock)
+                        fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
+                }
+            }
+        } else {
+            for (int64_t u = threadIdx.x; u < full; u += kBlock)
+                fused_unit_rt<GT, false>(s, a.W, a.n_groups, ch.start + u * VEC, VEC);
         }
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0) {

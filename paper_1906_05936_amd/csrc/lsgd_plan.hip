@@ -36,12 +36,12 @@ using PlanKernel = void (*)(PlanArgs);
 template <typename GT, int W>
 PlanKernel pick_plan_g(int G) {
     switch (G) {
-        case 1: return step_plan_kernel<GT, W, 1>;
-        case 2: return step_plan_kernel<GT, W, 2>;
-        case 4: return step_plan_kernel<GT, W, 4>;
-        case 8: return step_plan_kernel<GT, W, 8>;
+        case 1: return step_plan_kernel<GT, W, 1, TileUnits<GT>::U>;
+        case 2: return step_plan_kernel<GT, W, 2, TileUnits<GT>::U>;
+        case 4: return step_plan_kernel<GT, W, 4, TileUnits<GT>::U>;
+        case 8: return step_plan_kernel<GT, W, 8, TileUnits<GT>::U>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16>;
+            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16, TileUnits<GT>::U>;
             else return nullptr;
     }
     return nullptr;
@@ -57,7 +57,7 @@ PlanKernel pick_plan(int W, int G) {
         case 8: k = pick_plan_g<GT, 8>(G); break;
         case 16: k = pick_plan_g<GT, 16>(G); break;
     }
-    return k ? k : step_plan_kernel<GT, 0, 0>;
+    return k ? k : step_plan_kernel<GT, 0, 0, 1>;
 }
 
 void free_plan(lsgd_plan* p) {

@@ -207,8 +207,8 @@ def test_launch_shape_setter():
     get = lambda: lib.lsgd_get_launch_shape(ctypes.byref(c), ctypes.byref(b), ctypes.byref(u))
     assert get() == OK
     default = (c.value, b.value, u.value)
-    assert default == (256, 0, 1)
-    assert lib.lsgd_set_launch_shape(-1, 0, 1) == SIZE
+    assert default == (-1, 0, 1)
+    assert lib.lsgd_set_launch_shape(-2, 0, 1) == SIZE
     assert lib.lsgd_set_launch_shape(0, 5000, 1) == SIZE
     assert lib.lsgd_set_launch_shape(70000, 0, 1) == SIZE
     assert lib.lsgd_set_launch_shape(0, 0, 0) == SIZE

@@ -396,8 +396,8 @@ def test_workload_full_size_sampled(name):
 def test_results_independent_of_launch_shape():
     """Every launch shape (XCD chunking, grid-stride caps, units per lane) gives
     the same bits: each element is computed by one lane from its own inputs."""
-    shapes = [(16, 0, 1), (0, 0, 1), (256, 0, 1), (0, 8, 1), (16, 0, 4), (4, 2, 8), (0, 1, 1),
-              (1, 0, 3)]
+    shapes = [(-1, 0, 1), (0, 0, 1), (256, 0, 1), (0, 8, 1), (16, 0, 4), (4, 2, 8), (0, 1, 1),
+              (1, 0, 3), (64, 0, 1)]
     default = lsgd.get_launch_shape()
     try:
         for gdt, G, W, n in [("f32", 4, 4, 1_000_003), ("bf16", 8, 8, 400_009), ("f32", 3, 5, 77_777)]:
