@@ -97,7 +97,8 @@ LSGD_API const char* lsgd_last_error(void);
  * Launch shape of the planless kernels, process-wide (a tuning knob; results
  * are bit-identical for every shape, because each element is computed by one
  * lane from its own inputs in a fixed order). Plans launch one workgroup per
- * bucket and ignore it.
+ * bucket: xcd_chunk applies at each lsgd_step_plan, units_per_lane at
+ * lsgd_plan_create, blocks_per_cu not at all.
  *   xcd_chunk       0 = workgroups in hardware order; C > 0 = each of the eight
  *                   XCDs runs C consecutive logical workgroups per turn (the grid
  *                   is padded to a multiple of 8*C; not applied to grids smaller
@@ -107,7 +108,8 @@ LSGD_API const char* lsgd_last_error(void);
  *                   compute unit, grid-stride. Range [0, 4096].
  *   units_per_lane  P: a workgroup walks P consecutive passes of its lane tiles
  *                   (256 lanes, each a tile of one or two 16-byte units) of
- *                   every buffer. Range [1, 256].
+ *                   every buffer; plans created while P is set cut tensors into
+ *                   pieces of P passes. Range [1, 256].
  * Defaults: xcd_chunk LSGD_XCD_CHUNK_AUTO, blocks_per_cu 0, units_per_lane 1.
  * Takes effect for
  * launches made after the call returns. Errors: LSGD_ERR_SIZE (out of range),
@@ -174,8 +176,9 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
  * Multi-tensor plan: the fused step over a model's list of parameter tensors
  * (e.g. the 161 tensors of ResNet-50, the model of Sec. 5.3) in ONE kernel
  * launch. The plan copies a chunk table and a pointer table to device memory
- * once; lsgd_step_plan then launches one kernel. Small tensors are bucketed so
- * that one workgroup covers several of them.
+ * once; lsgd_step_plan then launches one kernel. Tensors are cut into pieces
+ * of 2048 elements (times the launch shape's units_per_lane at creation);
+ * small tensors are bucketed so that one workgroup covers several of them.
  *   numel     [n_tensors] host int64, elements of each tensor (>= 0).
  *   params, momentum [n_tensors] device pointers (binary32).
  *   grads     [n_workers * n_tensors] device pointers, worker-major:

@@ -98,11 +98,10 @@ int device_cus() {
     return c;
 }
 
-namespace {
 // `blocks` logical workgroups padded to a multiple of 8 * xcd_chunk (the chunk
 // is dropped for grids smaller than one full turn of the eight XCDs). The
 // automatic chunk gives each XCD kAutoChunkBytes of every buffer per turn:
-// a workgroup pass covers kBlock lanes * tile units * 16 bytes.
+// a workgroup covers `block_bytes` of each buffer.
 LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
     LaunchShape ls;
     int64_t need = blocks < 1 ? 1 : blocks;
@@ -122,7 +121,8 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
     ls.upl = 1;
     return ls;
 }
-}  // namespace
+
+int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_order_relaxed); }
 
 LaunchShape launch_shape(int64_t units, int tile) {
     const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);

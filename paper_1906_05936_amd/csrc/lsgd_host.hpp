@@ -58,6 +58,14 @@ struct LaunchShape {
 // for the XCD chunking.
 LaunchShape launch_shape(int64_t units, int tile = 1);
 
+// The launch shape's passes per workgroup (units_per_lane).
+int32_t launch_passes_per_block();
+
+// Grid of exactly `blocks` logical workgroups, each covering `block_bytes` of
+// every buffer, padded for the XCD chunking (kernels skip logical blocks
+// >= `blocks`).
+LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes);
+
 // Compute units of the current device (cached per device).
 int device_cus();
 

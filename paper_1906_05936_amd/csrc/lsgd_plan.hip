@@ -1,11 +1,15 @@
 // Multi-tensor plans of liblsgd: the fused step over a list of parameter
 // tensors (a model's per-layer tensors) in one kernel launch.
 //
-// lsgd_plan_create cuts every tensor into pieces of at most kPiece elements
-// (starting at multiples of the 16-byte unit), then packs consecutive pieces
-// into buckets of at most kPiece elements: a large tensor yields one bucket per
-// piece, while runs of small tensors (ResNet-50's 64..4096-element batch-norm
-// and bias vectors) share a bucket. One workgroup runs one bucket.
+// lsgd_plan_create cuts every tensor into pieces of P workgroup tile passes
+// (256 lanes x the kernel's lane tile: 2048 elements for binary32 and bf16
+// gradients alike, times P = the launch shape's passes per workgroup at plan
+// creation, 1 by default), starting on unit boundaries, then packs consecutive pieces
+// into buckets of at most one piece: a large tensor yields one bucket per piece
+// (so it is walked exactly like the flat kernel walks a vector), while runs of
+// small tensors (ResNet-50's 64..1024-element batch-norm and bias vectors)
+// share a bucket. One workgroup runs one bucket; buckets are taken in the
+// XCD-chunked order of the launch shape.
 #include <string.h>
 
 #include <algorithm>
@@ -18,6 +22,7 @@ struct lsgd_plan {
     int32_t n_tensors, n_workers, n_groups, W, n_replicas;
     lsgd_dtype gdt, rdt;
     int32_t n_buckets, n_chunks, stride;
+    int64_t piece;  // elements per piece and per bucket
     lsgd::PlanChunk* d_chunks;
     int32_t* d_bucket_begin;
     void** d_ptrs;
@@ -26,10 +31,11 @@ struct lsgd_plan {
 namespace lsgd {
 namespace {
 
-// Elements per piece and per bucket: 8 units of 16 bytes per thread for
-// binary32 gradients.
-constexpr int64_t kPiece = 8192;
-constexpr int64_t kUnitAlign = 8;  // piece starts are multiples of 8 elements (16 B of bf16)
+// Elements per piece and per bucket: one tile pass of the compile-time kernel.
+template <typename GT>
+constexpr int64_t piece_elems() { return static_cast<int64_t>(kBlock) * Unit<GT>::VEC * TileUnits<GT>::U; }
+static_assert(piece_elems<float>() % 8 == 0 && piece_elems<uint16_t>() % 8 == 0,
+              "pieces must start on unit boundaries");
 
 using PlanKernel = void (*)(PlanArgs);
 
@@ -100,6 +106,9 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     std::vector<Range> ranges;
     std::vector<PlanChunk> chunks;
     std::vector<int32_t> bucket_begin;
+    // one tile pass of the kernel, times the launch shape's passes per workgroup
+    const int64_t kPiece = (gdt == LSGD_BF16 ? piece_elems<uint16_t>() : piece_elems<float>()) *
+                           launch_passes_per_block();
     int64_t bucket_fill = kPiece;  // forces a new bucket at the first piece
     for (int32_t t = 0; t < n_tensors; ++t) {
         const int64_t ne = numel[t];
@@ -134,8 +143,7 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
                 bucket_begin.push_back(static_cast<int32_t>(chunks.size()));
                 bucket_fill = 0;
             }
-            // every piece but a tensor's last has len == kPiece (a multiple of kUnitAlign)
-            static_assert(kPiece % kUnitAlign == 0, "pieces must start on unit boundaries");
+            // every piece but a tensor's last has len == kPiece (a multiple of the unit)
             chunks.push_back(PlanChunk{t, 0, s0, len});
             bucket_fill += len;
         }
@@ -160,6 +168,7 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     p->n_chunks = static_cast<int32_t>(chunks.size());
     p->n_buckets = static_cast<int32_t>(bucket_begin.size()) - 1;
     p->stride = stride;
+    p->piece = kPiece;
     hipError_t e = hipSuccess;
     const size_t chunk_bytes = std::max<size_t>(1, chunks.size()) * sizeof(PlanChunk);
     const size_t bucket_bytes = bucket_begin.size() * sizeof(int32_t);
@@ -200,12 +209,12 @@ LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momen
     a.rdt = static_cast<int32_t>(plan->rdt);
     a.h = Hyper{lr, momentum_coef, weight_decay};
     a.n_buckets = plan->n_buckets;
-    // One workgroup per bucket in hardware order: a bucket already walks up to
-    // 32 KB of each buffer, and measurements favoured no XCD renumbering here.
-    a.xcd_chunk = 0;
+    const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
+    const LaunchShape ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
+    a.xcd_chunk = ls.xcd_chunk;
     PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups)
                                           : pick_plan<float>(plan->W, plan->n_groups);
-    hipLaunchKernelGGL(k, dim3(plan->n_buckets), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_step_plan");
 }
 

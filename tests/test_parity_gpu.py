@@ -433,3 +433,76 @@ def test_stream_copy_is_exact(nbytes):
     lsgd.stream_copy(dst, src)
     torch.cuda.synchronize()
     assert torch.equal(dst, src)
+
+
+def test_resume_from_host_copy_is_bit_exact():
+    """The optimizer state is (params, momentum): copying it to host memory and
+    back into fresh buffers mid-run continues bit for bit."""
+    rng = np.random.default_rng(21)
+    n, G, W = 200_003, 4, 4
+    gow = groups_for(G, W, "shuffled", seed=2)
+    steps = [[to_dev(rand_host(rng, n, 1e-2, "f32")) for _ in range(G * W)] for _ in range(6)]
+    p0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+    p, m = p0.clone(), torch.zeros(n, device=DEV)
+    for g in steps:
+        lsgd.step(p, m, g, gow, G, 0.1, 0.9, 1e-4)
+    q, v = p0.clone(), torch.zeros(n, device=DEV)
+    for g in steps[:3]:
+        lsgd.step(q, v, g, gow, G, 0.1, 0.9, 1e-4)
+    host_p, host_m = to_host(q).copy(), to_host(v).copy()
+    del q, v
+    q, v = to_dev(host_p), to_dev(host_m)
+    for g in steps[3:]:
+        lsgd.step(q, v, g, gow, G, 0.1, 0.9, 1e-4)
+    assert torch.equal(p, q) and torch.equal(m, v)
+
+
+def test_graph_capture_replays_match_eager():
+    """lsgd_step and lsgd_step_plan captured in a HIP graph: every replay (with
+    eager work and synchronizations in between) gives the eager bits."""
+    rng = np.random.default_rng(22)
+    n, G, W = 100_003, 2, 4
+    gow = groups_for(G, W, "shuffled", seed=3)
+    grads = [to_dev(rand_host(rng, n, 1e-2, "f32")) for _ in range(G * W)]
+    p0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+    sizes = [1000, 4096, 3, 70_000]
+    pt0 = [to_dev((rng.standard_normal(s) * 0.05).astype(np.float32)) for s in sizes]
+    gt = [[to_dev(rand_host(rng, s, 1e-2, "f32")) for s in sizes] for _ in range(G * W)]
+
+    # eager reference: three steps
+    pe, me = p0.clone(), torch.zeros(n, device=DEV)
+    re = [torch.empty(n, device=DEV) for _ in range(2)]
+    pte, mte = [x.clone() for x in pt0], [torch.zeros_like(x) for x in pt0]
+    plan_e = lsgd.Plan(pte, mte, gt, gow, G)
+    eager = []
+    for _ in range(3):
+        lsgd.step(pe, me, grads, gow, G, 0.1, 0.9, 1e-4, re)
+        plan_e.step(0.1, 0.9, 1e-4)
+        torch.cuda.synchronize()
+        eager.append((pe.clone(), me.clone(), re[1].clone(), [x.clone() for x in pte]))
+    plan_e.close()
+
+    pg, mg = p0.clone(), torch.zeros(n, device=DEV)
+    rg = [torch.empty(n, device=DEV) for _ in range(2)]
+    ptg, mtg = [x.clone() for x in pt0], [torch.zeros_like(x) for x in pt0]
+    plan_g = lsgd.Plan(ptg, mtg, gt, gow, G)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            lsgd.step(pg, mg, grads, gow, G, 0.1, 0.9, 1e-4, rg, stream=s)
+            plan_g.step(0.1, 0.9, 1e-4, stream=s)
+    torch.cuda.synchronize()
+    # capture does not execute: state is still the initial one
+    assert torch.equal(pg, p0)
+    for k in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        _ = (torch.ones(1000, device=DEV) * 2).sum().item()   # eager work between replays
+        assert torch.equal(pg, eager[k][0]) and torch.equal(mg, eager[k][1]), k
+        assert torch.equal(rg[1], eager[k][2]), k
+        for a, b in zip(ptg, eager[k][3]):
+            assert torch.equal(a, b), k
+    del graph
+    plan_g.close()
