@@ -50,6 +50,11 @@ def _load():
         lib.oracle_bf16_to_f32.restype = ctypes.c_float
         lib.oracle_f32_to_bf16_array.argtypes = [P, P, i64]
         lib.oracle_bf16_to_f32_array.argtypes = [P, P, i64]
+        lib.oracle_partition.argtypes = [i32, P, i32, P, P]
+        lib.oracle_partition.restype = c_int
+        lib.oracle_lr_at.argtypes = [i64, ctypes.c_double, ctypes.c_double, ctypes.c_double, i64, i64,
+                                     ctypes.c_double]
+        lib.oracle_lr_at.restype = ctypes.c_float
         for sfx, real in (("_f32", ctypes.c_float), ("_f64", ctypes.c_double)):
             f = getattr(lib, "oracle_pairwise" + sfx)
             f.argtypes, f.restype = [P, i32], real
@@ -61,6 +66,9 @@ def _load():
             f.argtypes, f.restype = [P, P, P, i64, real, real, real, P, i32, c_int], c_int
             f = getattr(lib, "oracle_lsgd_step" + sfx)
             f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int]
+            f.restype = c_int
+            f = getattr(lib, "oracle_lsgd_step_literal" + sfx)
+            f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int, c_int]
             f.restype = c_int
         _lib = lib
     return _lib
@@ -185,3 +193,36 @@ def lsgd_step(p, mom, grads, group_of_worker, n_groups, lr, mu, wd, replicas=(),
         _ptr(gow), n_groups, p.size, lr, mu, wd,
         _ptr_array(list(replicas)) if replicas else None, len(replicas), rdt)
     _check(st, "lsgd_step")
+
+
+def partition(group_of_worker, n_groups):
+    """(members, group_start) of any partition into non-empty groups."""
+    lib = _load()
+    gow = np.ascontiguousarray(group_of_worker, dtype=np.int32)
+    members = np.zeros(max(1, gow.size), dtype=np.int32)
+    start = np.zeros(max(1, n_groups + 1), dtype=np.int32)
+    _check(lib.oracle_partition(gow.size, _ptr(gow), n_groups, _ptr(members), _ptr(start)), "partition")
+    return members[: gow.size], start[: n_groups + 1]
+
+
+def lr_at(t, base_lr, base_batch, global_batch, warmup_iters, decay_iters, decay_factor):
+    """Learning rate of iteration t (linear scaling, warmup, step decay)."""
+    return _load().oracle_lr_at(int(t), base_lr, base_batch, global_batch, int(warmup_iters),
+                                int(decay_iters), decay_factor)
+
+
+def lsgd_step_literal(p, mom, grads, group_of_worker, n_groups, lr, mu, wd, replicas=(), rdt=F32,
+                      broadcast_grad=False):
+    """Paper-literal step (each group's sum / N, then summed) in place; any
+    partition into non-empty groups. With broadcast_grad every gradient array
+    (float32) receives the mean gradient in place."""
+    lib = _load()
+    assert p.flags.c_contiguous and mom.flags.c_contiguous and mom.dtype == p.dtype
+    for g in grads:
+        assert g.flags.c_contiguous and g.size == p.size
+    gow = np.ascontiguousarray(group_of_worker, dtype=np.int32)
+    st = getattr(lib, "oracle_lsgd_step_literal" + _sfx(p.dtype))(
+        _ptr(p), _ptr(mom), _ptr_array(list(grads)), _gdt(grads), len(grads), _ptr(gow), n_groups,
+        p.size, lr, mu, wd, _ptr_array(list(replicas)) if replicas else None, len(replicas), rdt,
+        1 if broadcast_grad else 0)
+    _check(st, "lsgd_step_literal")

@@ -107,6 +107,55 @@ uint16_t oracle_f32_to_bf16(float f)
     return (uint16_t)kept;
 }
 
+/*
+ * Subgroup indexing for the paper-literal reduction, which admits any
+ * partition: every group needs at least one member. members holds the N
+ * worker ids grouped by group id (ascending inside each group) and
+ * group_start[j] .. group_start[j+1] delimits group j (G+1 entries).
+ */
+int oracle_partition(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
+                     int32_t* members, int32_t* group_start)
+{
+    if (!group_of_worker || !members || !group_start) return ORACLE_ERR_NULL;
+    if (n_workers < 1 || n_groups < 1) return ORACLE_ERR_SIZE;
+    for (int32_t i = 0; i < n_workers; ++i)
+        if (group_of_worker[i] < 0 || group_of_worker[i] >= n_groups) return ORACLE_ERR_GROUPS;
+    int32_t at = 0;
+    for (int32_t j = 0; j < n_groups; ++j) {
+        group_start[j] = at;
+        for (int32_t i = 0; i < n_workers; ++i)
+            if (group_of_worker[i] == j) members[at++] = i;
+        if (at == group_start[j]) return ORACLE_ERR_GROUPS;   /* empty group */
+    }
+    group_start[n_groups] = at;
+    return ORACLE_OK;
+}
+
+/*
+ * Learning-rate schedule of Sec. 5.3: the linear scaling rule (the rate grows
+ * with the global minibatch: base_lr at base_batch, so the target is
+ * base_lr * global_batch / base_batch), a warmup that raises the rate from
+ * base_lr to the target linearly at every iteration over warmup_iters
+ * iterations, and a decay by decay_factor every decay_iters iterations
+ * (every 30 epochs in the paper). Computed in binary64, rounded to binary32
+ * once at the end; the decay power is a product of decay_factor terms.
+ */
+float oracle_lr_at(int64_t t, double base_lr, double base_batch, double global_batch,
+                   int64_t warmup_iters, int64_t decay_iters, double decay_factor)
+{
+    double target = base_lr * (global_batch / base_batch);
+    double lr = target;
+    if (warmup_iters > 0 && t < warmup_iters)
+        lr = base_lr + (target - base_lr) * ((double)t / (double)warmup_iters);
+    if (decay_iters > 0) {
+        int64_t k = t / decay_iters;
+        double f = 1.0;
+        for (int64_t i = 0; i < k; ++i) f = f * decay_factor;
+        lr = lr * f;
+    }
+    return (float)lr;
+}
+
 #define REAL float
 #define SFX(name) name##_f32
 #include "oracle_real.inc"

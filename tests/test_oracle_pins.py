@@ -440,3 +440,132 @@ def test_workload_shapes():
             assert sum(wl.tensor_sizes) == wl.n
     big = workloads.WORKLOADS["large"]
     assert big.n_workers == 64 and big.algorithmic_bytes(0) == big.n * (64 * 2 + 16)
+
+
+# ---------------------------------------------------------------- paper-literal reduction
+
+@pytest.mark.parametrize("G,W,gdt", [(2, 2, "f32"), (4, 4, "f32"), (16, 8, "f32"), (8, 8, "bf16"),
+                                     (1, 16, "f32")])
+def test_literal_reduction_equals_mean_of_means_for_powers_of_two(G, W, gdt):
+    """Alg. 3 as printed (each communicator divides its sum by N, the allreduce
+    sums) and the mean of subgroup means agree bit for bit when W and G are
+    powers of two: dividing by 2^k commutes with rounding."""
+    rng = np.random.default_rng(300 + G * W)
+    n = 1200
+    grads = rand_grads(rng, G * W, n)
+    if gdt == "bf16":
+        grads = [oracle.f32_to_bf16(g) for g in grads]
+    gow = workloads.shuffled_groups(G, W, seed=G + W)
+    p = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m = (rng.standard_normal(n) * 0.01).astype(np.float32)
+    a = run_step(p, m, grads, gow, G, 0.1, 0.9, 1e-4)
+    pl, ml = p.copy(), m.copy()
+    oracle.lsgd_step_literal(pl, ml, grads, gow, G, 0.1, 0.9, 1e-4)
+    assert pl.tobytes() == a[0].tobytes() and ml.tobytes() == a[1].tobytes()
+
+
+def _literal_bound_check(grads, gow, G, gbar_out):
+    """The literal reduction of any partition has the flat mean sum(g)/N as its
+    exact value (sum_j (S_j / N) = S / N): check the binary32 result against it
+    within the forward error bound of the per-group pairwise sums, the
+    divisions and the pairwise sum over groups."""
+    N = len(grads)
+    members, start = oracle.partition(gow, G)
+    for i in range(gbar_out.size):
+        exact = sum(_exact(g[i]) for g in grads) / N
+        err = 0.0
+        parts_abs = 0.0
+        for j in range(G):
+            xs = [_exact(grads[w][i]) for w in members[start[j]:start[j + 1]]]
+            k = len(xs)
+            h = math.ceil(math.log2(k)) if k > 1 else 0
+            s_err = h * U / (1 - h * U) * float(sum(abs(x) for x in xs))
+            c = sum(xs) / N
+            c_err = _bounded_op(c, s_err / N)
+            err += c_err
+            parts_abs += abs(float(c)) + c_err
+        hg = math.ceil(math.log2(G)) if G > 1 else 0
+        err += hg * U / (1 - hg * U) * parts_abs
+        assert abs(_exact(gbar_out[i]) - exact) <= Fraction(err * (1 + 16 * U)), i
+
+
+@pytest.mark.parametrize("gow,G", [([0, 1, 1, 1], 2), ([0, 0, 1, 2, 2, 2, 2], 3),
+                                   ([2, 0, 1, 1, 2, 0, 0, 0, 1], 3), ([0] * 5 + [1], 2),
+                                   (list(range(5)), 5)])
+def test_literal_reduction_of_unequal_groups_is_the_flat_mean(gow, G):
+    """Any partition, even with unequal subgroups, reaches the conventional
+    mean of Alg. 2 (Sec. 4.2: Algorithms 1-3 compute the same SGD)."""
+    rng = np.random.default_rng(len(gow) * 7 + G)
+    n = 8
+    grads = rand_grads(rng, len(gow), n)
+    work = [g.copy() for g in grads]
+    p = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m = np.zeros(n, np.float32)
+    oracle.lsgd_step_literal(p, m, work, gow, G, 0.1, 0.9, 1e-4, broadcast_grad=True)
+    for w in work[1:]:
+        assert w.tobytes() == work[0].tobytes()        # every worker received the same mean
+    _literal_bound_check(grads, gow, G, work[0])
+
+
+def test_literal_reduction_single_group_is_alg2():
+    """G = 1: the communicator sums all N and divides by N, exactly the
+    mean-of-means oracle with one group."""
+    rng = np.random.default_rng(41)
+    grads = rand_grads(rng, 6, 500)
+    p = (rng.standard_normal(500) * 0.05).astype(np.float32)
+    a = run_step(p, np.zeros(500, np.float32), grads, [0] * 6, 1, 0.1, 0.9, 1e-4)
+    pl, ml = p.copy(), np.zeros(500, np.float32)
+    oracle.lsgd_step_literal(pl, ml, grads, [0] * 6, 1, 0.1, 0.9, 1e-4)
+    assert pl.tobytes() == a[0].tobytes() and ml.tobytes() == a[1].tobytes()
+
+
+def test_gradient_broadcast_delivers_the_global_mean():
+    """Broadcast of the gathered gradient (Sec. 4.1, item 3): afterwards every
+    worker's buffer holds the mean gradient, bitwise equal to the global mean of
+    the group means for power-of-two groups."""
+    rng = np.random.default_rng(42)
+    G, W, n = 4, 4, 3000
+    grads = rand_grads(rng, G * W, n)
+    gow = workloads.contiguous_groups(G, W)
+    want = oracle.global_mean(oracle.group_means(grads, gow, G))
+    work = [g.copy() for g in grads]
+    p = np.zeros(n, np.float32)
+    oracle.lsgd_step_literal(p, np.zeros(n, np.float32), work, gow, G, 0.1, 0.9, 1e-4,
+                             broadcast_grad=True)
+    for w in work:
+        assert w.tobytes() == want.tobytes()
+
+
+@pytest.mark.parametrize("gow,G", [([0, 0, 2, 2], 3), ([0, 1, 3], 3), ([-1, 0], 1)])
+def test_partition_rejects_empty_groups_and_bad_ids(gow, G):
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.partition(gow, G)
+    assert e.value.status == oracle.ERR_GROUPS
+
+
+# ---------------------------------------------------------------- learning-rate schedule
+
+def test_lr_schedule_matches_the_paper():
+    with open(os.path.join(GOLDEN, "lr_schedule.json")) as f:
+        gold = json.load(f)
+    ipe = gold["iters_per_epoch"]
+    args = (gold["base_lr"], gold["base_batch"], gold["global_batch"], gold["warmup_epochs"] * ipe,
+            gold["decay_epochs"] * ipe, gold["decay_factor"])
+    for pt in gold["points"]:
+        t = pt["epoch_iter"][0] * ipe + pt["epoch_iter"][1]
+        got = oracle.lr_at(t, *args)
+        assert abs(got - pt["lr"]) <= 2e-7 * pt["lr"] + 1e-12, (t, got, pt["lr"])
+
+
+def test_lr_schedule_shape():
+    """Linear warmup (equal per-iteration increments), constant plateau, then
+    a tenfold drop at every decay boundary."""
+    a = (0.1, 256.0, 16384.0, 390, 2340, 0.1)
+    w = np.array([oracle.lr_at(t, *a) for t in range(391)], np.float64)
+    inc = np.diff(w[:390])
+    assert np.allclose(inc, (6.4 - 0.1) / 390, rtol=1e-4)
+    assert all(oracle.lr_at(t, *a) == np.float32(6.4) for t in (390, 1000, 2339))
+    assert oracle.lr_at(2340, *a) == np.float32(0.64)
+    assert oracle.lr_at(4680, *a) == np.float32(6.4 * 0.1 * 0.1)
+    # no warmup, no decay: the linearly scaled rate
+    assert oracle.lr_at(10 ** 9, 0.1, 256.0, 1024.0, 0, 0, 0.1) == np.float32(0.4)
