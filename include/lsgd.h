@@ -72,7 +72,8 @@ typedef enum lsgd_status {
     LSGD_ERR_ALIGN = 4,  /* a buffer is not 16-byte aligned                            */
     LSGD_ERR_DTYPE = 5,  /* dtype is not one of lsgd_dtype                             */
     LSGD_ERR_HIP = 6,    /* the HIP runtime reported an error; see lsgd_last_error()   */
-    LSGD_ERR_ALIAS = 7   /* a written buffer overlaps another buffer of the call       */
+    LSGD_ERR_ALIAS = 7,  /* a written buffer overlaps another buffer of the call       */
+    LSGD_ERR_UNSUPPORTED = 8 /* an option value or combination this call does not take */
 } lsgd_status;
 
 typedef enum lsgd_dtype {
@@ -173,6 +174,84 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
                                void* stream);
 
 /*
+ * Variants of the fused step: the paper-literal form of the local layer, the
+ * broadcast of the mean gradient, and a learning rate held in device memory.
+ *
+ * reduction
+ *   LSGD_REDUCE_MEAN_OF_MEANS  as lsgd_step: equal subgroups, mean of each
+ *                              group's W members, then mean of the G means.
+ *   LSGD_REDUCE_LITERAL        Alg. 3 as printed: each communicator divides its
+ *                              members' pairwise sum by N (all workers), the
+ *                              allreduce over communicators sums (PW, ascending
+ *                              group id) without a further division. Any
+ *                              partition into non-empty groups (LSGD_ERR_GROUPS
+ *                              for an empty group); the exact value is the flat
+ *                              mean of Alg. 2 for every partition, and for equal
+ *                              power-of-two groups the bits equal lsgd_step's.
+ * broadcast_grad
+ *   nonzero: every worker's gradient buffer receives the mean gradient in
+ *   place (Alg. 3 Broadcast of the gathered gradient, Sec. 4.1 item 3: what the
+ *   allreduce-and-divide of Alg. 2 leaves in each worker). binary32 gradients
+ *   only (LSGD_ERR_DTYPE); the gradient buffers are then written buffers and may
+ *   not overlap each other or any other buffer (LSGD_ERR_ALIAS).
+ * lr_device
+ *   non-NULL: the learning rate is read from this device address (4-byte
+ *   aligned, LSGD_ERR_ALIGN) when the kernel runs, and the lr argument is
+ *   ignored; with lsgd_lr_schedule_step in the same stream a captured HIP graph
+ *   of whole steps follows the schedule on every replay.
+ * A zero-initialised struct (or options == NULL) is lsgd_step.
+ */
+typedef enum lsgd_reduction {
+    LSGD_REDUCE_MEAN_OF_MEANS = 0,
+    LSGD_REDUCE_LITERAL = 1
+} lsgd_reduction;
+
+typedef struct lsgd_step_options {
+    int32_t reduction;       /* lsgd_reduction                                  */
+    int32_t broadcast_grad;  /* nonzero: write the mean gradient into every grad */
+    const float* lr_device;  /* NULL: use the lr argument                       */
+} lsgd_step_options;
+
+LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* grads,
+                                  lsgd_dtype gdt, int32_t n_workers,
+                                  const int32_t* group_of_worker, int32_t n_groups, int64_t n,
+                                  float lr, float momentum_coef, float weight_decay,
+                                  void* const* replicas, int32_t n_replicas, lsgd_dtype rdt,
+                                  const lsgd_step_options* options, void* stream);
+
+/*
+ * Learning-rate schedule of Sec. 5.3: linear scaling (the target rate is
+ * base_lr * global_batch / base_batch: 0.1 at 256, 6.4 at 16,384 in the paper),
+ * a linear warmup from base_lr to the target over warmup_iters iterations
+ * (0 = none), and a multiplication by decay_factor every decay_iters
+ * iterations counted from the start (0 = never; 0.1 every 30 epochs in the
+ * paper). Evaluated in binary64 and rounded to binary32 once:
+ *   lr(t) = (t < warmup_iters ? base_lr + (target - base_lr) * (t / warmup_iters)
+ *                             : target) * decay_factor^(t / decay_iters)
+ * with the power taken as a running product of decay_factor terms.
+ */
+typedef struct lsgd_lr_schedule {
+    double base_lr;
+    double base_batch;
+    double global_batch;
+    int64_t warmup_iters;
+    int64_t decay_iters;
+    double decay_factor;
+} lsgd_lr_schedule;
+
+/* The schedule's rate for iteration t, on the host (same operations and bits as
+ * the device step). Returns NaN for a NULL schedule, base_batch <= 0, or
+ * negative t, warmup_iters or decay_iters. */
+LSGD_API float lsgd_lr_at(const lsgd_lr_schedule* schedule, int64_t t);
+
+/* Device-side schedule step, stream-ordered: lr_out[0] = lr(iteration[0]), then
+ * iteration[0] += 1. iteration: device int64 (8-byte aligned), lr_out: device
+ * float (4-byte aligned). The schedule struct is copied at the call. Errors:
+ * LSGD_ERR_NULL, LSGD_ERR_ALIGN, LSGD_ERR_SIZE (invalid schedule fields). */
+LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int64_t* iteration,
+                                           float* lr_out, void* stream);
+
+/*
  * Multi-tensor plan: the fused step over a model's list of parameter tensors
  * (e.g. the 161 tensors of ResNet-50, the model of Sec. 5.3) in ONE kernel
  * launch. The plan copies a chunk table and a pointer table to device memory
@@ -203,6 +282,12 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
 
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                     float weight_decay, void* stream);
+
+/* lsgd_step_plan with options: only lr_device is taken (reduction must be
+ * LSGD_REDUCE_MEAN_OF_MEANS and broadcast_grad zero, else LSGD_ERR_UNSUPPORTED). */
+LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float momentum_coef,
+                                       float weight_decay, const lsgd_step_options* options,
+                                       void* stream);
 
 /* Frees the plan's device tables. NULL-safe. The caller synchronizes every
  * stream that ran lsgd_step_plan with this plan first. */

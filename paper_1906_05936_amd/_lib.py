@@ -21,12 +21,29 @@ MAX_WORKERS = 128
 MAX_REPLICAS = 128
 
 STATUS_NAMES = {0: "LSGD_OK", 1: "LSGD_ERR_NULL", 2: "LSGD_ERR_SIZE", 3: "LSGD_ERR_GROUPS",
-                4: "LSGD_ERR_ALIGN", 5: "LSGD_ERR_DTYPE", 6: "LSGD_ERR_HIP", 7: "LSGD_ERR_ALIAS"}
+                4: "LSGD_ERR_ALIGN", 5: "LSGD_ERR_DTYPE", 6: "LSGD_ERR_HIP", 7: "LSGD_ERR_ALIAS",
+                8: "LSGD_ERR_UNSUPPORTED"}
+REDUCE_MEAN_OF_MEANS = 0
+REDUCE_LITERAL = 1
+XCD_CHUNK_AUTO = -1
 
 EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_get_launch_shape", "lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step",
-           "lsgd_step", "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
-           "lsgd_stream_copy")
+           "lsgd_step", "lsgd_step_ex", "lsgd_lr_at", "lsgd_lr_schedule_step", "lsgd_plan_create",
+           "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy")
+
+
+class StepOptions(ctypes.Structure):
+    """lsgd_step_options."""
+    _fields_ = [("reduction", ctypes.c_int32), ("broadcast_grad", ctypes.c_int32),
+                ("lr_device", ctypes.c_void_p)]
+
+
+class LrSchedule(ctypes.Structure):
+    """lsgd_lr_schedule: linear scaling, warmup, step decay (Sec. 5.3)."""
+    _fields_ = [("base_lr", ctypes.c_double), ("base_batch", ctypes.c_double),
+                ("global_batch", ctypes.c_double), ("warmup_iters", ctypes.c_int64),
+                ("decay_iters", ctypes.c_int64), ("decay_factor", ctypes.c_double)]
 
 
 class LsgdError(RuntimeError):
@@ -58,9 +75,15 @@ def _load():
     lib.lsgd_step_plan.argtypes = [P, f32, f32, f32, P]
     lib.lsgd_plan_destroy.argtypes, lib.lsgd_plan_destroy.restype = [P], None
     lib.lsgd_stream_copy.argtypes = [P, P, i64, P]
+    lib.lsgd_step_ex.argtypes = [P, P, P, c_int, i32, P, i32, i64, f32, f32, f32, P, i32, c_int,
+                                 ctypes.POINTER(StepOptions), P]
+    lib.lsgd_step_plan_ex.argtypes = [P, f32, f32, f32, ctypes.POINTER(StepOptions), P]
+    lib.lsgd_lr_at.argtypes, lib.lsgd_lr_at.restype = [ctypes.POINTER(LrSchedule), i64], f32
+    lib.lsgd_lr_schedule_step.argtypes = [ctypes.POINTER(LrSchedule), P, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
-                 "lsgd_get_launch_shape", "lsgd_stream_copy"):
+                 "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_step_plan_ex",
+                 "lsgd_lr_schedule_step"):
         getattr(lib, name).restype = c_int
     return lib
 
@@ -156,14 +179,35 @@ def stream_copy(dst, src, stream=None):
         check(lib.lsgd_stream_copy(dst.data_ptr(), src.data_ptr(), nbytes, _stream(stream, dst.device)))
 
 
+def _options(reduction, broadcast_grad, lr_device, device=None):
+    if reduction in ("mean_of_means", REDUCE_MEAN_OF_MEANS):
+        red = REDUCE_MEAN_OF_MEANS
+    elif reduction in ("literal", REDUCE_LITERAL):
+        red = REDUCE_LITERAL
+    else:
+        raise ValueError("reduction must be 'mean_of_means' or 'literal'")
+    ptr = None
+    if lr_device is not None:
+        _dev_tensor(lr_device, "lr_device", torch.float32, None, device)
+        if lr_device.numel() < 1:
+            raise ValueError("lr_device must hold one float")
+        ptr = lr_device.data_ptr()
+    return StepOptions(red, 1 if broadcast_grad else 0, ptr)
+
+
 def step(params, momentum, grads, group_of_worker, n_groups, lr, momentum_coef, weight_decay,
-         replicas=(), stream=None):
-    """lsgd_step: one fused Layered SGD step, in place on params and momentum.
+         replicas=(), stream=None, reduction="mean_of_means", broadcast_grad=False, lr_device=None):
+    """lsgd_step / lsgd_step_ex: one fused Layered SGD step, in place on params
+    and momentum.
 
     params, momentum: float32 GPU tensors of n elements. grads: N tensors of n
     elements (all float32 or all bfloat16). group_of_worker: N ints in
     [0, n_groups). replicas: R tensors of n elements (all float32 or all
-    bfloat16). Enqueued on ``stream`` (default: the current stream).
+    bfloat16). reduction: 'mean_of_means' (equal groups) or 'literal' (Alg. 3
+    as printed, any partition). broadcast_grad: write the mean gradient into
+    every gradient tensor. lr_device: a one-element float32 GPU tensor read for
+    the learning rate when the kernel runs. Enqueued on ``stream`` (default: the
+    current stream).
     """
     n = params.numel()
     dev = params.device
@@ -175,13 +219,37 @@ def step(params, momentum, grads, group_of_worker, n_groups, lr, momentum_coef, 
         _dev_tensor(r, "replica", None, n, dev)
     gdt = _common_dtype(grads, "grads")
     rdt = _common_dtype(replicas, "replicas")
+    plain = reduction in ("mean_of_means", REDUCE_MEAN_OF_MEANS) and not broadcast_grad and lr_device is None
     with torch.cuda.device(dev):
-        st = lib.lsgd_step(params.data_ptr(), momentum.data_ptr(),
-                           ptr_array([g.data_ptr() for g in grads]), gdt, len(grads),
-                           int32_array(group_of_worker), n_groups, n, lr, momentum_coef,
-                           weight_decay, ptr_array([r.data_ptr() for r in replicas]),
-                           len(replicas), rdt, _stream(stream, dev))
+        common = (params.data_ptr(), momentum.data_ptr(), ptr_array([g.data_ptr() for g in grads]), gdt,
+                  len(grads), int32_array(group_of_worker), n_groups, n, lr, momentum_coef,
+                  weight_decay, ptr_array([r.data_ptr() for r in replicas]), len(replicas), rdt)
+        if plain:
+            st = lib.lsgd_step(*common, _stream(stream, dev))
+        else:
+            opts = _options(reduction, broadcast_grad, lr_device, dev)
+            st = lib.lsgd_step_ex(*common, ctypes.byref(opts), _stream(stream, dev))
     check(st)
+
+
+def lr_schedule(base_lr, base_batch, global_batch, warmup_iters=0, decay_iters=0, decay_factor=0.1):
+    """An lsgd_lr_schedule (linear scaling, warmup, step decay of Sec. 5.3)."""
+    return LrSchedule(base_lr, base_batch, global_batch, warmup_iters, decay_iters, decay_factor)
+
+
+def lr_at(schedule, t):
+    """lsgd_lr_at: the schedule's rate for iteration t, computed on the host."""
+    return lib.lsgd_lr_at(ctypes.byref(schedule), int(t))
+
+
+def lr_schedule_step(schedule, iteration, lr_out, stream=None):
+    """lsgd_lr_schedule_step: lr_out[0] = rate of iteration[0]; iteration[0] += 1
+    (device int64 and float32 tensors), stream-ordered."""
+    _dev_tensor(iteration, "iteration", torch.int64)
+    _dev_tensor(lr_out, "lr_out", torch.float32, None, iteration.device)
+    with torch.cuda.device(iteration.device):
+        check(lib.lsgd_lr_schedule_step(ctypes.byref(schedule), iteration.data_ptr(), lr_out.data_ptr(),
+                                        _stream(stream, iteration.device)))
 
 
 def group_mean(grads, group_of_worker, n_groups, out, stream=None):
@@ -273,12 +341,18 @@ class Plan:
         check(st)
         self._handle = handle
 
-    def step(self, lr, momentum_coef, weight_decay, stream=None):
+    def step(self, lr, momentum_coef, weight_decay, stream=None, lr_device=None):
         if self._handle is None:
             raise RuntimeError("plan is closed")
         with torch.cuda.device(self.device):
-            check(lib.lsgd_step_plan(self._handle, lr, momentum_coef, weight_decay,
-                                     _stream(stream, self.device)))
+            if lr_device is None:
+                st = lib.lsgd_step_plan(self._handle, lr, momentum_coef, weight_decay,
+                                        _stream(stream, self.device))
+            else:
+                opts = _options("mean_of_means", False, lr_device, self.device)
+                st = lib.lsgd_step_plan_ex(self._handle, lr, momentum_coef, weight_decay,
+                                           ctypes.byref(opts), _stream(stream, self.device))
+        check(st)
 
     def close(self):
         if getattr(self, "_handle", None) is not None:

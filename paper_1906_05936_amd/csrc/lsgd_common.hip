@@ -65,6 +65,32 @@ lsgd_status member_order(int32_t n_workers, const int32_t* group_of_worker, int3
     return LSGD_OK;
 }
 
+lsgd_status partition_order(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
+                            std::vector<int32_t>& order, std::vector<int32_t>& group_start) {
+    if (n_workers < 1 || n_workers > kMaxWorkers)
+        return fail(LSGD_ERR_SIZE, "n_workers=%d outside [1, %d]", n_workers, kMaxWorkers);
+    if (n_groups < 1) return fail(LSGD_ERR_SIZE, "n_groups=%d < 1", n_groups);
+    if (!group_of_worker) return fail(LSGD_ERR_NULL, "group_of_worker is NULL");
+    if (n_groups > n_workers)
+        return fail(LSGD_ERR_GROUPS, "n_groups=%d > n_workers=%d leaves a group empty", n_groups, n_workers);
+    std::vector<int32_t> count(n_groups, 0);
+    for (int32_t i = 0; i < n_workers; ++i) {
+        const int32_t j = group_of_worker[i];
+        if (j < 0 || j >= n_groups)
+            return fail(LSGD_ERR_GROUPS, "group_of_worker[%d]=%d outside [0, %d)", i, j, n_groups);
+        ++count[j];
+    }
+    group_start.assign(n_groups + 1, 0);
+    for (int32_t j = 0; j < n_groups; ++j) {
+        if (count[j] == 0) return fail(LSGD_ERR_GROUPS, "group %d is empty", j);
+        group_start[j + 1] = group_start[j] + count[j];
+    }
+    order.assign(n_workers, -1);
+    std::vector<int32_t> fill(group_start.begin(), group_start.end() - 1);
+    for (int32_t i = 0; i < n_workers; ++i) order[fill[group_of_worker[i]]++] = i;
+    return LSGD_OK;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 lsgd_status check_overlap(std::vector<Range>& ranges) {
@@ -152,6 +178,7 @@ LSGD_API const char* lsgd_status_string(lsgd_status status) {
         case LSGD_ERR_DTYPE: return "LSGD_ERR_DTYPE: unsupported dtype";
         case LSGD_ERR_HIP: return "LSGD_ERR_HIP: the HIP runtime reported an error";
         case LSGD_ERR_ALIAS: return "LSGD_ERR_ALIAS: a written buffer overlaps another buffer";
+        case LSGD_ERR_UNSUPPORTED: return "LSGD_ERR_UNSUPPORTED: option not supported by this call";
     }
     return "unknown lsgd_status";
 }

@@ -50,6 +50,9 @@ FlatPick pick_flat(int W, int G) {
 
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
 
+// Name of gradient ranges in the aliasing check (compared by address).
+const char* const kGradRange = "grad";
+
 bool valid_dtype(lsgd_dtype d) { return d == LSGD_F32 || d == LSGD_BF16; }
 
 Range range_of(const void* p, int64_t n, size_t esize, bool written, const char* what) {
@@ -83,7 +86,7 @@ lsgd_status check_update_buffers(float* params, float* momentum, int64_t n, std:
     return LSGD_OK;
 }
 
-// Gradient pointers in member order (entry j*W + k) with their ranges.
+// Gradient pointers in member order with their ranges.
 lsgd_status check_grads(const void* const* grads, lsgd_dtype gdt, const std::vector<int32_t>& order,
                         int64_t n, bool check_ptrs, const void** out, std::vector<Range>& ranges) {
     if (!valid_dtype(gdt)) return fail(LSGD_ERR_DTYPE, "gradient dtype %d", static_cast<int>(gdt));
@@ -94,7 +97,7 @@ lsgd_status check_grads(const void* const* grads, lsgd_dtype gdt, const std::vec
         if (!g) return fail(LSGD_ERR_NULL, "grads[%d] is NULL", order[k]);
         if (!aligned16(g)) return fail(LSGD_ERR_ALIGN, "grads[%d] is not 16-byte aligned", order[k]);
         out[k] = g;
-        ranges.push_back(range_of(g, n, dtype_size(gdt), false, "grad"));
+        ranges.push_back(range_of(g, n, dtype_size(gdt), false, kGradRange));
     }
     return LSGD_OK;
 }
@@ -106,15 +109,24 @@ using namespace lsgd;
 
 extern "C" {
 
-LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
-                               lsgd_dtype gdt, int32_t n_workers, const int32_t* group_of_worker,
-                               int32_t n_groups, int64_t n, float lr, float momentum_coef,
-                               float weight_decay, void* const* replicas, int32_t n_replicas,
-                               lsgd_dtype rdt, void* stream) {
+LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* grads,
+                                  lsgd_dtype gdt, int32_t n_workers, const int32_t* group_of_worker,
+                                  int32_t n_groups, int64_t n, float lr, float momentum_coef,
+                                  float weight_decay, void* const* replicas, int32_t n_replicas,
+                                  lsgd_dtype rdt, const lsgd_step_options* options, void* stream) {
+    const lsgd_step_options none = {LSGD_REDUCE_MEAN_OF_MEANS, 0, nullptr};
+    const lsgd_step_options& o = options ? *options : none;
+    if (o.reduction != LSGD_REDUCE_MEAN_OF_MEANS && o.reduction != LSGD_REDUCE_LITERAL)
+        return fail(LSGD_ERR_UNSUPPORTED, "reduction %d", o.reduction);
+    const bool literal = o.reduction == LSGD_REDUCE_LITERAL;
+    const bool bcast = o.broadcast_grad != 0;
     if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
-    std::vector<int32_t> order;
-    lsgd_status st = member_order(n_workers, group_of_worker, n_groups, order);
+    std::vector<int32_t> order, gstart;
+    lsgd_status st = literal ? partition_order(n_workers, group_of_worker, n_groups, order, gstart)
+                             : member_order(n_workers, group_of_worker, n_groups, order);
     if (st != LSGD_OK) return st;
+    if (bcast && gdt != LSGD_F32)
+        return fail(LSGD_ERR_DTYPE, "broadcast_grad needs binary32 gradients, got dtype %d", static_cast<int>(gdt));
     const bool live = n > 0;
     StepArgs a;
     memset(&a, 0, sizeof a);
@@ -123,6 +135,14 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
     if ((st = check_replicas(replicas, n_replicas, rdt, n, live, ranges)) != LSGD_OK) return st;
     if (!live) return LSGD_OK;
     if ((st = check_update_buffers(params, momentum, n, ranges)) != LSGD_OK) return st;
+    if (bcast)   // the gradient buffers are written too
+        for (Range& r : ranges)
+            if (r.what == kGradRange) r.written = true;
+    if (o.lr_device) {
+        if ((reinterpret_cast<uintptr_t>(o.lr_device) & 3u) != 0)
+            return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
+        ranges.push_back(range_of(o.lr_device, 1, 4, false, "lr_device"));
+    }
     if ((st = check_overlap(ranges)) != LSGD_OK) return st;
 
     a.p = params;
@@ -134,15 +154,34 @@ LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const
     a.W = n_workers / n_groups;
     a.n_replicas = n_replicas;
     a.rdt = static_cast<int32_t>(rdt);
+    a.lr_ptr = o.lr_device;
+    a.bcast_grad = bcast ? 1 : 0;
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    const FlatPick k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    FlatPick k;
+    if (literal) {
+        for (int32_t j = 0; j <= n_groups; ++j) a.group_start[j] = static_cast<uint8_t>(gstart[j]);
+        k = FlatPick{gdt == LSGD_BF16 ? step_flat_literal<uint16_t> : step_flat_literal<float>, 1};
+    } else {
+        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    }
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
     hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
-    return check_launch("lsgd_step");
+    return check_launch(literal ? "lsgd_step_ex" : "lsgd_step");
+}
+
+LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
+                               lsgd_dtype gdt, int32_t n_workers, const int32_t* group_of_worker,
+                               int32_t n_groups, int64_t n, float lr, float momentum_coef,
+                               float weight_decay, void* const* replicas, int32_t n_replicas,
+                               lsgd_dtype rdt, void* stream) {
+    // Without options no gradient buffer is written, so dropping const is safe.
+    return lsgd_step_ex(params, momentum, const_cast<void* const*>(grads), gdt, n_workers,
+                        group_of_worker, n_groups, n, lr, momentum_coef, weight_decay, replicas,
+                        n_replicas, rdt, nullptr, stream);
 }
 
 LSGD_API lsgd_status lsgd_group_mean(const void* const* grads, lsgd_dtype gdt, int32_t n_workers,
@@ -246,6 +285,36 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     hipLaunchKernelGGL(sgd_kernel, dim3(ls.blocks), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_sgd_step");
+}
+
+namespace {
+bool schedule_valid(const lsgd_lr_schedule* c) {
+    return c && c->base_batch > 0 && c->warmup_iters >= 0 && c->decay_iters >= 0;
+}
+lsgd::Schedule to_schedule(const lsgd_lr_schedule& c) {
+    return lsgd::Schedule{c.base_lr, c.base_batch, c.global_batch, c.warmup_iters, c.decay_iters,
+                          c.decay_factor};
+}
+}  // namespace
+
+LSGD_API float lsgd_lr_at(const lsgd_lr_schedule* schedule, int64_t t) {
+    if (!schedule_valid(schedule) || t < 0) return __builtin_nanf("");
+    return schedule_lr(to_schedule(*schedule), t);
+}
+
+LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int64_t* iteration,
+                                           float* lr_out, void* stream) {
+    if (!schedule || !iteration || !lr_out) return fail(LSGD_ERR_NULL, "schedule, iteration or lr_out is NULL");
+    if (!schedule_valid(schedule))
+        return fail(LSGD_ERR_SIZE, "schedule needs base_batch > 0 and non-negative iteration counts");
+    if ((reinterpret_cast<uintptr_t>(iteration) & 7u) != 0 || (reinterpret_cast<uintptr_t>(lr_out) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "iteration must be 8-byte and lr_out 4-byte aligned");
+    std::vector<Range> ranges{range_of(iteration, 1, 8, true, "iteration"), range_of(lr_out, 1, 4, true, "lr_out")};
+    lsgd_status st = check_overlap(ranges);
+    if (st != LSGD_OK) return st;
+    hipLaunchKernelGGL(schedule_step_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream),
+                       to_schedule(*schedule), iteration, lr_out);
+    return check_launch("lsgd_lr_schedule_step");
 }
 
 }  // extern "C"

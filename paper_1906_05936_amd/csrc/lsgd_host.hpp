@@ -24,6 +24,13 @@ lsgd_status check_launch(const char* what);
 lsgd_status member_order(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
                          std::vector<int32_t>& order);
 
+// Any partition into non-empty groups (the paper-literal reduction): member
+// order grouped by group id, ascending worker id inside a group, and the
+// G + 1 group offsets into it. LSGD_ERR_GROUPS for an id out of range or an
+// empty group.
+lsgd_status partition_order(int32_t n_workers, const int32_t* group_of_worker, int32_t n_groups,
+                            std::vector<int32_t>& order, std::vector<int32_t>& group_start);
+
 bool aligned16(const void* p);
 
 // A byte range [begin, end) of one buffer argument; `written` for outputs.

@@ -329,9 +329,19 @@ struct StepArgs {
     int32_t n_workers, n_groups, W;
     int32_t n_replicas, rdt;
     uint32_t xcd_chunk, upl;
+    const float* lr_ptr;   // non-null: the learning rate is read here when the kernel runs
+    int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
+    uint8_t group_start[kMaxWorkers + 4];  // literal reduction: group j is members [start[j], start[j+1])
     const void* grads[kMaxWorkers];
     void* replicas[kMaxReplicas];
 };
+
+// The hyperparameters a kernel uses: lr from device memory when given.
+__device__ __forceinline__ Hyper resolve_hyper(const Hyper& h, const float* lr_ptr) {
+    Hyper r = h;
+    if (lr_ptr) r.lr = *lr_ptr;
+    return r;
+}
 
 // Group-mean outputs of lsgd_group_mean / inputs of lsgd_global_mean.
 struct MeanArgs {
@@ -358,6 +368,43 @@ template <> struct TileUnits<uint16_t> { static constexpr int U = 1; };
 // occupancy) for the 64- and 128-worker groupings.
 constexpr int kUnrollFloats = 128;
 constexpr int kStreamFloats = 64;
+
+// Everything after the mean gradient, for a tile of U units: optional
+// broadcast of gbar into every worker's (binary32) gradient buffer, the
+// update, and the copy-out.
+template <typename GT, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U], int cnt,
+                                            float (&gbar)[U * Unit<GT>::VEC]) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    if constexpr (sizeof(GT) == 4) {
+        if (s.bcast_grad()) {
+            const int nw = s.n_workers();
+            for (int k = 0; k < nw; ++k) {
+                float* g = static_cast<float*>(const_cast<void*>(s.grad(k)));
+#pragma unroll
+                for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(g, e0[q], cnt, slice<VEC, T>(gbar, q));
+            }
+        }
+    }
+    float p[T], m[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    sgd_update<T>(s.hyper(), gbar, p, m);
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    const int R = s.n_replicas();
+    const int rdt = s.rdt();
+    for (int r = 0; r < R; ++r) {
+        void* rp = s.replica(r);
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(p, q));
+    }
+}
 
 // Fused step on one tile of U units, compile-time W and G (powers of two).
 // Every array holds T = U*VEC floats: the tree is the same PW for each of them.
@@ -401,23 +448,7 @@ __device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[
 #pragma unroll
     for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
 
-    float p[T], m[T];
-#pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
-#pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
-    sgd_update<T>(s.hyper(), gbar, p, m);
-#pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
-#pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
-    const int R = s.n_replicas();
-    const int rdt = s.rdt();
-    for (int r = 0; r < R; ++r) {
-        void* rp = s.replica(r);
-#pragma unroll
-        for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(p, q));
-    }
+    finish_tile<GT, U, TAIL>(s, e0, cnt, gbar);
 }
 
 template <typename GT, int W, int G, bool TAIL, typename Src>
@@ -446,28 +477,50 @@ __device__ __forceinline__ void fused_unit_rt(const Src& s, int W, int G, int64_
     groups.result(gbar, glevels);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
+    const int64_t e[1] = {e0};
+    finish_tile<GT, 1, TAIL>(s, e, cnt, gbar);
+}
 
-    float p[VEC], m[VEC];
-    load_f32<VEC, TAIL>(s.p(), e0, cnt, p);
-    load_f32<VEC, TAIL>(s.m(), e0, cnt, m);
-    sgd_update<VEC>(s.hyper(), gbar, p, m);
-    store_f32<VEC, TAIL>(s.p(), e0, cnt, p);
-    store_f32<VEC, TAIL>(s.m(), e0, cnt, m);
-    const int R = s.n_replicas();
-    const int rdt = s.rdt();
-    for (int r = 0; r < R; ++r) store_replica<VEC, TAIL>(s.replica(r), rdt, e0, cnt, p);
+// Fused step on one unit with the paper-literal reduction: group j (members
+// start[j] .. start[j+1] in member order, any non-empty size) contributes its
+// pairwise sum divided by N, and the group contributions are summed pairwise
+// without a further division.
+template <typename GT, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_unit_literal(const Src& s, const uint8_t* start, int N, int G,
+                                                   int64_t e0, int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const float nf = static_cast<float>(N);
+    PwAcc<VEC> groups;
+    const int glevels = acc_levels(G);
+    for (int j = 0; j < G; ++j) {
+        const int off = start[j];
+        float part[VEC];
+        pw_runtime<VEC>(start[j + 1] - off, [&](int k, float (&x)[VEC]) {
+            load_grad<GT, TAIL>(s.grad(off + k), e0, cnt, x);
+        }, part);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) part[v] = part[v] / nf;
+        groups.push(part, glevels);
+    }
+    float gbar[VEC];
+    groups.result(gbar, glevels);
+    const int64_t e[1] = {e0};
+    finish_tile<GT, 1, TAIL>(s, e, cnt, gbar);
 }
 
 // Pointer source for the planless fused step: everything from StepArgs.
 struct FlatSrc {
     const StepArgs& a;
+    Hyper h;
     __device__ const void* grad(int k) const { return a.grads[k]; }
     __device__ float* p() const { return a.p; }
     __device__ float* m() const { return a.m; }
     __device__ void* replica(int r) const { return a.replicas[r]; }
     __device__ int n_replicas() const { return a.n_replicas; }
     __device__ int rdt() const { return a.rdt; }
-    __device__ Hyper hyper() const { return a.h; }
+    __device__ Hyper hyper() const { return h; }
+    __device__ int bcast_grad() const { return a.bcast_grad; }
+    __device__ int n_workers() const { return a.n_workers; }
 };
 
 // ------------------------------------------------------------- flat kernels
@@ -479,7 +532,7 @@ struct FlatSrc {
 template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrc s{a};
+    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     for_tiles<U, VEC>(
@@ -492,9 +545,21 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
 }
 
 template <typename GT>
+__global__ __launch_bounds__(kBlock) void step_flat_literal(StepArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
+    const int64_t full = a.n / VEC;
+    const int rem = static_cast<int>(a.n - full * VEC);
+    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
+        if (u < full) fused_unit_literal<GT, false>(s, a.group_start, a.n_workers, a.n_groups, u * VEC, VEC);
+        else fused_unit_literal<GT, true>(s, a.group_start, a.n_workers, a.n_groups, u * VEC, rem);
+    });
+}
+
+template <typename GT>
 __global__ __launch_bounds__(kBlock) void step_flat_rt(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrc s{a};
+    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
@@ -595,19 +660,23 @@ struct PlanArgs {
     int32_t n_replicas, rdt;
     int32_t n_buckets;
     uint32_t xcd_chunk;
+    const float* lr_ptr;
     Hyper h;
 };
 
 struct PlanSrc {
     void* const* t;  // this tensor's row of the pointer table
     const PlanArgs& a;
+    Hyper h;
     __device__ const void* grad(int k) const { return t[2 + k]; }
     __device__ float* p() const { return static_cast<float*>(t[0]); }
     __device__ float* m() const { return static_cast<float*>(t[1]); }
     __device__ void* replica(int r) const { return t[2 + a.n_workers + r]; }
     __device__ int n_replicas() const { return a.n_replicas; }
     __device__ int rdt() const { return a.rdt; }
-    __device__ Hyper hyper() const { return a.h; }
+    __device__ Hyper hyper() const { return h; }
+    __device__ int bcast_grad() const { return 0; }
+    __device__ int n_workers() const { return a.n_workers; }
 };
 
 // One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
@@ -618,10 +687,11 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
     if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
+    const Hyper h = resolve_hyper(a.h, a.lr_ptr);
     const int32_t c_end = a.bucket_begin[b + 1];
     for (int32_t c = a.bucket_begin[b]; c < c_end; ++c) {
         const PlanChunk ch = a.chunks[c];
-        const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a};
+        const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
         const int64_t full = ch.len / VEC;
         if constexpr (W > 0) {
             // tiles of U units kBlock apart, then the units of a partial last tile
@@ -659,6 +729,43 @@ static __global__ __launch_bounds__(kBlock) void stream_copy_kernel(u32x4* __res
     for_units(units, chunk, 1, [&](int64_t u) {
         __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
     });
+}
+
+}  // namespace lsgd
+
+namespace lsgd {
+
+// Learning-rate schedule (linear scaling, warmup, step decay), evaluated in
+// binary64 and rounded to binary32 once. Shared by the host function and the
+// device step so that both give the same bits.
+struct Schedule {
+    double base_lr, base_batch, global_batch;
+    int64_t warmup_iters, decay_iters;
+    double decay_factor;
+};
+
+__host__ __device__ inline float schedule_lr(const Schedule& c, int64_t t) {
+    const double target = c.base_lr * (c.global_batch / c.base_batch);
+    double lr = target;
+    if (c.warmup_iters > 0 && t < c.warmup_iters)
+        lr = c.base_lr + (target - c.base_lr) * (static_cast<double>(t) / static_cast<double>(c.warmup_iters));
+    if (c.decay_iters > 0) {
+        const int64_t k = t / c.decay_iters;
+        double f = 1.0;
+        for (int64_t i = 0; i < k; ++i) f = f * c.decay_factor;
+        lr = lr * f;
+    }
+    return static_cast<float>(lr);
+}
+
+// One lane reads the iteration, writes its rate and advances the counter.
+static __global__ __launch_bounds__(64) void schedule_step_kernel(Schedule c, int64_t* iteration,
+                                                                  float* lr_out) {
+    if (threadIdx.x == 0) {
+        const int64_t t = *iteration;
+        *lr_out = schedule_lr(c, t);
+        *iteration = t + 1;
+    }
 }
 
 }  // namespace lsgd

@@ -189,9 +189,18 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     return LSGD_OK;
 }
 
-LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
-                                    float weight_decay, void* stream) {
+LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float momentum_coef,
+                                       float weight_decay, const lsgd_step_options* options,
+                                       void* stream) {
     if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    const float* lr_device = nullptr;
+    if (options) {
+        if (options->reduction != LSGD_REDUCE_MEAN_OF_MEANS || options->broadcast_grad != 0)
+            return fail(LSGD_ERR_UNSUPPORTED, "plans take only lr_device among the step options");
+        lr_device = options->lr_device;
+        if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
+            return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
+    }
     if (plan->n_buckets == 0) return LSGD_OK;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
@@ -208,6 +217,7 @@ LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momen
     a.n_replicas = plan->n_replicas;
     a.rdt = static_cast<int32_t>(plan->rdt);
     a.h = Hyper{lr, momentum_coef, weight_decay};
+    a.lr_ptr = lr_device;
     a.n_buckets = plan->n_buckets;
     const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
     const LaunchShape ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
@@ -216,6 +226,11 @@ LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momen
                                           : pick_plan<float>(plan->W, plan->n_groups);
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_step_plan");
+}
+
+LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
+                                    float weight_decay, void* stream) {
+    return lsgd_step_plan_ex(plan, lr, momentum_coef, weight_decay, nullptr, stream);
 }
 
 LSGD_API void lsgd_plan_destroy(lsgd_plan* plan) { free_plan(plan); }

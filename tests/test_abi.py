@@ -27,7 +27,7 @@ L = pytest.importorskip("paper_1906_05936_amd._lib")
 lib = L.lib
 pa, i32a, i64a = L.ptr_array, L.int32_array, L.int64_array
 
-OK, NULL, SIZE, GROUPS, ALIGN, DTYPE, HIP, ALIAS = range(8)
+OK, NULL, SIZE, GROUPS, ALIGN, DTYPE, HIP, ALIAS, UNSUPPORTED = range(9)
 A = 1 << 20   # fake, 16-byte aligned "device" addresses: never dereferenced
 MB = 1 << 20
 
@@ -44,7 +44,8 @@ def test_header_declares_the_boundary():
     assert {"lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
             "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
             "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
-            "lsgd_get_launch_shape", "lsgd_stream_copy"} == names
+            "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
+            "lsgd_lr_schedule_step", "lsgd_step_plan_ex"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -228,3 +229,42 @@ def test_stream_copy_validation():
     assert f(0, A, 64, None) == NULL
     assert f(A + 8, A + 100 * MB, 64, None) == ALIGN
     assert f(A, A + 32, 64, None) == ALIAS
+
+
+def step_ex(reduction=0, bcast=0, lr_dev=None, gow=(0, 0, 1, 1), G=2, grads=None, gdt=0, n=1000):
+    if grads is None:
+        grads = [A + (k + 2) * 100 * MB for k in range(len(gow))]
+    opts = L.StepOptions(reduction, bcast, lr_dev)
+    return lib.lsgd_step_ex(A, A + 100 * MB, pa(grads), gdt, len(gow), i32a(gow), G, n, 0.1, 0.9,
+                            1e-4, None, 0, 0, ctypes.byref(opts), None)
+
+
+def test_step_ex_validation():
+    assert step_ex(reduction=2) == UNSUPPORTED
+    # literal reduction: any partition into non-empty groups, equal sizes not required
+    assert step_ex(reduction=1, gow=(0, 1, 1, 1), G=3) == GROUPS           # group 2 empty
+    assert step_ex(reduction=1, gow=(0, 1, 2), G=4) == GROUPS              # more groups than workers
+    assert step_ex(reduction=1, gow=(0, 3, 1, 1), G=3) == GROUPS           # id out of range
+    assert step_ex(reduction=0, gow=(0, 1, 1, 1), G=2) == GROUPS           # mean of means needs equal groups
+    assert step_ex(reduction=1, gow=(0, 1, 1, 1), G=2, n=0) == OK          # validated no-op
+    # broadcast writes the gradient buffers: binary32 only, no two workers may share one
+    assert step_ex(bcast=1, gdt=1) == DTYPE
+    g = A + 200 * MB
+    assert step_ex(bcast=1, grads=[g, g, A + 300 * MB, A + 400 * MB]) == ALIAS
+    assert step_ex(bcast=1, grads=[A + 16, A + 300 * MB, A + 400 * MB, A + 500 * MB]) == ALIAS
+    assert step_ex(lr_dev=A + 700 * MB + 2) == ALIGN
+    assert step_ex(lr_dev=A + 8) == ALIAS                                  # inside the written params
+
+
+def test_plan_ex_and_schedule_validation():
+    opts = L.StepOptions(1, 0, None)
+    assert lib.lsgd_step_plan_ex(None, 0.1, 0.9, 1e-4, ctypes.byref(opts), None) == NULL
+    sched = L.LrSchedule(0.1, 256.0, 16384.0, 390, 2340, 0.1)
+    f = lib.lsgd_lr_schedule_step
+    assert f(None, A, A + 64, None) == NULL
+    assert f(ctypes.byref(sched), 0, A + 64, None) == NULL
+    assert f(ctypes.byref(sched), A + 4, A + 64, None) == ALIGN
+    assert f(ctypes.byref(sched), A, A + 66, None) == ALIGN
+    assert f(ctypes.byref(sched), A, A + 4, None) == ALIAS
+    bad = L.LrSchedule(0.1, 0.0, 16384.0, 390, 2340, 0.1)
+    assert f(ctypes.byref(bad), A, A + 64, None) == SIZE

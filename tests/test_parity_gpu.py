@@ -506,3 +506,141 @@ def test_graph_capture_replays_match_eager():
             assert torch.equal(a, b), k
     del graph
     plan_g.close()
+
+
+# ---------------------------------------------------------------- step variants (lsgd_step_ex)
+
+LITERAL_CASES = [
+    # group_of_worker, G, gdt, n, R, broadcast
+    ([0, 1, 1, 1], 2, "f32", 100_003, 2, False),
+    ([2, 0, 1, 1, 2, 0, 0, 0, 1], 3, "bf16", 50_001, 1, False),
+    ("shuffled4x4", 4, "f32", 65_541, 0, True),
+    ([0] * 5 + [1], 2, "f32", 7, 1, True),
+    (list(range(7)), 7, "f32", 3_001, 0, False),
+    ([0, 0, 0, 1, 1, 2] * 20, 3, "f32", 4_099, 3, True),
+]
+
+
+@pytest.mark.parametrize("gow,G,gdt,n,R,bcast", LITERAL_CASES)
+def test_literal_reduction_matches_oracle(gow, G, gdt, n, R, bcast):
+    if gow == "shuffled4x4":
+        gow = workloads.shuffled_groups(4, 4, seed=9)
+    log("literal G=%d N=%d %s n=%d R=%d bcast=%s" % (G, len(gow), gdt, n, R, bcast))
+    rng = np.random.default_rng(n + G)
+    gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(len(gow))]
+    grads = [to_dev(x) for x in gh]
+    p_ref = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m_ref = (rng.standard_normal(n) * 0.01).astype(np.float32)
+    p, m = to_dev(p_ref), to_dev(m_ref)
+    reps = [torch.empty(n, device=DEV) for _ in range(R)]
+    lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps, reduction="literal", broadcast_grad=bcast)
+    rr = [np.zeros(n, np.float32) for _ in range(R)]
+    gw = [x.copy() for x in gh]
+    oracle.lsgd_step_literal(p_ref, m_ref, gw, gow, G, 0.1, 0.9, 1e-4, rr, broadcast_grad=bcast)
+    torch.cuda.synchronize()
+    assert_close(to_host(p), p_ref, "params")
+    assert_close(to_host(m), m_ref, "momentum")
+    for r in range(R):
+        assert np.array_equal(to_host(reps[r]), rr[r])
+    for w in range(len(gow)):
+        assert np.array_equal(to_host(grads[w]), gw[w]), w   # broadcast target (or untouched)
+
+
+@pytest.mark.parametrize("G,W", [(4, 4), (3, 5), (2, 16)])
+def test_gradient_broadcast_with_mean_of_means(G, W):
+    """broadcast_grad with the default reduction: every worker buffer receives
+    the global mean of the group means; params and momentum as lsgd_step."""
+    n = 70_001
+    rng = np.random.default_rng(G * W)
+    gow = groups_for(G, W, "shuffled", seed=4)
+    gh = [rand_host(rng, n, 1e-2, "f32") for _ in range(G * W)]
+    grads = [to_dev(x) for x in gh]
+    p_ref = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m_ref = np.zeros(n, np.float32)
+    p, m = to_dev(p_ref), to_dev(m_ref)
+    lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, broadcast_grad=True)
+    want = oracle.global_mean(oracle.group_means(gh, gow, G))
+    oracle.lsgd_step(p_ref, m_ref, gh, gow, G, 0.1, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    assert_close(to_host(p), p_ref, "params")
+    assert_close(to_host(m), m_ref, "momentum")
+    for g in grads:
+        assert to_host(g).tobytes() == want.tobytes()
+
+
+def test_learning_rate_from_device_memory():
+    n, G, W = 50_003, 2, 4
+    rng = np.random.default_rng(5)
+    gow = groups_for(G, W, "contiguous")
+    gh = [rand_host(rng, n, 1e-2, "f32") for _ in range(G * W)]
+    grads = [to_dev(x) for x in gh]
+    lr_t = torch.tensor([0.37], device=DEV)
+    p_ref = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m_ref = np.zeros(n, np.float32)
+    p, m = to_dev(p_ref), to_dev(m_ref)
+    lsgd.step(p, m, grads, gow, G, 123.0, 0.9, 1e-4, lr_device=lr_t)   # the lr argument is ignored
+    oracle.lsgd_step(p_ref, m_ref, gh, gow, G, np.float32(0.37), 0.9, 1e-4)
+    sizes = [1000, 3, 4097]
+    ph = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in sizes]
+    gth = [[rand_host(rng, s, 1e-2, "f32") for s in sizes] for _ in range(G * W)]
+    pt = [to_dev(x) for x in ph]
+    mt = [torch.zeros(s, device=DEV) for s in sizes]
+    plan = lsgd.Plan(pt, mt, [[to_dev(x) for x in row] for row in gth], gow, G)
+    plan.step(-1.0, 0.9, 1e-4, lr_device=lr_t)
+    torch.cuda.synchronize()
+    assert_close(to_host(p), p_ref, "params")
+    assert_close(to_host(m), m_ref, "momentum")
+    for t, s in enumerate(sizes):
+        mm = np.zeros(s, np.float32)
+        oracle.lsgd_step(ph[t], mm, [gth[w][t] for w in range(G * W)], gow, G, np.float32(0.37), 0.9, 1e-4)
+        assert_close(to_host(pt[t]), ph[t], "plan params %d" % t)
+    plan.close()
+
+
+def test_device_schedule_matches_oracle():
+    sched = (0.1, 256.0, 16384.0, 390, 2340, 0.1)
+    s = lsgd.lr_schedule(*sched)
+    it = torch.tensor([2300], device=DEV, dtype=torch.int64)
+    lr_out = torch.empty(1, device=DEV)
+    hist = torch.empty(100, device=DEV)
+    for k in range(100):
+        lsgd.lr_schedule_step(s, it, lr_out)
+        hist[k:k + 1].copy_(lr_out)
+    torch.cuda.synchronize()
+    assert it.item() == 2400
+    want = np.array([oracle.lr_at(2300 + k, *sched) for k in range(100)], np.float32)
+    assert to_host(hist).tobytes() == want.tobytes()
+
+
+def test_graph_captured_whole_step_follows_the_schedule():
+    """A HIP graph holding (schedule step, fused step reading the rate from
+    device memory): each replay advances the schedule, bitwise equal to eager
+    steps run with the oracle's rates."""
+    n, G, W = 40_009, 2, 2
+    rng = np.random.default_rng(6)
+    gow = groups_for(G, W, "contiguous")
+    grads = [to_dev(rand_host(rng, n, 1e-2, "f32")) for _ in range(G * W)]
+    p0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+    sched = (0.1, 256.0, 1024.0, 4, 7, 0.5)
+    s = lsgd.lr_schedule(*sched)
+    it = torch.zeros(1, device=DEV, dtype=torch.int64)
+    lr_t = torch.zeros(1, device=DEV)
+    p, m = p0.clone(), torch.zeros(n, device=DEV)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            lsgd.lr_schedule_step(s, it, lr_t, stream=stream)
+            lsgd.step(p, m, grads, gow, G, 0.0, 0.9, 1e-4, lr_device=lr_t, stream=stream)
+    torch.cuda.synchronize()
+    pe, me = p0.clone(), torch.zeros(n, device=DEV)
+    for k in range(12):
+        graph.replay()
+        lr_k = float(oracle.lr_at(k, *sched))
+        lsgd.step(pe, me, grads, gow, G, lr_k, 0.9, 1e-4)
+        torch.cuda.synchronize()
+        assert abs(lr_t.item() - lr_k) == 0.0, k
+        assert torch.equal(p, pe) and torch.equal(m, me), k
+    assert it.item() == 12
+    del graph
