@@ -48,6 +48,9 @@ def parse_args(argv=None):
     ap.add_argument("--no-r0", action="store_true", help="skip the secondary R=0 measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also launch a plain 1 GiB copy kernel (counter calibration)")
+    ap.add_argument("--path", choices=("fused", "unfused"), default="fused",
+                    help="fused: one lsgd_step per step; unfused: lsgd_group_mean, "
+                         "lsgd_global_mean, lsgd_sgd_step per step (flat workloads)")
     ap.add_argument("--derive-traffic", action="store_true")
     ap.add_argument("--fetch-csv")
     ap.add_argument("--write-csv")
@@ -168,6 +171,76 @@ def copy_ceiling(dev, calibrate):
     del src, dst
     torch.cuda.empty_cache()
     return gbps
+
+
+class UnfusedSetup:
+    """The three-call path of a flat workload: group means and the mean
+    gradient go through HBM (G + 1 extra fp32 vectors written and read)."""
+
+    def __init__(self, wl, R, dev):
+        import torch
+        import workloads
+        from paper_1906_05936_amd._lib import lib, ptr_array, int32_array, check
+        if wl.tensor_sizes:
+            raise SystemExit("the unfused path is measured on flat workloads")
+        self.wl, self.R = wl, R
+        N, G = wl.n_workers, wl.groups
+        self.gow = workloads.contiguous_groups(G, wl.workers_per_group)
+        rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
+        stream = torch.cuda.current_stream(dev)
+        self.params = [workloads.init_params(wl, dev)]
+        self.mom = [torch.zeros_like(self.params[0])]
+        scratch = torch.empty(wl.n, device=dev) if wl.grad_dtype == "bf16" else None
+        self.grads = []
+        for w in range(N):
+            g = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
+            workloads.fill_worker_grad(wl, 0, w, g, scratch)
+            self.grads.append([g])
+        del scratch
+        self.reps = [[torch.empty(wl.n, device=dev, dtype=rtd)] for _ in range(R)]
+        self.means = [torch.empty(wl.n, device=dev) for _ in range(G)]
+        self.gbar = torch.empty(wl.n, device=dev)
+        s = ctypes.c_void_p(stream.cuda_stream)
+        gdt = 1 if wl.grad_dtype == "bf16" else 0
+        a1 = (ptr_array([g[0].data_ptr() for g in self.grads]), gdt, N, int32_array(self.gow), G, wl.n,
+              ptr_array([m.data_ptr() for m in self.means]), s)
+        a2 = (ptr_array([m.data_ptr() for m in self.means]), G, wl.n, self.gbar.data_ptr(), s)
+        a3 = (self.params[0].data_ptr(), self.mom[0].data_ptr(), self.gbar.data_ptr(), wl.n,
+              ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd),
+              ptr_array([r[0].data_ptr() for r in self.reps]), R, 1 if rtd == torch.bfloat16 else 0, s)
+        self.calls = [lambda: check(lib.lsgd_group_mean(*a1)), lambda: check(lib.lsgd_global_mean(*a2)),
+                      lambda: check(lib.lsgd_sgd_step(*a3))]
+        self.stream = stream
+        self.plan = None
+
+    def step(self):
+        for c in self.calls:
+            c()
+
+    def close(self):
+        pass
+
+    def bytes_per_call(self):
+        wl, n, G = self.wl, self.wl.n, self.wl.groups
+        rb = 2 if wl.replica_dtype == "bf16" else 4
+        return [n * (wl.n_workers * wl.grad_bytes + 4 * G),      # group means: read N, write G
+                n * (4 * G + 4),                                   # global mean: read G, write 1
+                n * (4 + 16 + self.R * rb)]                        # update: read gbar, p, m; write p, m, R
+
+    def time_calls(self, steps, warmup):
+        """Average ms per call of each of the three kernels (events between them)."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        for k in range(steps):
+            for c in range(3):
+                ev[k][c].record(self.stream)
+                self.calls[c]()
+            ev[k][3].record(self.stream)
+        torch.cuda.synchronize()
+        return [sum(ev[k][c].elapsed_time(ev[k][c + 1]) for k in range(steps)) / steps for c in range(3)]
 
 
 # ---------------------------------------------------------------- CPU baseline
@@ -332,6 +405,31 @@ def main(argv=None):
     print("bench: %s n=%d G=%d W=%d %s R=%d" % (wl.name, wl.n, wl.groups, wl.workers_per_group,
                                                wl.grad_dtype, R), file=sys.stderr, flush=True)
     ceiling = copy_ceiling(dev, args.calibrate_copy)
+    if args.path == "unfused":
+        setup = UnfusedSetup(wl, R, dev)
+        ms = time_steps(setup, args.steps, args.warmup)
+        per_call = setup.time_calls(args.steps, args.warmup)
+        nbytes = setup.bytes_per_call()
+        alg = sum(nbytes)
+        gbps = alg / (ms * 1e-3) / 1e9
+        names = ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step")
+        result = {
+            "metric": METRIC + " (unfused three-call path)", "value": round(gbps, 2), "unit": "GB/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+            "data": "synthetic",
+            "config": {"workload": wl.name, "path": "unfused", "n": wl.n, "groups": wl.groups,
+                       "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
+                       "replicas": R},
+            "steps_per_s": round(1e3 / ms, 2),
+            "calls": {nm: {"ms": round(t, 6), "bytes": b, "GBps": round(b / (t * 1e-3) / 1e9, 2),
+                           "frac": round(b / (t * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+                      for nm, t, b in zip(names, per_call, nbytes)},
+            "fused_equivalent_bytes": wl.algorithmic_bytes(R),
+            "copy_ceiling_GBps": round(ceiling, 1),
+        }
+        print(json.dumps(result), flush=True)
+        return
     setup = Setup(wl, R, dev)
     ms = time_steps(setup, args.steps, args.warmup)
     alg = wl.algorithmic_bytes(R)

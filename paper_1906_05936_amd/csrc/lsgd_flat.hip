@@ -48,6 +48,42 @@ FlatPick pick_flat(int W, int G) {
     return FlatPick{step_flat_rt<GT>, 1};
 }
 
+using MeanKernel = void (*)(MeanArgs);
+
+struct MeanPick {
+    MeanKernel kernel;
+    int tile;
+};
+
+// Group means: compile-time W for powers of two up to 16, else runtime W.
+template <typename GT>
+MeanPick pick_group_mean(int W) {
+    constexpr int U = TileUnits<GT>::U;
+    switch (W) {
+        case 1: return MeanPick{group_mean_kernel_ct<GT, 1, U>, U};
+        case 2: return MeanPick{group_mean_kernel_ct<GT, 2, U>, U};
+        case 4: return MeanPick{group_mean_kernel_ct<GT, 4, U>, U};
+        case 8: return MeanPick{group_mean_kernel_ct<GT, 8, U>, U};
+        case 16: return MeanPick{group_mean_kernel_ct<GT, 16, U>, U};
+    }
+    return MeanPick{group_mean_kernel<GT>, 1};
+}
+
+// Global mean: compile-time G for powers of two up to 128, else runtime G.
+MeanPick pick_global_mean(int G) {
+    switch (G) {
+        case 1: return MeanPick{global_mean_kernel_ct<1, 2>, 2};
+        case 2: return MeanPick{global_mean_kernel_ct<2, 2>, 2};
+        case 4: return MeanPick{global_mean_kernel_ct<4, 2>, 2};
+        case 8: return MeanPick{global_mean_kernel_ct<8, 2>, 2};
+        case 16: return MeanPick{global_mean_kernel_ct<16, 2>, 2};
+        case 32: return MeanPick{global_mean_kernel_ct<32, 2>, 2};
+        case 64: return MeanPick{global_mean_kernel_ct<64, 2>, 2};
+        case 128: return MeanPick{global_mean_kernel_ct<128, 2>, 2};
+    }
+    return MeanPick{global_mean_kernel, 1};
+}
+
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
 
 // Name of gradient ranges in the aliasing check (compared by address).
@@ -210,15 +246,11 @@ LSGD_API lsgd_status lsgd_group_mean(const void* const* grads, lsgd_dtype gdt, i
     a.n_groups = n_groups;
     a.W = n_workers / n_groups;
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    const LaunchShape ls = launch_shape((n + vec - 1) / vec);
+    const MeanPick k = gdt == LSGD_BF16 ? pick_group_mean<uint16_t>(a.W) : pick_group_mean<float>(a.W);
+    const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    if (gdt == LSGD_BF16)
-        hipLaunchKernelGGL(group_mean_kernel<uint16_t>, dim3(ls.blocks), dim3(kBlock), 0,
-                           static_cast<hipStream_t>(stream), a);
-    else
-        hipLaunchKernelGGL(group_mean_kernel<float>, dim3(ls.blocks), dim3(kBlock), 0,
-                           static_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_group_mean");
 }
 
@@ -246,11 +278,11 @@ LSGD_API lsgd_status lsgd_global_mean(const float* const* group_means, int32_t n
     a.out[0] = grad_mean;
     a.n = n;
     a.n_groups = n_groups;
-    const LaunchShape ls = launch_shape((n + 3) / 4);
+    const MeanPick k = pick_global_mean(n_groups);
+    const LaunchShape ls = launch_shape((n + 3) / 4, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    hipLaunchKernelGGL(global_mean_kernel, dim3(ls.blocks), dim3(kBlock), 0,
-                       static_cast<hipStream_t>(stream), a);
+    hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_global_mean");
 }
 
@@ -279,10 +311,11 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     a.n_replicas = n_replicas;
     a.rdt = static_cast<int32_t>(rdt);
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
-    const LaunchShape ls = launch_shape((n + 3) / 4);
+    constexpr int kSgdTile = 2;
+    const LaunchShape ls = launch_shape((n + 3) / 4, kSgdTile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    hipLaunchKernelGGL(sgd_kernel, dim3(ls.blocks), dim3(kBlock), 0,
+    hipLaunchKernelGGL(sgd_kernel<kSgdTile>, dim3(ls.blocks), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_sgd_step");
 }

@@ -369,6 +369,31 @@ template <> struct TileUnits<uint16_t> { static constexpr int U = 1; };
 constexpr int kUnrollFloats = 128;
 constexpr int kStreamFloats = 64;
 
+// Pairwise sum of K leaves (compile-time K, a power of two) of T floats each:
+// unrolled while K * LW floats (LW = floats a leaf loads) stay within
+// kUnrollFloats, so that every load is issued up front; otherwise streamed in
+// batches of about kStreamFloats through a compile-time-sized pairwise
+// accumulator. Both give PW over the K leaves in order.
+template <int K, int T, int LW, typename Leaf>
+__device__ __forceinline__ void pw_leaves(const Leaf& leaf, float (&out)[T]) {
+    if constexpr (K * LW <= kUnrollFloats) {
+        pw_tree<0, K, T>(leaf, out);
+    } else {
+        constexpr int B0 = kStreamFloats / LW;
+        constexpr int B = B0 < 1 ? 1 : (B0 > K ? K : B0);
+        PwAcc<T, ilog2(K) + 1> acc;
+#pragma unroll 1
+        for (int j0 = 0; j0 < K; j0 += B) {
+            float x[B][T];
+#pragma unroll
+            for (int q = 0; q < B; ++q) leaf(j0 + q, x[q]);
+#pragma unroll
+            for (int q = 0; q < B; ++q) acc.push(x[q]);
+        }
+        acc.result(out);
+    }
+}
+
 // Everything after the mean gradient, for a tile of U units: optional
 // broadcast of gbar into every worker's (binary32) gradient buffer, the
 // update, and the copy-out.
@@ -429,22 +454,7 @@ __device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[
         for (int v = 0; v < T; ++v) gm[v] = sum[v] / static_cast<float>(W);
     };
     float tot[T], gbar[T];
-    if constexpr (W * G * T <= kUnrollFloats) {
-        pw_tree<0, G, T>(group_leaf, tot);
-    } else {
-        constexpr int GU0 = kStreamFloats / (W * T);
-        constexpr int GU = GU0 < 1 ? 1 : (GU0 > G ? G : GU0);
-        PwAcc<T, ilog2(G) + 1> groups;
-#pragma unroll 1
-        for (int j0 = 0; j0 < G; j0 += GU) {
-            float gm[GU][T];
-#pragma unroll
-            for (int q = 0; q < GU; ++q) group_leaf(j0 + q, gm[q]);
-#pragma unroll
-            for (int q = 0; q < GU; ++q) groups.push(gm[q]);
-        }
-        groups.result(tot);
-    }
+    pw_leaves<G, T, W * T>(group_leaf, tot);
 #pragma unroll
     for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
 
@@ -568,7 +578,42 @@ __global__ __launch_bounds__(kBlock) void step_flat_rt(StepArgs a) {
     });
 }
 
-// lsgd_group_mean: every group's mean of its W members, for one unit.
+// lsgd_group_mean, compile-time W (a power of two): every group's mean of its
+// W members for one tile of U units, stored stream-major.
+template <typename GT, int W, int U, bool TAIL>
+__device__ __forceinline__ void group_mean_tile(const MeanArgs& a, const int64_t (&e0)[U], int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    for (int j = 0; j < a.n_groups; ++j) {
+        float sum[T];
+        pw_leaves<W, T, T>([&](int k, float (&x)[T]) {
+            const void* g = a.in[j * W + k];
+#pragma unroll
+            for (int q = 0; q < U; ++q) load_grad<GT, TAIL>(g, e0[q], cnt, slice<VEC, T>(x, q));
+        }, sum);
+#pragma unroll
+        for (int v = 0; v < T; ++v) sum[v] = sum[v] / static_cast<float>(W);
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(a.out[j], e0[q], cnt, slice<VEC, T>(sum, q));
+    }
+}
+
+template <typename GT, int W, int U>
+__global__ __launch_bounds__(kBlock) void group_mean_kernel_ct(MeanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int64_t full = a.n / VEC;
+    const int rem = static_cast<int>(a.n - full * VEC);
+    for_tiles<U, VEC>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { group_mean_tile<GT, W, U, false>(a, e0, VEC); },
+        [&](int64_t u) {
+            const int64_t e[1] = {u * VEC};
+            if (u < full) group_mean_tile<GT, W, 1, false>(a, e, VEC);
+            else group_mean_tile<GT, W, 1, true>(a, e, rem);
+        });
+}
+
+// lsgd_group_mean, runtime W (any equal-size grouping), one unit.
 template <typename GT, bool TAIL>
 __device__ __forceinline__ void group_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
     constexpr int VEC = Unit<GT>::VEC;
@@ -595,7 +640,38 @@ __global__ __launch_bounds__(kBlock) void group_mean_kernel(MeanArgs a) {
     });
 }
 
-// lsgd_global_mean: PW over the G group means, / G, for one 4-element unit.
+// lsgd_global_mean, compile-time G (a power of two): PW over the G group
+// means, / G, for one tile of U 4-element units.
+template <int G, int U, bool TAIL>
+__device__ __forceinline__ void global_mean_tile(const MeanArgs& a, const int64_t (&e0)[U], int cnt) {
+    constexpr int T = U * 4;
+    float s[T];
+    pw_leaves<G, T, T>([&](int j, float (&x)[T]) {
+        const float* in = static_cast<const float*>(a.in[j]);
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_f32<4, TAIL>(in, e0[q], cnt, slice<4, T>(x, q));
+    }, s);
+#pragma unroll
+    for (int v = 0; v < T; ++v) s[v] = s[v] / static_cast<float>(G);
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.out[0], e0[q], cnt, slice<4, T>(s, q));
+}
+
+template <int G, int U>
+__global__ __launch_bounds__(kBlock) void global_mean_kernel_ct(MeanArgs a) {
+    const int64_t full = a.n / 4;
+    const int rem = static_cast<int>(a.n - full * 4);
+    for_tiles<U, 4>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { global_mean_tile<G, U, false>(a, e0, 4); },
+        [&](int64_t u) {
+            const int64_t e[1] = {u * 4};
+            if (u < full) global_mean_tile<G, 1, false>(a, e, 4);
+            else global_mean_tile<G, 1, true>(a, e, rem);
+        });
+}
+
+// lsgd_global_mean, runtime G, one unit.
 template <bool TAIL>
 __device__ __forceinline__ void global_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
     float s[4];
@@ -617,26 +693,44 @@ static __global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) 
     });
 }
 
-// lsgd_sgd_step: update and copy-out from a precomputed mean gradient.
-template <bool TAIL>
-__device__ __forceinline__ void sgd_unit(const StepArgs& a, int64_t e0, int cnt) {
-    float g[4], p[4], m[4];
-    load_f32<4, TAIL>(a.gbar, e0, cnt, g);
-    load_f32<4, TAIL>(a.p, e0, cnt, p);
-    load_f32<4, TAIL>(a.m, e0, cnt, m);
-    sgd_update<4>(a.h, g, p, m);
-    store_f32<4, TAIL>(a.p, e0, cnt, p);
-    store_f32<4, TAIL>(a.m, e0, cnt, m);
-    for (int r = 0; r < a.n_replicas; ++r) store_replica<4, TAIL>(a.replicas[r], a.rdt, e0, cnt, p);
+// lsgd_sgd_step: update and copy-out from a precomputed mean gradient, one
+// tile of U 4-element units, stream-major.
+template <int U, bool TAIL>
+__device__ __forceinline__ void sgd_tile(const StepArgs& a, const Hyper& h, const int64_t (&e0)[U],
+                                         int cnt) {
+    constexpr int T = U * 4;
+    float g[T], p[T], m[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.gbar, e0[q], cnt, slice<4, T>(g, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    sgd_update<T>(h, g, p, m);
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    for (int r = 0; r < a.n_replicas; ++r) {
+        void* rp = a.replicas[r];
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_replica<4, TAIL>(rp, a.rdt, e0[q], cnt, slice<4, T>(p, q));
+    }
 }
 
-static __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
+template <int U>
+__global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
+    const Hyper h = resolve_hyper(a.h, a.lr_ptr);
     const int64_t full = a.n / 4;
     const int rem = static_cast<int>(a.n - full * 4);
-    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) sgd_unit<false>(a, u * 4, 4);
-        else sgd_unit<true>(a, u * 4, rem);
-    });
+    for_tiles<U, 4>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { sgd_tile<U, false>(a, h, e0, 4); },
+        [&](int64_t u) {
+            const int64_t e[1] = {u * 4};
+            if (u < full) sgd_tile<1, false>(a, h, e, 4);
+            else sgd_tile<1, true>(a, h, e, rem);
+        });
 }
 
 // ------------------------------------------------------------- multi-tensor plan
