@@ -33,45 +33,69 @@ class OracleError(RuntimeError):
 _lib = None
 
 
+def _configure(lib):
+    P = ctypes.c_void_p
+    i32, i64, c_int = ctypes.c_int32, ctypes.c_int64, ctypes.c_int
+    lib.oracle_members.argtypes = [i32, P, i32, P]
+    lib.oracle_members.restype = c_int
+    lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
+    lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
+    lib.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    lib.oracle_bf16_to_f32.restype = ctypes.c_float
+    lib.oracle_f32_to_bf16_array.argtypes = [P, P, i64]
+    lib.oracle_bf16_to_f32_array.argtypes = [P, P, i64]
+    lib.oracle_partition.argtypes = [i32, P, i32, P, P]
+    lib.oracle_partition.restype = c_int
+    lib.oracle_lr_at.argtypes = [i64, ctypes.c_double, ctypes.c_double, ctypes.c_double, i64, i64,
+                                 ctypes.c_double]
+    lib.oracle_lr_at.restype = ctypes.c_float
+    for sfx, real in (("_f32", ctypes.c_float), ("_f64", ctypes.c_double)):
+        f = getattr(lib, "oracle_pairwise" + sfx)
+        f.argtypes, f.restype = [P, i32], real
+        f = getattr(lib, "oracle_group_means" + sfx)
+        f.argtypes, f.restype = [P, c_int, i32, P, i32, i64, P], c_int
+        f = getattr(lib, "oracle_global_mean" + sfx)
+        f.argtypes, f.restype = [P, i32, i64, P], c_int
+        f = getattr(lib, "oracle_sgd_step" + sfx)
+        f.argtypes, f.restype = [P, P, P, i64, real, real, real, P, i32, c_int], c_int
+        f = getattr(lib, "oracle_lsgd_step" + sfx)
+        f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int]
+        f.restype = c_int
+        f = getattr(lib, "oracle_lsgd_step_literal" + sfx)
+        f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int, c_int]
+        f.restype = c_int
+    return lib
+
+
 def _load():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             from . import build as _build
             _build.build()
-        lib = ctypes.CDLL(LIB_PATH)
-        P = ctypes.c_void_p
-        i32, i64, c_int = ctypes.c_int32, ctypes.c_int64, ctypes.c_int
-        lib.oracle_members.argtypes = [i32, P, i32, P]
-        lib.oracle_members.restype = c_int
-        lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
-        lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
-        lib.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
-        lib.oracle_bf16_to_f32.restype = ctypes.c_float
-        lib.oracle_f32_to_bf16_array.argtypes = [P, P, i64]
-        lib.oracle_bf16_to_f32_array.argtypes = [P, P, i64]
-        lib.oracle_partition.argtypes = [i32, P, i32, P, P]
-        lib.oracle_partition.restype = c_int
-        lib.oracle_lr_at.argtypes = [i64, ctypes.c_double, ctypes.c_double, ctypes.c_double, i64, i64,
-                                     ctypes.c_double]
-        lib.oracle_lr_at.restype = ctypes.c_float
-        for sfx, real in (("_f32", ctypes.c_float), ("_f64", ctypes.c_double)):
-            f = getattr(lib, "oracle_pairwise" + sfx)
-            f.argtypes, f.restype = [P, i32], real
-            f = getattr(lib, "oracle_group_means" + sfx)
-            f.argtypes, f.restype = [P, c_int, i32, P, i32, i64, P], c_int
-            f = getattr(lib, "oracle_global_mean" + sfx)
-            f.argtypes, f.restype = [P, i32, i64, P], c_int
-            f = getattr(lib, "oracle_sgd_step" + sfx)
-            f.argtypes, f.restype = [P, P, P, i64, real, real, real, P, i32, c_int], c_int
-            f = getattr(lib, "oracle_lsgd_step" + sfx)
-            f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int]
-            f.restype = c_int
-            f = getattr(lib, "oracle_lsgd_step_literal" + sfx)
-            f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int, c_int]
-            f.restype = c_int
-        _lib = lib
+        _lib = _configure(ctypes.CDLL(LIB_PATH))
     return _lib
+
+
+class use_library:
+    """Context manager: route every function of this module to the oracle
+    library at `path` (a build of a modified oracle source), then restore.
+    Used by the tests that plant a mistake in the oracle to show that the pins
+    catch it."""
+
+    def __init__(self, path):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self._saved = _load()
+        _lib = _configure(ctypes.CDLL(self.path))
+        return self
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self._saved
+        return False
 
 
 def _ptr(a):

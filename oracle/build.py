@@ -12,17 +12,21 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "liblsgd_oracle.so")
 
 
-def build(verbose: bool = False) -> str:
-    src = os.path.join(HERE, "lsgd_oracle.c")
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
-           "-fexcess-precision=standard", "-Wall", "-Wextra", "-Werror",
-           "-shared", "-fPIC", "-o", tmp, src]
+CFLAGS = ["-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fexcess-precision=standard",
+          "-Wall", "-Wextra", "-Werror"]
+
+
+def build(verbose: bool = False, src_dir: str = HERE, out: str = LIB, cflags=None) -> str:
+    """Compile lsgd_oracle.c from `src_dir` into `out` (defaults: this
+    directory's source and library)."""
+    src = os.path.join(src_dir, "lsgd_oracle.c")
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = ["gcc"] + (cflags if cflags is not None else CFLAGS) + ["-shared", "-fPIC", "-o", tmp, src]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
-    subprocess.run(cmd, check=True, cwd=HERE)
-    os.replace(tmp, LIB)
-    return LIB
+    subprocess.run(cmd, check=True, cwd=src_dir)
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -268,3 +268,20 @@ def test_plan_ex_and_schedule_validation():
     assert f(ctypes.byref(sched), A, A + 4, None) == ALIAS
     bad = L.LrSchedule(0.1, 0.0, 16384.0, 390, 2340, 0.1)
     assert f(ctypes.byref(bad), A, A + 64, None) == SIZE
+
+
+def test_last_error_is_per_thread():
+    import threading
+    barrier = threading.Barrier(2)
+    seen = {}
+
+    def worker(name, call):
+        seen[name + "_status"] = call()
+        barrier.wait()          # both threads have failed before either reads
+        seen[name] = lib.lsgd_last_error().decode()
+
+    ta = threading.Thread(target=worker, args=("a", lambda: step(n=-7)))
+    tb = threading.Thread(target=worker, args=("b", lambda: step(gow=(0, 0, 1), G=2)))
+    ta.start(); tb.start(); ta.join(); tb.join()
+    assert seen["a_status"] == SIZE and "n=-7" in seen["a"]
+    assert seen["b_status"] == GROUPS and "divide" in seen["b"]

@@ -71,6 +71,29 @@ def test_pairwise_split_written_out():
     assert np.float32(half) != np.float32(expect[6])
 
 
+def test_group_sums_follow_ascending_worker_id():
+    """Each group is summed in ascending worker id with the pairwise split
+    (members of a non-power-of-two group written out), then divided by W;
+    groups are combined in ascending group id."""
+    f = np.float32
+    # row = worker, column = element; in column 0 group 0 holds (1, 1e8, -1e8): ascending
+    # order gives (1 + 1e8) - 1e8 = 0, the reverse order (-1e8 + 1e8) + 1 = 1
+    vals = np.array([[2.0, 1e8], [1.0, -3.0], [3.0, -1e8], [1e8, 7.0], [4.0, 2.5], [-1e8, 1e-3]],
+                    dtype=np.float32)
+    grads = [vals[w].copy() for w in range(6)]
+    gow = [1, 0, 1, 0, 1, 0]                      # group 0 = {1, 3, 5}, group 1 = {0, 2, 4}
+    gm = oracle.group_means(grads, gow, 2)
+    for i in range(2):
+        g = vals[:, i]
+        m0 = ((g[1] + g[3]) + g[5]) / f(3)
+        m1 = ((g[0] + g[2]) + g[4]) / f(3)
+        assert gm[0][i].tobytes() == f(m0).tobytes() and gm[1][i].tobytes() == f(m1).tobytes(), i
+        reversed_m0 = ((g[5] + g[3]) + g[1]) / f(3)
+        assert i != 0 or f(reversed_m0) != f(m0)      # the order is observable here
+    gbar = oracle.global_mean(gm)
+    assert gbar.tobytes() == ((gm[0] + gm[1]) / f(2)).tobytes()
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 5, 8, 13, 64, 100, 128, 255])
 def test_pairwise_error_bound(k):
     """|PW(x) - sum(x)| <= gamma_h * sum|x|, h = ceil(log2 k): the pairwise bound
