@@ -42,12 +42,19 @@ def parse_args(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="resnet50_flat")
+    ap.add_argument("--grouping", default=None, metavar="GxW",
+                    help="override the workload's grouping with G equal groups of W workers")
     ap.add_argument("--replicas", type=int, default=-1, help="replicas written per step (default N)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget")
     ap.add_argument("--no-r0", action="store_true", help="skip the secondary R=0 measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also launch a plain 1 GiB copy kernel (counter calibration)")
+    ap.add_argument("--reduction", choices=("mean_of_means", "literal"), default=None,
+                    help="fused step reduction (default: mean_of_means; literal for workloads "
+                         "with unequal subgroups)")
+    ap.add_argument("--broadcast-grad", action="store_true",
+                    help="fused step also writes the mean gradient into every worker buffer")
     ap.add_argument("--path", choices=("fused", "unfused"), default="fused",
                     help="fused: one lsgd_step per step; unfused: lsgd_group_mean, "
                          "lsgd_global_mean, lsgd_sgd_step per step (flat workloads)")
@@ -62,15 +69,20 @@ def parse_args(argv=None):
 class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
-    def __init__(self, wl, R, dev):
+    def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
-        from paper_1906_05936_amd._lib import lib, ptr_array, int32_array, check
+        from paper_1906_05936_amd._lib import lib, ptr_array, int32_array, check, StepOptions
 
         self.wl, self.R = wl, R
         N, G = wl.n_workers, wl.groups
-        self.gow = workloads.contiguous_groups(G, wl.workers_per_group)
+        self.gow = wl.group_of_worker()
+        if reduction is None:
+            reduction = "literal" if wl.group_sizes else "mean_of_means"
+        self.reduction, self.broadcast_grad = reduction, broadcast_grad
+        if wl.tensor_sizes and (reduction != "mean_of_means" or broadcast_grad):
+            raise SystemExit("plans run the mean-of-means step without broadcast")
         rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
         stream = torch.cuda.current_stream(dev)
         flat_p = workloads.init_params(wl, dev)
@@ -105,13 +117,20 @@ class Setup:
                 workloads.fill_worker_grad(wl, 0, w, g, scratch)
                 self.grads.append([g])
             self.reps = [[torch.empty(wl.n, device=dev, dtype=rtd)] for _ in range(R)]
-            fn = lib.lsgd_step
-            args = (self.params[0].data_ptr(), self.mom[0].data_ptr(),
-                    ptr_array([g[0].data_ptr() for g in self.grads]),
-                    1 if wl.grad_dtype == "bf16" else 0, N, int32_array(self.gow), G, wl.n,
-                    ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd),
-                    ptr_array([r[0].data_ptr() for r in self.reps]), R,
-                    1 if rtd == torch.bfloat16 else 0, ctypes.c_void_p(stream.cuda_stream))
+            common = (self.params[0].data_ptr(), self.mom[0].data_ptr(),
+                      ptr_array([g[0].data_ptr() for g in self.grads]),
+                      1 if wl.grad_dtype == "bf16" else 0, N, int32_array(self.gow), G, wl.n,
+                      ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd),
+                      ptr_array([r[0].data_ptr() for r in self.reps]), R,
+                      1 if rtd == torch.bfloat16 else 0)
+            if reduction == "mean_of_means" and not broadcast_grad:
+                fn = lib.lsgd_step
+                args = common + (ctypes.c_void_p(stream.cuda_stream),)
+            else:
+                self._opts = StepOptions(1 if reduction == "literal" else 0, 1 if broadcast_grad else 0,
+                                         None)
+                fn = lib.lsgd_step_ex
+                args = common + (ctypes.byref(self._opts), ctypes.c_void_p(stream.cuda_stream))
 
             def step():
                 check(fn(*args))
@@ -185,6 +204,8 @@ class UnfusedSetup:
             raise SystemExit("the unfused path is measured on flat workloads")
         self.wl, self.R = wl, R
         N, G = wl.n_workers, wl.groups
+        if wl.group_sizes:
+            raise SystemExit("the unfused calls take equal subgroups")
         self.gow = workloads.contiguous_groups(G, wl.workers_per_group)
         rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
         stream = torch.cuda.current_stream(dev)
@@ -276,13 +297,17 @@ def cpu_baseline(setup, seconds):
     steps = 0
     t0 = time.perf_counter()
     while True:
-        oracle.lsgd_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, reps, rdt)
+        if setup.reduction == "literal" or setup.broadcast_grad:
+            oracle.lsgd_step_literal(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, reps,
+                                     rdt, broadcast_grad=setup.broadcast_grad)
+        else:
+            oracle.lsgd_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, reps, rdt)
         steps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
             break
     elem_per_s = S * steps / el
-    per_elem = wl.algorithmic_bytes(R) / wl.n
+    per_elem = (wl.algorithmic_bytes(R) / wl.n + (4 * wl.n_workers if setup.broadcast_grad else 0))
     return {"value": round(elem_per_s * per_elem / 1e9, 4), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
             "steps_per_s": round(elem_per_s / wl.n, 6),
@@ -330,11 +355,12 @@ def _calib_kib(rows, counter):
     return sum(vals.values()) / len(vals), len(vals)
 
 
-def kernel_match(wl):
+def kernel_match(wl, reduction=None):
+    ct = (not wl.group_sizes and reduction != "literal" and wl.groups in (1, 2, 4, 8, 16)
+          and wl.workers_per_group in (1, 2, 4, 8, 16) and wl.n_workers <= 128)
     if wl.tensor_sizes:
-        return "step_plan_kernel"
-    return "step_flat_ct" if (wl.groups in (1, 2, 4, 8, 16) and
-                              wl.workers_per_group in (1, 2, 4, 8, 16)) else "step_flat_rt"
+        return "step_plan_kernel" if ct else "step_plan_seg"
+    return "step_flat_ct" if ct else "step_flat_seg"
 
 
 def derive_traffic(args):
@@ -343,7 +369,7 @@ def derive_traffic(args):
     1 GiB written) launched by --calibrate-copy."""
     import workloads
     from paper_1906_05936_amd import build as libbuild
-    wl = workloads.WORKLOADS[args.workload]
+    wl = workloads.resolve(args.workload, args.grouping)
     R = wl.n_workers if args.replicas < 0 else args.replicas
     fetch_rows = _read_counters(args.fetch_csv)
     write_rows = _read_counters(args.write_csv)
@@ -398,7 +424,7 @@ def main(argv=None):
     import torch
     import workloads
 
-    wl = workloads.WORKLOADS[args.workload]
+    wl = workloads.resolve(args.workload, args.grouping)
     R = wl.n_workers if args.replicas < 0 else args.replicas
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -430,9 +456,9 @@ def main(argv=None):
         }
         print(json.dumps(result), flush=True)
         return
-    setup = Setup(wl, R, dev)
+    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad)
     ms = time_steps(setup, args.steps, args.warmup)
-    alg = wl.algorithmic_bytes(R)
+    alg = wl.algorithmic_bytes(R) + (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0)
     gbps = alg / (ms * 1e-3) / 1e9
     traffic = stored_traffic(wl, R)
     result = {
@@ -443,21 +469,23 @@ def main(argv=None):
         "config": {"workload": wl.name, "n": wl.n, "groups": wl.groups,
                    "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                    "replicas": R, "replica_dtype": wl.replica_dtype,
-                   "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1},
+                   "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1,
+                   "reduction": setup.reduction, "broadcast_grad": setup.broadcast_grad,
+                   **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {})},
         "steps_per_s": round(1e3 / ms, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": alg,
-                     "kernel": kernel_match(wl)},
+                     "kernel": kernel_match(wl, setup.reduction)},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if R != 0 and not args.no_r0:
         setup.close()
         del setup
         torch.cuda.empty_cache()
-        setup = Setup(wl, 0, dev)
+        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad)
         ms0 = time_steps(setup, args.steps, args.warmup)
-        alg0 = wl.algorithmic_bytes(0)
+        alg0 = wl.algorithmic_bytes(0) + (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0)
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
                         "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),
                         "frac": round(alg0 / (ms0 * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}

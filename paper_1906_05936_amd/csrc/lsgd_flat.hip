@@ -2,6 +2,8 @@
 // lsgd_sgd_step and the fused lsgd_step over one flat parameter vector.
 #include <string.h>
 
+#include <algorithm>
+
 #include "lsgd_host.hpp"
 #include "lsgd_kernels.hpp"
 
@@ -45,7 +47,13 @@ FlatPick pick_flat(int W, int G) {
         case 16: k = pick_flat_g<GT, 16>(G); break;
     }
     if (k) return FlatPick{k, TileUnits<GT>::U};
-    return FlatPick{step_flat_rt<GT>, 1};
+    return FlatPick{nullptr, 1};
+}
+
+// Runtime group layouts: accumulator levels for the largest count.
+template <typename GT>
+FlatPick pick_flat_seg(int max_count) {
+    return FlatPick{seg_levels(max_count) == 5 ? step_flat_seg<GT, 5> : step_flat_seg<GT, 8>, 1};
 }
 
 using MeanKernel = void (*)(MeanArgs);
@@ -66,7 +74,7 @@ MeanPick pick_group_mean(int W) {
         case 8: return MeanPick{group_mean_kernel_ct<GT, 8, U>, U};
         case 16: return MeanPick{group_mean_kernel_ct<GT, 16, U>, U};
     }
-    return MeanPick{group_mean_kernel<GT>, 1};
+    return MeanPick{seg_levels(W) == 5 ? group_mean_kernel<GT, 5> : group_mean_kernel<GT, 8>, 1};
 }
 
 // Global mean: compile-time G for powers of two up to 128, else runtime G.
@@ -81,7 +89,7 @@ MeanPick pick_global_mean(int G) {
         case 64: return MeanPick{global_mean_kernel_ct<64, 2>, 2};
         case 128: return MeanPick{global_mean_kernel_ct<128, 2>, 2};
     }
-    return MeanPick{global_mean_kernel, 1};
+    return MeanPick{seg_levels(G) == 5 ? global_mean_kernel<5> : global_mean_kernel<8>, 1};
 }
 
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
@@ -195,12 +203,18 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    FlatPick k;
-    if (literal) {
-        for (int32_t j = 0; j <= n_groups; ++j) a.group_start[j] = static_cast<uint8_t>(gstart[j]);
-        k = FlatPick{gdt == LSGD_BF16 ? step_flat_literal<uint16_t> : step_flat_literal<float>, 1};
-    } else {
-        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    FlatPick k{nullptr, 1};
+    if (!literal) k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    if (!k.kernel) {
+        // runtime layout: group j is members [start[j], start[j+1]) of the member order
+        int32_t max_count = n_groups;
+        for (int32_t j = 0; j <= n_groups; ++j) {
+            const int32_t b = literal ? gstart[j] : j * a.W;
+            a.group_start[j] = static_cast<uint8_t>(b);
+            if (j > 0) max_count = std::max(max_count, b - static_cast<int32_t>(a.group_start[j - 1]));
+        }
+        a.literal = literal ? 1 : 0;
+        k = gdt == LSGD_BF16 ? pick_flat_seg<uint16_t>(max_count) : pick_flat_seg<float>(max_count);
     }
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;

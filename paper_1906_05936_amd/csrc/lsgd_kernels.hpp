@@ -207,6 +207,41 @@ __device__ __forceinline__ void store_replica(void* r, int rdt, int64_t e0, int 
     }
 }
 
+// One 16-byte gradient unit as raw bits (4 binary32 or 8 bfloat16 values), so
+// that a batch of loads in flight costs four registers each whatever the
+// dtype. TAIL units read cnt elements and leave the rest zero.
+template <typename GT, bool TAIL>
+__device__ __forceinline__ u32x4 load_raw(const void* g, int64_t e0, int cnt) {
+    const GT* p = static_cast<const GT*>(g) + e0;
+    if constexpr (!TAIL) {
+        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    } else {
+        constexpr int VEC = Unit<GT>::VEC;
+        uint32_t h[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            if constexpr (sizeof(GT) == 4) h[v] = v < cnt ? reinterpret_cast<const uint32_t*>(p)[v] : 0u;
+            else h[v] = v < cnt ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(p)[v]) : 0u;
+        }
+        if constexpr (sizeof(GT) == 4) return u32x4{h[0], h[1], h[2], h[3]};
+        else return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+    }
+}
+
+// Raw unit bits -> binary32 values (bfloat16 widening is exact).
+template <typename GT>
+__device__ __forceinline__ void widen(const u32x4& r, float (&x)[Unit<GT>::VEC]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(GT) == 4) {
+            x[q] = __uint_as_float(r[q]);
+        } else {
+            x[2 * q] = __uint_as_float(r[q] << 16);
+            x[2 * q + 1] = __uint_as_float(r[q] & 0xffff0000u);
+        }
+    }
+}
+
 // ------------------------------------------------------------- pairwise sums
 
 // Compile-time pairwise tree over leaves LO .. LO+CNT-1: leaf(k, x) produces the
@@ -278,23 +313,66 @@ __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x
 // Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
 
-// Runtime-count pairwise sum of `cnt` terms, loading up to 8 terms ahead so
-// that several 128-bit loads are in flight before they are folded in.
-template <int VEC, typename Load>
-__device__ __forceinline__ void pw_runtime(int cnt, const Load& load, float (&out)[VEC]) {
-    PwAcc<VEC> acc;
-    const int levels = acc_levels(cnt);
-    for (int k0 = 0; k0 < cnt; k0 += 8) {
-        float x[8][VEC];
+// Member gradients a lane holds in one register batch of the segmented sum.
+constexpr int kSegBatch = 8;
+
+// Pairwise sums of consecutive runs of the N member-ordered gradient units of
+// one lane, for group layouts known only at run time: group j holds members
+// [gs(j), gs(j+1)), j < G, and done(j, sum) receives PW over them. Loads run
+// ahead of the additions in two alternating register batches of kSegBatch
+// members that ignore group boundaries, so a lane keeps between one and two
+// batches of 128-bit loads in flight whatever the group sizes. Each group is
+// folded through a binary-counter accumulator (LV levels: sizes below 2^LV).
+// N, G and gs are uniform, so every branch here is uniform.
+template <typename GT, int LV, bool TAIL, typename Ptr, typename Start, typename Done>
+__device__ __forceinline__ void pw_segments(int N, int G, const Ptr& ptr, const Start& gs, int64_t e0,
+                                            int cnt, const Done& done) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int B = kSegBatch;
+    u32x4 xa[B], xb[B];
+    PwAcc<VEC, LV> acc;
+    int j = 0;
+    int gend = gs(1);
+    int lv = acc_levels(gend - gs(0));
+    auto fetch = [&](int k0, u32x4 (&x)[B]) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-            if (k0 + q < cnt) load(k0 + q, x[q]);
+        for (int q = 0; q < B; ++q)
+            if (k0 + q < N) x[q] = load_raw<GT, TAIL>(ptr(k0 + q), e0, cnt);
+    };
+    auto consume = [&](int k0, const u32x4 (&x)[B]) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-            if (k0 + q < cnt) acc.push(x[q], levels);
+        for (int q = 0; q < B; ++q) {
+            if (k0 + q < N) {
+                float v[VEC];
+                widen<GT>(x[q], v);
+                acc.push(v, lv);
+                if (k0 + q + 1 == gend) {
+                    float sum[VEC];
+                    acc.result(sum, lv);
+                    acc.count = 0;
+                    done(j, sum);
+                    if (++j < G) {
+                        const int gbeg = gend;
+                        gend = gs(j + 1);
+                        lv = acc_levels(gend - gbeg);
+                    }
+                }
+            }
+        }
+    };
+    fetch(0, xa);
+#pragma unroll 1
+    for (int k0 = 0; k0 < N; k0 += 2 * B) {
+        if (k0 + B < N) fetch(k0 + B, xb);
+        consume(k0, xa);
+        if (k0 + 2 * B < N) fetch(k0 + 2 * B, xa);
+        if (k0 + B < N) consume(k0 + B, xb);
     }
-    acc.result(out, levels);
 }
+
+// Accumulator levels for runtime counts up to `max_count` (host side): the
+// segmented kernels are built for 5 levels (counts up to 31) and 8 (255).
+__host__ __device__ constexpr int seg_levels(int max_count) { return max_count <= 31 ? 5 : 8; }
 
 // ------------------------------------------------------------- the update
 
@@ -331,7 +409,8 @@ struct StepArgs {
     uint32_t xcd_chunk, upl;
     const float* lr_ptr;   // non-null: the learning rate is read here when the kernel runs
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
-    uint8_t group_start[kMaxWorkers + 4];  // literal reduction: group j is members [start[j], start[j+1])
+    int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
+    uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
     const void* grads[kMaxWorkers];
     void* replicas[kMaxReplicas];
 };
@@ -394,12 +473,11 @@ __device__ __forceinline__ void pw_leaves(const Leaf& leaf, float (&out)[T]) {
     }
 }
 
-// Everything after the mean gradient, for a tile of U units: optional
-// broadcast of gbar into every worker's (binary32) gradient buffer, the
-// update, and the copy-out.
+// Optional broadcast of the mean gradient into every worker's (binary32)
+// gradient buffer.
 template <typename GT, int U, bool TAIL, typename Src>
-__device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U], int cnt,
-                                            float (&gbar)[U * Unit<GT>::VEC]) {
+__device__ __forceinline__ void broadcast_mean(const Src& s, const int64_t (&e0)[U], int cnt,
+                                               float (&gbar)[U * Unit<GT>::VEC]) {
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
     if constexpr (sizeof(GT) == 4) {
@@ -412,11 +490,24 @@ __device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U]
             }
         }
     }
-    float p[T], m[T];
+}
+
+template <int VEC, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void load_state(const Src& s, const int64_t (&e0)[U], int cnt,
+                                           float (&p)[U * VEC], float (&m)[U * VEC]) {
+    constexpr int T = U * VEC;
 #pragma unroll
     for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
 #pragma unroll
     for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+}
+
+// The update on loaded state, then parameters, momentum and replicas stored.
+template <int VEC, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void update_and_store(const Src& s, const int64_t (&e0)[U], int cnt,
+                                                 const float (&gbar)[U * VEC], float (&p)[U * VEC],
+                                                 float (&m)[U * VEC]) {
+    constexpr int T = U * VEC;
     sgd_update<T>(s.hyper(), gbar, p, m);
 #pragma unroll
     for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
@@ -429,6 +520,19 @@ __device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U]
 #pragma unroll
         for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(p, q));
     }
+}
+
+// Everything after the mean gradient, for a tile of U units: optional
+// broadcast, the update, and the copy-out.
+template <typename GT, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U], int cnt,
+                                            float (&gbar)[U * Unit<GT>::VEC]) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    broadcast_mean<GT, U, TAIL>(s, e0, cnt, gbar);
+    float p[T], m[T];
+    load_state<VEC, U, TAIL>(s, e0, cnt, p, m);
+    update_and_store<VEC, U, TAIL>(s, e0, cnt, gbar, p, m);
 }
 
 // Fused step on one tile of U units, compile-time W and G (powers of two).
@@ -467,55 +571,37 @@ __device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt)
     fused_tile_ct<GT, W, G, 1, TAIL>(s, e, cnt);
 }
 
-// Fused step on one unit, runtime W and G (any equal-size grouping).
-template <typename GT, bool TAIL, typename Src>
-__device__ __forceinline__ void fused_unit_rt(const Src& s, int W, int G, int64_t e0, int cnt) {
+// Fused step on one unit for group layouts known only at run time. Group j
+// is members [gs(j), gs(j+1)) of the member-ordered gradients. Mean of means
+// (literal = false, equal groups of W): each group's PW sum / W, PW over the G
+// results, / G. Paper-literal (any partition): each group's PW sum / N, PW
+// over the G results, no further division. Parameters and momentum are
+// loaded first so that their latency overlaps the gradient stream.
+template <typename GT, int LV, bool TAIL, typename Src, typename Start>
+__device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                               int64_t e0, int cnt) {
     constexpr int VEC = Unit<GT>::VEC;
-    const float wf = static_cast<float>(W), gf = static_cast<float>(G);
-    PwAcc<VEC> groups;
+    const int64_t e[1] = {e0};
+    float p[VEC], m[VEC];
+    load_state<VEC, 1, TAIL>(s, e, cnt, p, m);
+    const float dg = static_cast<float>(literal ? N : gs(1) - gs(0));
+    PwAcc<VEC, LV> groups;
     const int glevels = acc_levels(G);
-    for (int j = 0; j < G; ++j) {
-        float gm[VEC];
-        pw_runtime<VEC>(W, [&](int k, float (&x)[VEC]) {
-            load_grad<GT, TAIL>(s.grad(j * W + k), e0, cnt, x);
-        }, gm);
+    pw_segments<GT, LV, TAIL>(N, G, [&](int k) { return s.grad(k); }, gs, e0, cnt,
+                              [&](int, float (&sum)[VEC]) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) gm[v] = gm[v] / wf;
-        groups.push(gm, glevels);
-    }
+                                  for (int v = 0; v < VEC; ++v) sum[v] = sum[v] / dg;
+                                  groups.push(sum, glevels);
+                              });
     float gbar[VEC];
     groups.result(gbar, glevels);
+    if (!literal) {
+        const float gf = static_cast<float>(G);
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
-    const int64_t e[1] = {e0};
-    finish_tile<GT, 1, TAIL>(s, e, cnt, gbar);
-}
-
-// Fused step on one unit with the paper-literal reduction: group j (members
-// start[j] .. start[j+1] in member order, any non-empty size) contributes its
-// pairwise sum divided by N, and the group contributions are summed pairwise
-// without a further division.
-template <typename GT, bool TAIL, typename Src>
-__device__ __forceinline__ void fused_unit_literal(const Src& s, const uint8_t* start, int N, int G,
-                                                   int64_t e0, int cnt) {
-    constexpr int VEC = Unit<GT>::VEC;
-    const float nf = static_cast<float>(N);
-    PwAcc<VEC> groups;
-    const int glevels = acc_levels(G);
-    for (int j = 0; j < G; ++j) {
-        const int off = start[j];
-        float part[VEC];
-        pw_runtime<VEC>(start[j + 1] - off, [&](int k, float (&x)[VEC]) {
-            load_grad<GT, TAIL>(s.grad(off + k), e0, cnt, x);
-        }, part);
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) part[v] = part[v] / nf;
-        groups.push(part, glevels);
+        for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
     }
-    float gbar[VEC];
-    groups.result(gbar, glevels);
-    const int64_t e[1] = {e0};
-    finish_tile<GT, 1, TAIL>(s, e, cnt, gbar);
+    broadcast_mean<GT, 1, TAIL>(s, e, cnt, gbar);
+    update_and_store<VEC, 1, TAIL>(s, e, cnt, gbar, p, m);
 }
 
 // Pointer source for the planless fused step: everything from StepArgs.
@@ -554,27 +640,20 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
         });
 }
 
-template <typename GT>
-__global__ __launch_bounds__(kBlock) void step_flat_literal(StepArgs a) {
+// Runtime group layouts (non-power-of-two or large counts, and the
+// paper-literal reduction): group j is members [group_start[j],
+// group_start[j+1]) of the member-ordered pointer table.
+template <typename GT, int LV>
+__global__ __launch_bounds__(kBlock) void step_flat_seg(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
+    const bool literal = a.literal != 0;
+    auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
     for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) fused_unit_literal<GT, false>(s, a.group_start, a.n_workers, a.n_groups, u * VEC, VEC);
-        else fused_unit_literal<GT, true>(s, a.group_start, a.n_workers, a.n_groups, u * VEC, rem);
-    });
-}
-
-template <typename GT>
-__global__ __launch_bounds__(kBlock) void step_flat_rt(StepArgs a) {
-    constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
-    const int64_t full = a.n / VEC;
-    const int rem = static_cast<int>(a.n - full * VEC);
-    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) fused_unit_rt<GT, false>(s, a.W, a.n_groups, u * VEC, VEC);
-        else fused_unit_rt<GT, true>(s, a.W, a.n_groups, u * VEC, rem);
+        if (u < full) fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, VEC);
+        else fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, rem);
     });
 }
 
@@ -614,29 +693,27 @@ __global__ __launch_bounds__(kBlock) void group_mean_kernel_ct(MeanArgs a) {
 }
 
 // lsgd_group_mean, runtime W (any equal-size grouping), one unit.
-template <typename GT, bool TAIL>
+template <typename GT, int LV, bool TAIL>
 __device__ __forceinline__ void group_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
     constexpr int VEC = Unit<GT>::VEC;
-    const float wf = static_cast<float>(a.W);
-    for (int j = 0; j < a.n_groups; ++j) {
-        float gm[VEC];
-        pw_runtime<VEC>(a.W, [&](int k, float (&x)[VEC]) {
-            load_grad<GT, TAIL>(a.in[j * a.W + k], e0, cnt, x);
-        }, gm);
+    const int W = a.W;
+    const float wf = static_cast<float>(W);
+    pw_segments<GT, LV, TAIL>(a.n_workers, a.n_groups, [&](int k) { return a.in[k]; },
+                              [&](int j) { return j * W; }, e0, cnt, [&](int j, float (&sum)[VEC]) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) gm[v] = gm[v] / wf;
-        store_f32<VEC, TAIL>(a.out[j], e0, cnt, gm);
-    }
+                                  for (int v = 0; v < VEC; ++v) sum[v] = sum[v] / wf;
+                                  store_f32<VEC, TAIL>(a.out[j], e0, cnt, sum);
+                              });
 }
 
-template <typename GT>
+template <typename GT, int LV>
 __global__ __launch_bounds__(kBlock) void group_mean_kernel(MeanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) group_mean_unit<GT, false>(a, u * VEC, VEC);
-        else group_mean_unit<GT, true>(a, u * VEC, rem);
+        if (u < full) group_mean_unit<GT, LV, false>(a, u * VEC, VEC);
+        else group_mean_unit<GT, LV, true>(a, u * VEC, rem);
     });
 }
 
@@ -671,25 +748,26 @@ __global__ __launch_bounds__(kBlock) void global_mean_kernel_ct(MeanArgs a) {
         });
 }
 
-// lsgd_global_mean, runtime G, one unit.
-template <bool TAIL>
+// lsgd_global_mean, runtime G, one unit: the G means form one run.
+template <int LV, bool TAIL>
 __device__ __forceinline__ void global_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
-    float s[4];
-    pw_runtime<4>(a.n_groups, [&](int j, float (&x)[4]) {
-        load_f32<4, TAIL>(static_cast<const float*>(a.in[j]), e0, cnt, x);
-    }, s);
-    const float gf = static_cast<float>(a.n_groups);
+    const int G = a.n_groups;
+    const float gf = static_cast<float>(G);
+    pw_segments<float, LV, TAIL>(G, 1, [&](int j) { return a.in[j]; }, [&](int j) { return j * G; },
+                                 e0, cnt, [&](int, float (&sum)[4]) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) s[v] = s[v] / gf;
-    store_f32<4, TAIL>(a.out[0], e0, cnt, s);
+                                     for (int v = 0; v < 4; ++v) sum[v] = sum[v] / gf;
+                                     store_f32<4, TAIL>(a.out[0], e0, cnt, sum);
+                                 });
 }
 
-static __global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) {
+template <int LV>
+__global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) {
     const int64_t full = a.n / 4;
     const int rem = static_cast<int>(a.n - full * 4);
     for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) global_mean_unit<false>(a, u * 4, 4);
-        else global_mean_unit<true>(a, u * 4, rem);
+        if (u < full) global_mean_unit<LV, false>(a, u * 4, 4);
+        else global_mean_unit<LV, true>(a, u * 4, rem);
     });
 }
 
@@ -775,10 +853,9 @@ struct PlanSrc {
 
 // One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
 // (one large piece, or several small tensors). Chunk and pointer-table reads
-// are uniform per workgroup.
-template <typename GT, int W, int G, int U>
-__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
-    constexpr int VEC = Unit<GT>::VEC;
+// are uniform per workgroup. chunk(s, ch) processes one chunk.
+template <typename ChunkFn>
+__device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn& chunk) {
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
     if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
     const Hyper h = resolve_hyper(a.h, a.lr_ptr);
@@ -786,30 +863,47 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     for (int32_t c = a.bucket_begin[b]; c < c_end; ++c) {
         const PlanChunk ch = a.chunks[c];
         const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
+        chunk(s, ch);
+    }
+}
+
+// Compile-time (W, G): tiles of U units kBlock apart, then the units of a
+// partial last tile, then the ragged end (thread 0).
+template <typename GT, int W, int G, int U>
+__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch) {
         const int64_t full = ch.len / VEC;
-        if constexpr (W > 0) {
-            // tiles of U units kBlock apart, then the units of a partial last tile
-            for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
-                if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
-                    int64_t e0[U];
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
 #pragma unroll
-                    for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
-                    fused_tile_ct<GT, W, G, U, false>(s, e0, VEC);
-                } else {
-                    for (int64_t u = t0; u < full; u += kBlock)
-                        fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
-                }
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                fused_tile_ct<GT, W, G, U, false>(s, e0, VEC);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock)
+                    fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
             }
-        } else {
-            for (int64_t u = threadIdx.x; u < full; u += kBlock)
-                fused_unit_rt<GT, false>(s, a.W, a.n_groups, ch.start + u * VEC, VEC);
         }
         const int rem = static_cast<int>(ch.len - full * VEC);
-        if (rem != 0 && threadIdx.x == 0) {
-            if constexpr (W > 0) fused_unit_ct<GT, W, G, true>(s, ch.start + full * VEC, rem);
-            else fused_unit_rt<GT, true>(s, a.W, a.n_groups, ch.start + full * VEC, rem);
-        }
-    }
+        if (rem != 0 && threadIdx.x == 0) fused_unit_ct<GT, W, G, true>(s, ch.start + full * VEC, rem);
+    });
+}
+
+// Runtime W and G (any equal-size grouping): one unit per lane.
+template <typename GT, int LV>
+__global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int W = a.W;
+    auto gs = [&](int j) { return j * W; };
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch) {
+        const int64_t full = ch.len / VEC;
+        for (int64_t u = threadIdx.x; u < full; u += kBlock)
+            fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, false, ch.start + u * VEC, VEC);
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0)
+            fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, false, ch.start + full * VEC, rem);
+    });
 }
 
 }  // namespace lsgd

@@ -63,7 +63,8 @@ PlanKernel pick_plan(int W, int G) {
         case 8: k = pick_plan_g<GT, 8>(G); break;
         case 16: k = pick_plan_g<GT, 16>(G); break;
     }
-    return k ? k : step_plan_kernel<GT, 0, 0, 1>;
+    if (k) return k;
+    return seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>;
 }
 
 void free_plan(lsgd_plan* p) {

@@ -461,6 +461,10 @@ def test_workload_shapes():
     for wl in workloads.WORKLOADS.values():
         if wl.tensor_sizes:
             assert sum(wl.tensor_sizes) == wl.n
+    uneq = workloads.WORKLOADS["resnet50_unequal"]
+    gow = uneq.group_of_worker()
+    assert uneq.n_workers == 16 and len(gow) == 16 and sorted(set(gow)) == [0, 1, 2, 3]
+    assert [gow.count(j) for j in range(4)] == [2, 3, 5, 6]
     big = workloads.WORKLOADS["large"]
     assert big.n_workers == 64 and big.algorithmic_bytes(0) == big.n * (64 * 2 + 16)
 

@@ -320,15 +320,17 @@ def test_bf16_gradients_within_2e3_of_fp32_gradients():
 
 # ---------------------------------------------------------------- full-size workloads
 
-@pytest.mark.parametrize("name", workloads.ORDER)
+@pytest.mark.parametrize("name", workloads.ORDER + ["resnet50_unequal"])
 def test_workload_full_size_sampled(name):
     """Each workload at its full size and step count, R = N replicas, in the
     benchmark's launch configuration. Inputs are regenerated every step; the
-    oracle follows the sampled elements (all of them for the tiny workload)."""
+    oracle follows the sampled elements (all of them for the tiny workload).
+    Unequal subgroups take the paper-literal reduction."""
     wl = workloads.WORKLOADS[name]
     N, G, W = wl.n_workers, wl.groups, wl.workers_per_group
     log("workload %s: n=%d G=%d W=%d %s steps=%d" % (name, wl.n, G, W, wl.grad_dtype, wl.steps))
-    gow = workloads.contiguous_groups(G, W)
+    gow = wl.group_of_worker()
+    literal = bool(wl.group_sizes)
     rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
     R = N
     flat_p = workloads.init_params(wl, DEV)
@@ -376,10 +378,11 @@ def test_workload_full_size_sampled(name):
             plan.step(wl.lr, wl.mu, wl.wd)
         else:
             lsgd.step(params[0], mom[0], [g[0] for g in grads], gow, G, wl.lr, wl.mu, wl.wd,
-                      [r[0] for r in reps])
+                      [r[0] for r in reps], reduction="literal" if literal else "mean_of_means")
         rr = [np.zeros(idx.size, np.uint16 if rtd == torch.bfloat16 else np.float32) for _ in range(R)]
-        oracle.lsgd_step(p_ref, m_ref, g_ref, gow, G, wl.lr, wl.mu, wl.wd, rr,
-                         oracle.BF16 if rtd == torch.bfloat16 else oracle.F32)
+        ref_step = oracle.lsgd_step_literal if literal else oracle.lsgd_step
+        ref_step(p_ref, m_ref, g_ref, gow, G, wl.lr, wl.mu, wl.wd, rr,
+                 oracle.BF16 if rtd == torch.bfloat16 else oracle.F32)
         torch.cuda.synchronize()
         assert_close(gather(params), p_ref, "%s params step %d" % (name, step))
         assert_close(gather(mom), m_ref, "%s momentum step %d" % (name, step))

@@ -67,10 +67,19 @@ class Workload:
     seed: int
     scale_range: Optional[Tuple[float, float]] = None   # per-worker, per-step U(lo, hi) scale
     tensor_sizes: Optional[Tuple[int, ...]] = None      # multi-tensor layout
+    group_sizes: Optional[Tuple[int, ...]] = None       # unequal subgroups (literal reduction only)
 
     @property
     def n_workers(self) -> int:
+        if self.group_sizes:
+            return sum(self.group_sizes)
         return self.groups * self.workers_per_group
+
+    def group_of_worker(self) -> List[int]:
+        """Worker i's group: contiguous groups of the given (or equal) sizes."""
+        if self.group_sizes:
+            return [j for j, c in enumerate(self.group_sizes) for _ in range(c)]
+        return contiguous_groups(self.groups, self.workers_per_group)
 
     @property
     def grad_bytes(self) -> int:
@@ -107,8 +116,21 @@ WORKLOADS = {
                      seed=1004, scale_range=(0.5, 2.0)),
     "large": Workload("large", 350_000_000, 8, 8, "bf16", 0.02, 1e-3, 0.05, 0.9, 1e-4, 10,
                       seed=1005),
+    # 16 workers in subgroups of 2, 3, 5 and 6 (nodes of unequal size): the
+    # paper-literal reduction, whose exact value is still the flat mean
+    "resnet50_unequal": Workload("resnet50_unequal", RESNET50_NUMEL, 4, 0, "f32", 0.05, 1e-2, 0.1,
+                                 0.9, 1e-4, 100, seed=1006, group_sizes=(2, 3, 5, 6)),
 }
 ORDER = ["tiny", "resnet50_flat", "resnet50_tensors", "wide", "large"]
+
+
+def resolve(name: str, grouping: Optional[str] = None) -> Workload:
+    """A named workload, optionally regrouped as "GxW" (G equal groups of W)."""
+    wl = WORKLOADS[name]
+    if grouping:
+        g, w = (int(x) for x in grouping.lower().split("x"))
+        wl = wl.with_(name="%s_%dx%d" % (name, g, w), groups=g, workers_per_group=w, group_sizes=None)
+    return wl
 
 
 def _splitmix64(x: int) -> int:
