@@ -5,8 +5,8 @@
  * Method: K. Yu, T. Flynn, S. Yoo, N. D'Imperio, "Layered SGD: A Decentralized
  * and Synchronous SGD Algorithm for Scalable Deep Neural Network Training",
  * arXiv 1906.05936. N = G*W workers each hold a gradient of the flat parameter
- * vector w (Sec. 3, Alg. 2, "Delta w^i"). The workers are partitioned into G
- * equal subgroups (Alg. 3 require line: worker index i, node index j of G nodes;
+ * vector w (Sec. 3, Alg. 2: Δw^i of worker i). The workers are partitioned into G
+ * equal subgroups (the inputs Alg. 3 declares: worker index i, node index j of G nodes;
  * Sec. 3: equal-cardinality partition). Per element, with PW the fixed pairwise
  * sum described below:
  *

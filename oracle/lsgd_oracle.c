@@ -10,15 +10,15 @@
  * arXiv 1906.05936.
  *
  * What is computed, per parameter element, with N = G*W workers:
- *   1. subgroup means   m_j  = PW(g_{members[j][0..W)}) / W       (Alg. 3, "Reduce
- *                             to the communicator and divide"; Sec. 4.1 flow item 1)
- *   2. global mean      gbar = PW(m_0 .. m_{G-1}) / G              (Alg. 3, "Allreduce
- *                             over communicators"; Sec. 4.1 flow item 2)
+ *   1. subgroup means   m_j  = PW(g_{members[j][0..W)}) / W       (Alg. 3, reduce
+ *                             step at the communicator; Sec. 4.1 flow item 1)
+ *   2. global mean      gbar = PW(m_0 .. m_{G-1}) / G              (Alg. 3, allreduce
+ *                             step among communicators; Sec. 4.1 flow item 2)
  *   3. update           d = gbar + wd*p;  mom = mu*mom + d;  p = p - lr*mom
  *                             (Alg. 3 update step, in the epsilon-step form of
  *                             Alg. 1/2; momentum and weight decay from Sec. 5.3)
  *   4. copy-out         replica_r = p  (or its bfloat16 rounding)
- *                             (Alg. 3 "Broadcast to the workers from the communicator")
+ *                             (Alg. 3, broadcast step from the communicator to its workers)
  * PW is the pairwise sum: PW(x[0..k)) = x[0] if k == 1, else
  * PW(x[0..h)) + PW(x[h..k)) with h the largest power of two below k. Members of a
  * group are taken in ascending worker id, groups in ascending group id. Equal
@@ -48,7 +48,7 @@ enum { ORACLE_OK = 0, ORACLE_ERR_NULL = 1, ORACLE_ERR_SIZE = 2, ORACLE_ERR_GROUP
 enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
 
 /*
- * Subgroup indexing (Alg. 3 require line: worker index i of N, node index j of G;
+ * Subgroup indexing (the inputs Alg. 3 declares: worker index i of N, node index j of G;
  * Sec. 3: equal-cardinality partition; Sec. 5.1: four workers per node).
  * group_of_worker[i] in [0, G) names worker i's group. On success members holds
  * G rows of W = N/G worker ids, each row in ascending worker id.

@@ -115,6 +115,29 @@ __device__ __forceinline__ float (&slice(float (&x)[T], int q))[VEC] {
 
 // ---------------------------------------------------------------- loads/stores
 
+// Address-space views. Every buffer the kernels read or write is device
+// global memory: accessing it through a global-space pointer gives the
+// global_load / global_store forms, also for pointers the kernel itself read
+// from a table (for those the compiler would otherwise use the generic flat
+// forms). Tables that no kernel writes (the plans' chunk and pointer tables)
+// are read through the constant space, so that they become scalar loads
+// instead of vector loads the compiler must order after every store.
+#define LSGD_GLOBAL __attribute__((address_space(1)))
+#define LSGD_CONST __attribute__((address_space(4)))
+
+template <typename T>
+__device__ __forceinline__ const LSGD_GLOBAL T* gload_ptr(const void* p) {
+    return (const LSGD_GLOBAL T*)(p);
+}
+template <typename T>
+__device__ __forceinline__ LSGD_GLOBAL T* gstore_ptr(void* p) {
+    return (LSGD_GLOBAL T*)(p);
+}
+template <typename T>
+__device__ __forceinline__ T read_table(const T* p) {
+    return *(const LSGD_CONST T*)(p);
+}
+
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
 
 // binary32 -> bfloat16 bits, nearest-even via the carry of a 0x7fff(+1 if odd)
@@ -135,14 +158,14 @@ __device__ __forceinline__ void load_grad(const void* g, int64_t e0, int cnt,
     if constexpr (TAIL) {
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
-            if constexpr (sizeof(GT) == 4) x[v] = v < cnt ? reinterpret_cast<const float*>(p)[v] : 0.f;
-            else x[v] = v < cnt ? bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(p)[v]) : 0.f;
+            if constexpr (sizeof(GT) == 4) x[v] = v < cnt ? gload_ptr<float>(p)[v] : 0.f;
+            else x[v] = v < cnt ? bf16_bits_to_f32(gload_ptr<uint16_t>(p)[v]) : 0.f;
         }
     } else if constexpr (sizeof(GT) == 4) {
-        f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+        f32x4 t = __builtin_nontemporal_load(gload_ptr<f32x4>(p));
         x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
     } else {
-        u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        u32x4 t = __builtin_nontemporal_load(gload_ptr<u32x4>(p));
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             x[2 * q] = __uint_as_float(t[q] << 16);
@@ -156,11 +179,11 @@ template <int VEC, bool TAIL>
 __device__ __forceinline__ void load_f32(const float* p, int64_t e0, int cnt, float (&x)[VEC]) {
     if constexpr (TAIL) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) x[v] = v < cnt ? p[e0 + v] : 0.f;
+        for (int v = 0; v < VEC; ++v) x[v] = v < cnt ? gload_ptr<float>(p + e0)[v] : 0.f;
     } else {
 #pragma unroll
         for (int q = 0; q < VEC / 4; ++q) {
-            f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + e0) + q);
+            f32x4 t = __builtin_nontemporal_load(gload_ptr<f32x4>(p + e0) + q);
             x[4 * q] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
         }
     }
@@ -171,12 +194,12 @@ __device__ __forceinline__ void store_f32(float* p, int64_t e0, int cnt, const f
     if constexpr (TAIL) {
 #pragma unroll
         for (int v = 0; v < VEC; ++v)
-            if (v < cnt) p[e0 + v] = x[v];
+            if (v < cnt) gstore_ptr<float>(p + e0)[v] = x[v];
     } else {
 #pragma unroll
         for (int q = 0; q < VEC / 4; ++q) {
             f32x4 t = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
-            __builtin_nontemporal_store(t, reinterpret_cast<f32x4*>(p + e0) + q);
+            __builtin_nontemporal_store(t, gstore_ptr<f32x4>(p + e0) + q);
         }
     }
 }
@@ -193,17 +216,17 @@ __device__ __forceinline__ void store_replica(void* r, int rdt, int64_t e0, int 
     if constexpr (TAIL) {
 #pragma unroll
         for (int v = 0; v < VEC; ++v)
-            if (v < cnt) h[v] = static_cast<uint16_t>(f32_to_bf16_bits(x[v]));
+            if (v < cnt) gstore_ptr<uint16_t>(h)[v] = static_cast<uint16_t>(f32_to_bf16_bits(x[v]));
     } else if constexpr (VEC == 4) {
         u32x2 t = {f32_to_bf16_bits(x[0]) | (f32_to_bf16_bits(x[1]) << 16),
                    f32_to_bf16_bits(x[2]) | (f32_to_bf16_bits(x[3]) << 16)};
-        __builtin_nontemporal_store(t, reinterpret_cast<u32x2*>(h));
+        __builtin_nontemporal_store(t, gstore_ptr<u32x2>(h));
     } else {
         u32x4 t;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
             t[q] = f32_to_bf16_bits(x[2 * q]) | (f32_to_bf16_bits(x[2 * q + 1]) << 16);
-        __builtin_nontemporal_store(t, reinterpret_cast<u32x4*>(h));
+        __builtin_nontemporal_store(t, gstore_ptr<u32x4>(h));
     }
 }
 
@@ -214,14 +237,14 @@ template <typename GT, bool TAIL>
 __device__ __forceinline__ u32x4 load_raw(const void* g, int64_t e0, int cnt) {
     const GT* p = static_cast<const GT*>(g) + e0;
     if constexpr (!TAIL) {
-        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        return __builtin_nontemporal_load(gload_ptr<u32x4>(p));
     } else {
         constexpr int VEC = Unit<GT>::VEC;
         uint32_t h[VEC];
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
-            if constexpr (sizeof(GT) == 4) h[v] = v < cnt ? reinterpret_cast<const uint32_t*>(p)[v] : 0u;
-            else h[v] = v < cnt ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(p)[v]) : 0u;
+            if constexpr (sizeof(GT) == 4) h[v] = v < cnt ? gload_ptr<uint32_t>(p)[v] : 0u;
+            else h[v] = v < cnt ? static_cast<uint32_t>(gload_ptr<uint16_t>(p)[v]) : 0u;
         }
         if constexpr (sizeof(GT) == 4) return u32x4{h[0], h[1], h[2], h[3]};
         else return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
@@ -840,10 +863,10 @@ struct PlanSrc {
     void* const* t;  // this tensor's row of the pointer table
     const PlanArgs& a;
     Hyper h;
-    __device__ const void* grad(int k) const { return t[2 + k]; }
-    __device__ float* p() const { return static_cast<float*>(t[0]); }
-    __device__ float* m() const { return static_cast<float*>(t[1]); }
-    __device__ void* replica(int r) const { return t[2 + a.n_workers + r]; }
+    __device__ const void* grad(int k) const { return read_table(&t[2 + k]); }
+    __device__ float* p() const { return static_cast<float*>(read_table(&t[0])); }
+    __device__ float* m() const { return static_cast<float*>(read_table(&t[1])); }
+    __device__ void* replica(int r) const { return read_table(&t[2 + a.n_workers + r]); }
     __device__ int n_replicas() const { return a.n_replicas; }
     __device__ int rdt() const { return a.rdt; }
     __device__ Hyper hyper() const { return h; }
@@ -859,9 +882,10 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
     if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
     const Hyper h = resolve_hyper(a.h, a.lr_ptr);
-    const int32_t c_end = a.bucket_begin[b + 1];
-    for (int32_t c = a.bucket_begin[b]; c < c_end; ++c) {
-        const PlanChunk ch = a.chunks[c];
+    const int32_t c_end = read_table(&a.bucket_begin[b + 1]);
+    for (int32_t c = read_table(&a.bucket_begin[b]); c < c_end; ++c) {
+        const PlanChunk* cp = &a.chunks[c];
+        const PlanChunk ch{read_table(&cp->tensor), 0, read_table(&cp->start), read_table(&cp->len)};
         const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
         chunk(s, ch);
     }

@@ -3,8 +3,9 @@
 //
 // lsgd_plan_create cuts every tensor into pieces of P workgroup tile passes
 // (256 lanes x the kernel's lane tile: 2048 elements for binary32 and bf16
-// gradients alike, times P = the launch shape's passes per workgroup at plan
-// creation, 1 by default), starting on unit boundaries, then packs consecutive pieces
+// gradients alike with the compile-time kernels, 1024 (binary32) or 2048
+// (bf16) with the runtime-layout kernel, times P = the launch shape's passes
+// per workgroup at plan creation, 1 by default), starting on unit boundaries, then packs consecutive pieces
 // into buckets of at most one piece: a large tensor yields one bucket per piece
 // (so it is walked exactly like the flat kernel walks a vector), while runs of
 // small tensors (ResNet-50's 64..1024-element batch-norm and bias vectors)
@@ -31,13 +32,19 @@ struct lsgd_plan {
 namespace lsgd {
 namespace {
 
-// Elements per piece and per bucket: one tile pass of the compile-time kernel.
-template <typename GT>
-constexpr int64_t piece_elems() { return static_cast<int64_t>(kBlock) * Unit<GT>::VEC * TileUnits<GT>::U; }
-static_assert(piece_elems<float>() % 8 == 0 && piece_elems<uint16_t>() % 8 == 0,
-              "pieces must start on unit boundaries");
-
 using PlanKernel = void (*)(PlanArgs);
+
+// A kernel and the units per lane tile it processes.
+struct PlanPick {
+    PlanKernel kernel;
+    int tile;
+};
+
+// Elements per piece and per bucket: one tile pass of the plan's kernel.
+template <typename GT>
+constexpr int64_t piece_elems(int tile) { return static_cast<int64_t>(kBlock) * Unit<GT>::VEC * tile; }
+static_assert(piece_elems<float>(1) % 8 == 0 && piece_elems<uint16_t>(1) % 8 == 0,
+              "pieces must start on unit boundaries");
 
 template <typename GT, int W>
 PlanKernel pick_plan_g(int G) {
@@ -54,7 +61,7 @@ PlanKernel pick_plan_g(int G) {
 }
 
 template <typename GT>
-PlanKernel pick_plan(int W, int G) {
+PlanPick pick_plan(int W, int G) {
     PlanKernel k = nullptr;
     switch (W) {
         case 1: k = pick_plan_g<GT, 1>(G); break;
@@ -63,8 +70,8 @@ PlanKernel pick_plan(int W, int G) {
         case 8: k = pick_plan_g<GT, 8>(G); break;
         case 16: k = pick_plan_g<GT, 16>(G); break;
     }
-    if (k) return k;
-    return seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>;
+    if (k) return PlanPick{k, TileUnits<GT>::U};
+    return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>, 1};
 }
 
 void free_plan(lsgd_plan* p) {
@@ -108,7 +115,9 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     std::vector<PlanChunk> chunks;
     std::vector<int32_t> bucket_begin;
     // one tile pass of the kernel, times the launch shape's passes per workgroup
-    const int64_t kPiece = (gdt == LSGD_BF16 ? piece_elems<uint16_t>() : piece_elems<float>()) *
+    const int32_t W = n_workers / n_groups;
+    const int tile = gdt == LSGD_BF16 ? pick_plan<uint16_t>(W, n_groups).tile : pick_plan<float>(W, n_groups).tile;
+    const int64_t kPiece = (gdt == LSGD_BF16 ? piece_elems<uint16_t>(tile) : piece_elems<float>(tile)) *
                            launch_passes_per_block();
     int64_t bucket_fill = kPiece;  // forces a new bucket at the first piece
     for (int32_t t = 0; t < n_tensors; ++t) {
@@ -223,8 +232,8 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
     const LaunchShape ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
     a.xcd_chunk = ls.xcd_chunk;
-    PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups)
-                                          : pick_plan<float>(plan->W, plan->n_groups);
+    const PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
+                                                : pick_plan<float>(plan->W, plan->n_groups).kernel;
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     return check_launch("lsgd_step_plan");
 }
