@@ -64,6 +64,11 @@ def _configure(lib):
         f = getattr(lib, "oracle_lsgd_step_literal" + sfx)
         f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, P, i32, c_int, c_int]
         f.restype = c_int
+        f = getattr(lib, "oracle_lars_trust" + sfx)
+        f.argtypes, f.restype = [P, P, i64, real, real], real
+        f = getattr(lib, "oracle_lars_step" + sfx)
+        f.argtypes = [P, P, P, c_int, i32, P, i32, i64, real, real, real, real, P, i32, c_int, P]
+        f.restype = c_int
     return lib
 
 
@@ -250,3 +255,31 @@ def lsgd_step_literal(p, mom, grads, group_of_worker, n_groups, lr, mu, wd, repl
         p.size, lr, mu, wd, _ptr_array(list(replicas)) if replicas else None, len(replicas), rdt,
         1 if broadcast_grad else 0)
     _check(st, "lsgd_step_literal")
+
+
+def lars_trust(p, gbar, wd, eta):
+    """LARS trust ratio of one tensor: eta*||p|| / (||gbar|| + wd*||p||), 1 when
+    a norm is zero; norms in binary64, the result rounded once."""
+    lib = _load()
+    p = np.ascontiguousarray(p)
+    gbar = np.ascontiguousarray(gbar, dtype=p.dtype)
+    assert p.size == gbar.size
+    return getattr(lib, "oracle_lars_trust" + _sfx(p.dtype))(_ptr(p), _ptr(gbar), p.size, wd, eta)
+
+
+def lars_step(p, mom, grads, group_of_worker, n_groups, lr, mu, wd, eta, replicas=(), rdt=F32):
+    """One LARS step of one tensor in place on p and mom (mean-of-means
+    aggregation, trust-scaled update, copy-out); returns the trust ratio."""
+    lib = _load()
+    assert p.flags.c_contiguous and mom.flags.c_contiguous and mom.dtype == p.dtype
+    grads = [np.ascontiguousarray(g) for g in grads]
+    for g in grads:
+        assert g.size == p.size
+    gow = np.ascontiguousarray(group_of_worker, dtype=np.int32)
+    trust = np.zeros(1, dtype=p.dtype)
+    st = getattr(lib, "oracle_lars_step" + _sfx(p.dtype))(
+        _ptr(p), _ptr(mom), _ptr_array(grads), _gdt(grads) if grads else F32, len(grads),
+        _ptr(gow), n_groups, p.size, lr, mu, wd, eta,
+        _ptr_array(list(replicas)) if replicas else None, len(replicas), rdt, _ptr(trust))
+    _check(st, "lars_step")
+    return float(trust[0])

@@ -21,7 +21,7 @@ def build(verbose: bool = False, src_dir: str = HERE, out: str = LIB, cflags=Non
     directory's source and library)."""
     src = os.path.join(src_dir, "lsgd_oracle.c")
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = ["gcc"] + (cflags if cflags is not None else CFLAGS) + ["-shared", "-fPIC", "-o", tmp, src]
+    cmd = ["gcc"] + (cflags if cflags is not None else CFLAGS) + ["-shared", "-fPIC", "-o", tmp, src, "-lm"]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
     subprocess.run(cmd, check=True, cwd=src_dir)

@@ -19,6 +19,9 @@
  *                             Alg. 1/2; momentum and weight decay from Sec. 5.3)
  *   4. copy-out         replica_r = p  (or its bfloat16 rounding)
  *                             (Alg. 3, broadcast step from the communicator to its workers)
+ *   LARS (optional)     step 3 with d scaled by a per-tensor trust ratio (Sec. 2 and
+ *                             Sec. 6 name LARS; its definition follows the LARS paper,
+ *                             see oracle_lars_trust)
  * PW is the pairwise sum: PW(x[0..k)) = x[0] if k == 1, else
  * PW(x[0..h)) + PW(x[h..k)) with h the largest power of two below k. Members of a
  * group are taken in ascending worker id, groups in ascending group id. Equal
@@ -36,6 +39,7 @@
  * -ffast-math) and REAL=double (only used to pin the binary32 build against
  * closed forms and error bounds).
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>

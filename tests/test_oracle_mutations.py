@@ -6,6 +6,7 @@ test_oracle_pins.py reject the result. The GPU library is not involved."""
 import os
 import shutil
 
+import numpy as np
 import pytest
 
 import oracle
@@ -34,6 +35,11 @@ MUTATIONS = {
     "warmup ramp off by one": (MAIN_C, "((double)t / (double)warmup_iters)", "((double)(t + 1) / (double)warmup_iters)"),
     "decay power off by one": (MAIN_C, "for (int64_t i = 0; i < k; ++i) f = f * decay_factor;",
                                "for (int64_t i = 0; i <= k; ++i) f = f * decay_factor;"),
+    "lars squared norms": (REAL_INC, "double wn = sqrt(sp), gn = sqrt(sg);", "double wn = sp, gn = sg;"),
+    "lars no decay in denominator": (REAL_INC, "/ (gn + (double)wd * wn));", "/ gn);"),
+    "lars trust on gradient only": (REAL_INC, "REAL d = trust * decayed;", "REAL d = trust * gbar[i] + wd * p[i];"),
+    "lars no zero-norm fallback": (REAL_INC, "    if (wn == 0.0 || gn == 0.0) return (REAL)1;\n", ""),
+    "lars binary32 sums": (REAL_INC, "double sp = 0.0, sg = 0.0;", "REAL sp = 0.0, sg = 0.0;"),
 }
 
 PINS = [
@@ -54,6 +60,11 @@ PINS = [
     ("literal == mean of means", lambda: P.test_literal_reduction_equals_mean_of_means_for_powers_of_two(4, 4, "f32")),
     ("literal, unequal groups", lambda: P.test_literal_reduction_of_unequal_groups_is_the_flat_mean([0, 1, 1, 1], 2)),
     ("lr schedule, paper rates", P.test_lr_schedule_matches_the_paper),
+    ("lars worked by hand", lambda: P.test_lars_constant_tensor_worked_by_hand(np.float32)),
+    ("lars zero norm", P.test_lars_zero_norm_is_the_plain_step),
+    ("lars gradient scale", lambda: P.test_lars_gradient_scale_invariance(5)),
+    ("lars parameter scale", lambda: P.test_lars_parameter_scale_equivariance(3)),
+    ("lars 60 digits", lambda: P.test_lars_trust_against_60_digit_evaluation(1000, 1e-4)),
 ]
 
 

@@ -596,3 +596,135 @@ def test_lr_schedule_shape():
     assert oracle.lr_at(4680, *a) == np.float32(6.4 * 0.1 * 0.1)
     # no warmup, no decay: the linearly scaled rate
     assert oracle.lr_at(10 ** 9, 0.1, 256.0, 1024.0, 0, 0, 0.1) == np.float32(0.4)
+
+
+# ---------------------------------------------------------------- LARS (Sec. 2, Sec. 6)
+# The paper names LARS without defining it; the oracle follows You, Gitman and
+# Ginsburg (arXiv 1708.03888, eq. 6, Alg. 1). Pins: a step worked by hand, the
+# zero-norm fallback to the plain step, the scale symmetries of the trust
+# ratio, and the ratio against a 60-digit evaluation.
+
+def _lars(p, m, grads, gow, G, lr, mu, wd, eta):
+    p, m = p.copy(), m.copy()
+    t = oracle.lars_step(p, m, grads, gow, G, lr, mu, wd, eta)
+    return p, m, t
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_lars_constant_tensor_worked_by_hand(dtype):
+    """16 elements, p = 2 (or alternating +-2), all four workers (2 x 2) hold 0.5,
+    so gbar = 0.5 (fixed point): ||p|| = 8, ||gbar|| = 2, and with eta = 1/8,
+    wd = 1/4 the trust is (1/8 * 8) / (2 + 1/4 * 8) = 1/4. Then
+    d = 1/4 * (0.5 + 1/4 * p): 1/4 for p = 2, 0 for p = -2; m = d (m0 = 0);
+    p - 0.5 * m = 1.875 or -2. Every value is dyadic, so exact in any order."""
+    n, G, W = 16, 2, 2
+    grads = [np.full(n, 0.5, np.float32) for _ in range(G * W)]
+    gow = workloads.contiguous_groups(G, W)
+    p0 = np.full(n, 2.0, dtype)
+    p, m, t = _lars(p0, np.zeros(n, dtype), grads, gow, G, 0.5, 0.9, 0.25, 0.125)
+    assert t == 0.25
+    assert np.all(m == 0.25) and np.all(p == 1.875)
+    p0 = np.where(np.arange(n) % 2 == 0, 2.0, -2.0).astype(dtype)
+    p, m, t = _lars(p0, np.zeros(n, dtype), grads, gow, G, 0.5, 0.9, 0.25, 0.125)
+    assert t == 0.25
+    assert np.array_equal(m, np.where(np.arange(n) % 2 == 0, 0.25, 0.0).astype(dtype))
+    assert np.array_equal(p, np.where(np.arange(n) % 2 == 0, 1.875, -2.0).astype(dtype))
+
+
+def test_lars_zero_norm_is_the_plain_step():
+    """A tensor with ||p|| = 0 or ||gbar|| = 0 takes trust 1, and the LARS
+    step is then the plain momentum step bit for bit (zero parameters,
+    all-zero gradients, and two workers whose gradients cancel exactly)."""
+    rng = np.random.default_rng(41)
+    n, G, W = 1000, 2, 2
+    gow = workloads.contiguous_groups(G, W)
+    m0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    g = rand_grads(rng, G * W, n)
+    cases = [
+        (np.zeros(n, np.float32), g, gow, G),
+        ((rng.standard_normal(n) * 0.05).astype(np.float32), [np.zeros(n, np.float32)] * 4, gow, G),
+        ((rng.standard_normal(n) * 0.05).astype(np.float32), [g[0], -g[0]], [0, 0], 1),
+    ]
+    for p0, grads, gw, GG in cases:
+        pl, ml, t = _lars(p0, m0, grads, gw, GG, 0.1, 0.9, 1e-4, 1e-3)
+        pp, mp = run_step(p0, m0, grads, gw, GG, 0.1, 0.9, 1e-4)
+        assert t == 1.0
+        assert np.array_equal(pl, pp) and np.array_equal(ml, mp)
+
+
+@pytest.mark.parametrize("k", [5, -7])
+def test_lars_gradient_scale_invariance(k):
+    """With wd = 0 the LARS step does not depend on the gradient scale:
+    scaling every worker gradient by 2^k scales gbar and ||gbar|| by 2^k
+    exactly, the trust by 2^-k exactly, and leaves d = trust * gbar, hence m
+    and p, unchanged bit for bit."""
+    rng = np.random.default_rng(42)
+    n, G, W = 777, 4, 4
+    gow = workloads.contiguous_groups(G, W)
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    g = rand_grads(rng, G * W, n)
+    s = np.float32(2.0 ** k)
+    pa, ma, ta = _lars(p0, m0, g, gow, G, 0.1, 0.9, 0.0, 1e-3)
+    pb, mb, tb = _lars(p0, m0, [x * s for x in g], gow, G, 0.1, 0.9, 0.0, 1e-3)
+    assert np.float32(tb) * s == np.float32(ta)
+    assert np.array_equal(pa, pb) and np.array_equal(ma, mb)
+
+
+@pytest.mark.parametrize("k", [3, -4])
+def test_lars_parameter_scale_equivariance(k):
+    """With wd = 0 and m0 = 0, scaling p by 2^k scales ||p||, the trust, d, m
+    and the new p by 2^k exactly."""
+    rng = np.random.default_rng(43)
+    n, G, W = 513, 2, 4
+    gow = workloads.contiguous_groups(G, W)
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    g = rand_grads(rng, G * W, n)
+    s = np.float32(2.0 ** k)
+    z = np.zeros(n, np.float32)
+    pa, ma, ta = _lars(p0, z, g, gow, G, 0.1, 0.9, 0.0, 1e-3)
+    pb, mb, tb = _lars(p0 * s, z, g, gow, G, 0.1, 0.9, 0.0, 1e-3)
+    assert np.float32(ta) * s == np.float32(tb)
+    assert np.array_equal(pa * s, pb) and np.array_equal(ma * s, mb)
+
+
+def _trust_60_digits(p, gbar, wd, eta):
+    import decimal
+    ctx = decimal.Context(prec=60)
+    sp = sum(Fraction(float(x)) ** 2 for x in p)
+    sg = sum(Fraction(float(x)) ** 2 for x in gbar)
+    D = lambda fr: ctx.divide(decimal.Decimal(fr.numerator), decimal.Decimal(fr.denominator))
+    wn, gn = ctx.sqrt(D(sp)), ctx.sqrt(D(sg))
+    e, w = decimal.Decimal(float(np.float32(eta))), decimal.Decimal(float(np.float32(wd)))
+    return ctx.divide(ctx.multiply(e, wn), ctx.add(gn, ctx.multiply(w, wn)))
+
+
+@pytest.mark.parametrize("n,wd", [(257, 0.0), (1000, 1e-4), (4096, 5e-2)])
+def test_lars_trust_against_60_digit_evaluation(n, wd):
+    """The binary32 trust ratio is within half an ulp (plus the 1e-15 relative
+    slack of its binary64 evaluation) of the ratio evaluated with exact sums of
+    squares and 60-digit square roots and division."""
+    import decimal
+    rng = np.random.default_rng(n)
+    p = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    gbar = (rng.standard_normal(n) * 1e-2 * rng.uniform(0.1, 10)).astype(np.float32)
+    t = np.float32(oracle.lars_trust(p, gbar, wd, 1e-3))
+    exact = _trust_60_digits(p, gbar, wd, 1e-3)
+    ulp = np.spacing(t)
+    err = abs(decimal.Decimal(float(t)) - exact)
+    assert err <= decimal.Decimal(float(ulp)) / 2 + exact * decimal.Decimal("1e-15"), (t, exact)
+
+
+def test_lars_zero_trust_coefficient_keeps_only_momentum():
+    """eta = 0 gives trust 0, so d = 0 and the step decays the momentum:
+    m = mu*m, p = p - lr*m (two binary32 operations per element)."""
+    rng = np.random.default_rng(44)
+    n, G, W = 300, 2, 2
+    gow = workloads.contiguous_groups(G, W)
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    p, m, t = _lars(p0, m0, rand_grads(rng, G * W, n), gow, G, 0.1, 0.9, 1e-4, 0.0)
+    assert t == 0.0
+    m1 = (np.float32(0.9) * m0).astype(np.float32)
+    assert np.array_equal(m, m1)
+    assert np.array_equal(p, (p0 - np.float32(0.1) * m1).astype(np.float32))
