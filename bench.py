@@ -53,6 +53,9 @@ def parse_args(argv=None):
     ap.add_argument("--reduction", choices=("mean_of_means", "literal"), default=None,
                     help="fused step reduction (default: mean_of_means; literal for workloads "
                          "with unequal subgroups)")
+    ap.add_argument("--lars", action="store_true",
+                    help="LARS step (a trust ratio per tensor) on a multi-tensor workload's plan")
+    ap.add_argument("--trust-coef", type=float, default=1e-3, help="LARS trust coefficient")
     ap.add_argument("--broadcast-grad", action="store_true",
                     help="fused step also writes the mean gradient into every worker buffer")
     ap.add_argument("--path", choices=("fused", "unfused"), default="fused",
@@ -69,7 +72,7 @@ def parse_args(argv=None):
 class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
-    def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False):
+    def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
@@ -83,6 +86,9 @@ class Setup:
         self.reduction, self.broadcast_grad = reduction, broadcast_grad
         if wl.tensor_sizes and (reduction != "mean_of_means" or broadcast_grad):
             raise SystemExit("plans run the mean-of-means step without broadcast")
+        if lars and not wl.tensor_sizes:
+            raise SystemExit("--lars needs a workload with per-tensor sizes (a plan)")
+        self.lars, self.trust_coef = lars, trust_coef
         rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
         stream = torch.cuda.current_stream(dev)
         flat_p = workloads.init_params(wl, dev)
@@ -101,12 +107,21 @@ class Setup:
             self.reps = [[torch.empty(s, device=dev, dtype=rtd) for s in sizes] for _ in range(R)]
             self.plan = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps)
             h = self.plan._handle
-            fn = lib.lsgd_step_plan
             hyper = (ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd))
             s = ctypes.c_void_p(stream.cuda_stream)
+            if lars:
+                self.workspace = torch.empty(self.plan.lars_workspace_size(), dtype=torch.uint8, device=dev)
+                fn = lib.lsgd_lars_step_plan
+                extra = (ctypes.c_float(trust_coef), ctypes.c_void_p(self.workspace.data_ptr()),
+                         ctypes.c_size_t(self.workspace.numel()), None)
 
-            def step():
-                check(fn(h, *hyper, s))
+                def step():
+                    check(fn(h, *hyper, *extra, s))
+            else:
+                fn = lib.lsgd_step_plan
+
+                def step():
+                    check(fn(h, *hyper, s))
         else:
             self.plan = None
             self.params = [flat_p]
@@ -289,6 +304,8 @@ def cpu_baseline(setup, seconds):
             return x.view(torch.int16).numpy().view(np.uint16).copy()
         return x.numpy().copy()
 
+    if setup.lars:
+        return _cpu_baseline_lars(setup, seconds, S)
     p = head(setup.params)
     m = head(setup.mom)
     grads = [head(g) for g in setup.grads]
@@ -314,6 +331,40 @@ def cpu_baseline(setup, seconds):
             "sample": "first %d of %d elements, all %d worker gradients and %d replicas, "
                       "%d oracle steps in %.1f s on one host thread" % (S, wl.n, wl.n_workers, R,
                                                                           steps, el)}
+
+
+def _cpu_baseline_lars(setup, seconds, S):
+    """The oracle's LARS step, tensor by tensor, over the leading tensors that
+    hold about S elements (whole tensors: the trust ratio needs each one)."""
+    import numpy as np
+    import oracle
+
+    wl, R = setup.wl, setup.R
+    host = lambda t: t.detach().cpu().numpy().copy()
+    tensors, got = [], 0
+    for t in range(len(setup.params)):
+        if got >= S:
+            break
+        ne = setup.params[t].numel()
+        tensors.append((host(setup.params[t]), host(setup.mom[t]),
+                        [host(g[t]) for g in setup.grads], [np.zeros(ne, np.float32) for _ in range(R)]))
+        got += ne
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        for p, m, grads, reps in tensors:
+            oracle.lars_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, setup.trust_coef, reps)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    elem_per_s = got * steps / el
+    per_elem = wl.algorithmic_bytes(R) / wl.n + 12
+    return {"value": round(elem_per_s * per_elem / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "steps_per_s": round(elem_per_s / wl.n, 6),
+            "sample": "first %d tensors (%d of %d elements), all %d worker gradients and %d replicas, "
+                      "%d oracle LARS steps in %.1f s on one host thread"
+                      % (len(tensors), got, wl.n, wl.n_workers, R, steps, el)}
 
 
 # ---------------------------------------------------------------- counters
@@ -355,9 +406,11 @@ def _calib_kib(rows, counter):
     return sum(vals.values()) / len(vals), len(vals)
 
 
-def kernel_match(wl, reduction=None):
+def kernel_match(wl, reduction=None, lars=False):
     ct = (not wl.group_sizes and reduction != "literal" and wl.groups in (1, 2, 4, 8, 16)
           and wl.workers_per_group in (1, 2, 4, 8, 16) and wl.n_workers <= 128)
+    if lars:
+        return "lars_norms_kernel" if ct else "lars_norms_seg"
     if wl.tensor_sizes:
         return "step_plan_kernel" if ct else "step_plan_seg"
     return "step_flat_ct" if ct else "step_flat_seg"
@@ -373,6 +426,8 @@ def derive_traffic(args):
     R = wl.n_workers if args.replicas < 0 else args.replicas
     fetch_rows = _read_counters(args.fetch_csv)
     write_rows = _read_counters(args.write_csv)
+    if args.lars:
+        return _derive_traffic_lars(args, wl, R, fetch_rows, write_rows)
     kname = kernel_match(wl)
     f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
     w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
@@ -396,9 +451,50 @@ def derive_traffic(args):
     print(json.dumps(out))
 
 
-def stored_traffic(wl, R):
+def lars_kernel_bytes(wl, R):
+    """Algorithmic bytes of the three LARS kernels (per launch): the norms pass
+    reads the N gradients and p and writes the mean gradient; the trust pass
+    reads two binary64 partials per chunk (2048-element pieces) and writes one
+    float per tensor; the update reads the mean gradient, p and m and writes p,
+    m and the R replicas."""
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    chunks = sum((s + 2047) // 2048 for s in wl.tensor_sizes)
+    return {"lars_norms": wl.n * (wl.n_workers * wl.grad_bytes + 8),
+            "lars_trust": chunks * 16 + len(wl.tensor_sizes) * 4,
+            "lars_update": wl.n * (4 + 16 + R * rb)}
+
+
+def _derive_traffic_lars(args, wl, R, fetch_rows, write_rows):
     from paper_1906_05936_amd import build as libbuild
-    path = os.path.join(PROFILES, "traffic_%s_R%d.json" % (wl.name, R))
+    f_c, _ = _calib_kib(fetch_rows, "FETCH_SIZE")
+    w_c, _ = _calib_kib(write_rows, "WRITE_SIZE")
+    known = CALIB_ELEMS * 4 / 1024.0
+    f_scale, w_scale = known / f_c, known / w_c
+    alg = lars_kernel_bytes(wl, R)
+    per = {}
+    for kname in ("lars_norms", "lars_trust", "lars_update"):
+        f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
+        w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
+        rb, wb = f_k * f_scale * 1024, w_k * w_scale * 1024
+        per[kname] = {"fetch_kib_per_dispatch": f_k, "write_kib_per_dispatch": w_k, "dispatches": [nf, nw],
+                      "read_bytes": rb, "write_bytes": wb, "traffic_bytes": rb + wb,
+                      "algorithmic_bytes": alg[kname], "traffic_over_algorithmic": (rb + wb) / alg[kname]}
+    total = sum(v["traffic_bytes"] for v in per.values())
+    step_alg = wl.algorithmic_bytes(R) + 12 * wl.n
+    out = {"workload": wl.name, "replicas": R, "lars": True, "source_digest": libbuild.source_digest(),
+           "copy_fetch_kib": f_c, "copy_write_kib": w_c, "copy_known_kib": known,
+           "fetch_scale": f_scale, "write_scale": w_scale, "kernels": per,
+           "traffic_bytes": total, "algorithmic_bytes": step_alg, "traffic_over_algorithmic": total / step_alg}
+    os.makedirs(PROFILES, exist_ok=True)
+    path = os.path.join(PROFILES, "traffic_%s_lars_R%d.json" % (wl.name, R))
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
+def stored_traffic(wl, R, lars=False):
+    from paper_1906_05936_amd import build as libbuild
+    path = os.path.join(PROFILES, "traffic_%s%s_R%d.json" % (wl.name, "_lars" if lars else "", R))
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -456,13 +552,19 @@ def main(argv=None):
         }
         print(json.dumps(result), flush=True)
         return
-    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad)
+    def extra_bytes():
+        # gradient broadcast writes every worker buffer; LARS re-reads p and
+        # writes and re-reads the mean gradient
+        return (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0) + (12 * wl.n if args.lars else 0)
+
+    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef)
     ms = time_steps(setup, args.steps, args.warmup)
-    alg = wl.algorithmic_bytes(R) + (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0)
+    alg = wl.algorithmic_bytes(R) + extra_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
-    traffic = stored_traffic(wl, R)
+    traffic = stored_traffic(wl, R, args.lars)
     result = {
-        "metric": METRIC, "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1,
+        "metric": METRIC + (" (LARS plan step)" if args.lars else ""), "value": round(gbps, 2),
+        "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
@@ -471,21 +573,23 @@ def main(argv=None):
                    "replicas": R, "replica_dtype": wl.replica_dtype,
                    "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1,
                    "reduction": setup.reduction, "broadcast_grad": setup.broadcast_grad,
-                   **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {})},
+                   **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {}),
+                   **({"lars": True, "trust_coef": args.trust_coef} if args.lars else {})},
         "steps_per_s": round(1e3 / ms, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": alg,
-                     "kernel": kernel_match(wl, setup.reduction)},
+                     "kernel": kernel_match(wl, setup.reduction, args.lars)
+                               + (" + lars_trust_kernel + lars_update_kernel (whole step)" if args.lars else "")},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if R != 0 and not args.no_r0:
         setup.close()
         del setup
         torch.cuda.empty_cache()
-        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad)
+        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef)
         ms0 = time_steps(setup, args.steps, args.warmup)
-        alg0 = wl.algorithmic_bytes(0) + (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0)
+        alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
                         "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),
                         "frac": round(alg0 / (ms0 * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}

@@ -52,6 +52,7 @@
 #ifndef LSGD_H
 #define LSGD_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -289,8 +290,45 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
                                        float weight_decay, const lsgd_step_options* options,
                                        void* stream);
 
+/* ---- LARS on a plan: one trust ratio per tensor -------------------------
+ *
+ * The paper names layer-wise adaptive rate scaling (LARS) as compatible with
+ * LSGD (Sec. 2) and as future work (Sec. 6) without defining it; the step
+ * follows You, Gitman and Ginsburg, "Large Batch Training of Convolutional
+ * Networks" (arXiv 1708.03888, eq. 6 and Alg. 1). Per tensor t of the plan,
+ * with gbar the aggregated gradient of lsgd_step (mean of the G subgroup
+ * means, same pairwise order) and p the parameters before the step:
+ *   trust_t = trust_coef * ||p|| / (||gbar|| + weight_decay * ||p||),
+ *             1 when ||p|| or ||gbar|| is zero;
+ *   d = trust_t * (gbar + weight_decay * p);  m = momentum_coef * m + d;
+ *   p = p - lr * m;  replicas = p (binary32 or nearest-even bfloat16).
+ * Norms: sums of squares, square roots and the ratio in binary64, rounded
+ * once to binary32 (the sums run in a fixed blocked order, so a trust ratio
+ * can differ from a sequential binary64 evaluation only by the last bit in
+ * rare cases). The elementwise operations are binary32, each rounded, no
+ * fused multiply-add. lr sits outside the momentum (the heavy-ball form of
+ * lsgd_step); with a constant lr this is the LARS paper's update.
+ *
+ * The step runs three kernels on `stream`: the mean gradient plus per-chunk
+ * binary64 partial norms, the per-tensor trust ratios, then the update and
+ * copy-out. The workspace is caller-owned device memory of at least
+ * lsgd_lars_workspace_size bytes, 256-byte aligned, that must not overlap any
+ * buffer of the plan or trust_out; it holds the mean gradient (4 bytes per
+ * element), the partial norms and the trust ratios, and its contents are not
+ * needed between calls. Calls sharing a workspace must be ordered on one
+ * stream. trust_out (optional, device, n_tensors floats, 4-byte aligned)
+ * receives the trust ratios. Errors: LSGD_ERR_NULL (plan or workspace NULL),
+ * LSGD_ERR_SIZE (workspace too small), LSGD_ERR_ALIGN, LSGD_ERR_ALIAS,
+ * LSGD_ERR_HIP (wrong device or launch failure); nothing is launched on an
+ * argument error. */
+LSGD_API lsgd_status lsgd_lars_workspace_size(const lsgd_plan* plan, size_t* bytes);
+
+LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
+                                         float weight_decay, float trust_coef, void* workspace,
+                                         size_t workspace_bytes, float* trust_out, void* stream);
+
 /* Frees the plan's device tables. NULL-safe. The caller synchronizes every
- * stream that ran lsgd_step_plan with this plan first. */
+ * stream that ran lsgd_step_plan or lsgd_lars_step_plan with this plan first. */
 LSGD_API void lsgd_plan_destroy(lsgd_plan* plan);
 
 #ifdef __cplusplus

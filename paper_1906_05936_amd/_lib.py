@@ -30,7 +30,8 @@ XCD_CHUNK_AUTO = -1
 EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_get_launch_shape", "lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step",
            "lsgd_step", "lsgd_step_ex", "lsgd_lr_at", "lsgd_lr_schedule_step", "lsgd_plan_create",
-           "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy")
+           "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
+           "lsgd_lars_workspace_size", "lsgd_lars_step_plan")
 
 
 class StepOptions(ctypes.Structure):
@@ -80,6 +81,8 @@ def _load():
     lib.lsgd_step_plan_ex.argtypes = [P, f32, f32, f32, ctypes.POINTER(StepOptions), P]
     lib.lsgd_lr_at.argtypes, lib.lsgd_lr_at.restype = [ctypes.POINTER(LrSchedule), i64], f32
     lib.lsgd_lr_schedule_step.argtypes = [ctypes.POINTER(LrSchedule), P, P, P]
+    lib.lsgd_lars_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
                  "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_step_plan_ex",
@@ -352,6 +355,38 @@ class Plan:
                 opts = _options("mean_of_means", False, lr_device, self.device)
                 st = lib.lsgd_step_plan_ex(self._handle, lr, momentum_coef, weight_decay,
                                            ctypes.byref(opts), _stream(stream, self.device))
+        check(st)
+
+    def lars_workspace_size(self):
+        """Bytes of device workspace lsgd_lars_step_plan needs for this plan."""
+        n = ctypes.c_size_t()
+        check(lib.lsgd_lars_workspace_size(self._handle, ctypes.byref(n)))
+        return n.value
+
+    def lars_step(self, lr, momentum_coef, weight_decay, trust_coef, trust_out=None, workspace=None,
+                  stream=None):
+        """lsgd_lars_step_plan: one LARS step (a trust ratio per tensor).
+        workspace: a uint8 device tensor of at least lars_workspace_size()
+        bytes, 256-byte aligned; by default one is allocated on first use and
+        kept with the plan. trust_out: optional float32 device tensor of
+        n_tensors elements that receives the trust ratios."""
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        if workspace is None:
+            need = self.lars_workspace_size()
+            ws = getattr(self, "_lars_ws", None)
+            if ws is None or ws.numel() < need:
+                ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+                self._lars_ws = ws
+            workspace = ws
+        tp = None
+        if trust_out is not None:
+            _dev_tensor(trust_out, "trust_out", torch.float32, len(self._keep[0]), self.device)
+            tp = trust_out.data_ptr()
+        with torch.cuda.device(self.device):
+            st = lib.lsgd_lars_step_plan(self._handle, lr, momentum_coef, weight_decay, trust_coef,
+                                         workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                         tp, _stream(stream, self.device))
         check(st)
 
     def close(self):

@@ -112,6 +112,10 @@ template <int VEC, int T>
 __device__ __forceinline__ float (&slice(float (&x)[T], int q))[VEC] {
     return *reinterpret_cast<float(*)[VEC]>(&x[q * VEC]);
 }
+template <int VEC, int T>
+__device__ __forceinline__ const float (&slice(const float (&x)[T], int q))[VEC] {
+    return *reinterpret_cast<const float(*)[VEC]>(&x[q * VEC]);
+}
 
 // ---------------------------------------------------------------- loads/stores
 
@@ -201,6 +205,35 @@ __device__ __forceinline__ void store_f32(float* p, int64_t e0, int cnt, const f
             f32x4 t = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
             __builtin_nontemporal_store(t, gstore_ptr<f32x4>(p + e0) + q);
         }
+    }
+}
+
+// Plain (cache-allocating) variants, for data that is read again soon: the
+// LARS mean-gradient scratch (written by one kernel, read by the next).
+template <int VEC, bool TAIL>
+__device__ __forceinline__ void load_f32_cached(const float* p, int64_t e0, int cnt, float (&x)[VEC]) {
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) x[v] = v < cnt ? gload_ptr<float>(p + e0)[v] : 0.f;
+    } else {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            const f32x4 t = *(gload_ptr<f32x4>(p + e0) + q);
+            x[4 * q] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
+        }
+    }
+}
+
+template <int VEC, bool TAIL>
+__device__ __forceinline__ void store_f32_cached(float* p, int64_t e0, int cnt, const float (&x)[VEC]) {
+    if constexpr (TAIL) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+            if (v < cnt) gstore_ptr<float>(p + e0)[v] = x[v];
+    } else {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q)
+            *(gstore_ptr<f32x4>(p + e0) + q) = f32x4{x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
     }
 }
 
@@ -525,13 +558,11 @@ __device__ __forceinline__ void load_state(const Src& s, const int64_t (&e0)[U],
     for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
 }
 
-// The update on loaded state, then parameters, momentum and replicas stored.
+// Parameters, momentum and replicas stored.
 template <int VEC, int U, bool TAIL, typename Src>
-__device__ __forceinline__ void update_and_store(const Src& s, const int64_t (&e0)[U], int cnt,
-                                                 const float (&gbar)[U * VEC], float (&p)[U * VEC],
-                                                 float (&m)[U * VEC]) {
+__device__ __forceinline__ void store_state(const Src& s, const int64_t (&e0)[U], int cnt,
+                                            const float (&p)[U * VEC], const float (&m)[U * VEC]) {
     constexpr int T = U * VEC;
-    sgd_update<T>(s.hyper(), gbar, p, m);
 #pragma unroll
     for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
 #pragma unroll
@@ -543,6 +574,15 @@ __device__ __forceinline__ void update_and_store(const Src& s, const int64_t (&e
 #pragma unroll
         for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(p, q));
     }
+}
+
+// The update on loaded state, then parameters, momentum and replicas stored.
+template <int VEC, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void update_and_store(const Src& s, const int64_t (&e0)[U], int cnt,
+                                                 const float (&gbar)[U * VEC], float (&p)[U * VEC],
+                                                 float (&m)[U * VEC]) {
+    sgd_update<U * VEC>(s.hyper(), gbar, p, m);
+    store_state<VEC, U, TAIL>(s, e0, cnt, p, m);
 }
 
 // Everything after the mean gradient, for a tile of U units: optional
@@ -565,7 +605,8 @@ __device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U]
 // accumulator over groups, which yields the same PW order. TAIL (the ragged
 // end of a tensor, cnt < VEC elements) only with U = 1.
 template <typename GT, int W, int G, int U, bool TAIL, typename Src>
-__device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[U], int cnt) {
+__device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U], int cnt,
+                                             float (&gbar)[U * Unit<GT>::VEC]) {
     static_assert(!TAIL || U == 1, "ragged units are processed one at a time");
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
@@ -580,11 +621,16 @@ __device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[
 #pragma unroll
         for (int v = 0; v < T; ++v) gm[v] = sum[v] / static_cast<float>(W);
     };
-    float tot[T], gbar[T];
+    float tot[T];
     pw_leaves<G, T, W * T>(group_leaf, tot);
 #pragma unroll
     for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
+}
 
+template <typename GT, int W, int G, int U, bool TAIL, typename Src>
+__device__ __forceinline__ void fused_tile_ct(const Src& s, const int64_t (&e0)[U], int cnt) {
+    float gbar[U * Unit<GT>::VEC];
+    mean_tile_ct<GT, W, G, U, TAIL>(s, e0, cnt, gbar);
     finish_tile<GT, U, TAIL>(s, e0, cnt, gbar);
 }
 
@@ -594,19 +640,15 @@ __device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt)
     fused_tile_ct<GT, W, G, 1, TAIL>(s, e, cnt);
 }
 
-// Fused step on one unit for group layouts known only at run time. Group j
-// is members [gs(j), gs(j+1)) of the member-ordered gradients. Mean of means
-// (literal = false, equal groups of W): each group's PW sum / W, PW over the G
-// results, / G. Paper-literal (any partition): each group's PW sum / N, PW
-// over the G results, no further division. Parameters and momentum are
-// loaded first so that their latency overlaps the gradient stream.
+// The mean gradient of one unit for group layouts known only at run time.
+// Group j is members [gs(j), gs(j+1)) of the member-ordered gradients. Mean of
+// means (literal = false, equal groups of W): each group's PW sum / W, PW over
+// the G results, / G. Paper-literal (any partition): each group's PW sum / N,
+// PW over the G results, no further division.
 template <typename GT, int LV, bool TAIL, typename Src, typename Start>
-__device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
-                                               int64_t e0, int cnt) {
+__device__ __forceinline__ void mean_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                              int64_t e0, int cnt, float (&gbar)[Unit<GT>::VEC]) {
     constexpr int VEC = Unit<GT>::VEC;
-    const int64_t e[1] = {e0};
-    float p[VEC], m[VEC];
-    load_state<VEC, 1, TAIL>(s, e, cnt, p, m);
     const float dg = static_cast<float>(literal ? N : gs(1) - gs(0));
     PwAcc<VEC, LV> groups;
     const int glevels = acc_levels(G);
@@ -616,13 +658,25 @@ __device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const
                                   for (int v = 0; v < VEC; ++v) sum[v] = sum[v] / dg;
                                   groups.push(sum, glevels);
                               });
-    float gbar[VEC];
     groups.result(gbar, glevels);
     if (!literal) {
         const float gf = static_cast<float>(G);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
     }
+}
+
+// Fused step on one unit for runtime group layouts. Parameters and momentum
+// are loaded first so that their latency overlaps the gradient stream.
+template <typename GT, int LV, bool TAIL, typename Src, typename Start>
+__device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                               int64_t e0, int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int64_t e[1] = {e0};
+    float p[VEC], m[VEC];
+    load_state<VEC, 1, TAIL>(s, e, cnt, p, m);
+    float gbar[VEC];
+    mean_unit_seg<GT, LV, TAIL>(s, N, G, gs, literal, e0, cnt, gbar);
     broadcast_mean<GT, 1, TAIL>(s, e, cnt, gbar);
     update_and_store<VEC, 1, TAIL>(s, e, cnt, gbar, p, m);
 }
@@ -876,7 +930,7 @@ struct PlanSrc {
 
 // One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
 // (one large piece, or several small tensors). Chunk and pointer-table reads
-// are uniform per workgroup. chunk(s, ch) processes one chunk.
+// are uniform per workgroup. chunk(s, ch, c) processes chunk c.
 template <typename ChunkFn>
 __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn& chunk) {
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
@@ -887,7 +941,7 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
         const PlanChunk* cp = &a.chunks[c];
         const PlanChunk ch{read_table(&cp->tensor), 0, read_table(&cp->start), read_table(&cp->len)};
         const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
-        chunk(s, ch);
+        chunk(s, ch, c);
     }
 }
 
@@ -896,7 +950,7 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
 template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch) {
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
             if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
@@ -920,13 +974,248 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const int W = a.W;
     auto gs = [&](int j) { return j * W; };
-    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch) {
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t u = threadIdx.x; u < full; u += kBlock)
             fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, false, ch.start + u * VEC, VEC);
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0)
             fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, false, ch.start + full * VEC, rem);
+    });
+}
+
+}  // namespace lsgd
+
+namespace lsgd {
+
+// ------------------------------------------------------------- LARS on a plan
+//
+// Layer-wise trust ratios (LARS, which the paper names in Sec. 2 and Sec. 6;
+// definition of You, Gitman and Ginsburg, eq. 6 and Alg. 1) need each tensor's
+// ||p|| and ||gbar|| before any of its elements is updated, so a step takes
+// three launches over the plan:
+//   1. lars_norms_*: the mean gradient of every element (the same pairwise
+//      aggregation as the fused step), stored to a scratch slice per tensor,
+//      and per-chunk binary64 sums of p^2 and gbar^2 (one workgroup-level
+//      reduction per chunk, fixed order);
+//   2. lars_trust_kernel: one workgroup per tensor sums its chunks' partials
+//      (fixed order) and forms trust = eta*||p|| / (||gbar|| + wd*||p||) in
+//      binary64, rounded once to binary32; 1 when a norm is zero;
+//   3. lars_update_kernel: d = trust*(gbar + wd*p), the heavy-ball update and
+//      the copy-out, reading gbar back from the scratch.
+
+struct LarsArgs {
+    PlanArgs pa;                   // the plan's tables and counts
+    const int64_t* gbar_off;       // [n_tensors]: tensor t's slice of `gbar` starts here (floats)
+    const int32_t* tensor_chunks;  // [n_tensors + 1]: tensor t owns chunks [tc[t], tc[t+1])
+    float* gbar;                   // scratch: aggregated gradient, one slice per tensor
+    double* partials;              // [n_chunks][2]: sums of p^2 and gbar^2 over a chunk
+    float* trust;                  // [n_tensors]
+    float* trust_out;              // optional copy of the trust ratios
+    int32_t n_tensors;
+    float trust_coef;
+};
+
+// Workgroup sums of two doubles per lane, valid in thread 0. Within a wave an
+// xor butterfly: partners add the same two values, and addition is
+// commutative, so every lane holds the same bits after each round; then the
+// four wave sums in a fixed order. Every thread of the block calls it.
+__device__ __forceinline__ void block_sum2(double& a, double& b, double (*lds)[2]) {
+    static_assert(kBlock == 256, "four waves per workgroup");
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        lds[wave][0] = a;
+        lds[wave][1] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a = (lds[0][0] + lds[1][0]) + (lds[2][0] + lds[3][0]);
+        b = (lds[0][1] + lds[1][1]) + (lds[2][1] + lds[3][1]);
+    }
+    __syncthreads();
+}
+
+// Mean gradient of a tile stored to the scratch slice, squares accumulated.
+template <int T>
+__device__ __forceinline__ void lars_accumulate(const float (&p)[T], const float (&g)[T], int cnt_total,
+                                                double& sp, double& sg) {
+#pragma unroll
+    for (int v = 0; v < T; ++v) {
+        if (v < cnt_total) {
+            sp += static_cast<double>(p[v]) * static_cast<double>(p[v]);
+            sg += static_cast<double>(g[v]) * static_cast<double>(g[v]);
+        }
+    }
+}
+
+template <typename GT, int U, bool TAIL>
+__device__ __forceinline__ void lars_tile_out(const PlanSrc& s, float* gb, const int64_t (&e)[U], int cnt,
+                                              const float (&gbar)[U * Unit<GT>::VEC], double& sp, double& sg) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    float p[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        store_f32_cached<VEC, TAIL>(gb, e[q], cnt, slice<VEC, T>(gbar, q));
+        load_f32_cached<VEC, TAIL>(s.p(), e[q], cnt, slice<VEC, T>(p, q));
+    }
+    // zero-filled tail elements add nothing, but skip them anyway
+    lars_accumulate<T>(p, gbar, TAIL ? cnt : T, sp, sg);
+}
+
+// Pass 1, compile-time (W, G).
+template <typename GT, int W, int G, int U>
+__global__ __launch_bounds__(kBlock) void lars_norms_kernel(LarsArgs la) {
+    constexpr int VEC = Unit<GT>::VEC;
+    __shared__ double lds[kBlock / 64][2];
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t c) {
+        float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        double sp = 0.0, sg = 0.0;
+        const int64_t full = ch.len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                float gbar[U * VEC];
+                mean_tile_ct<GT, W, G, U, false>(s, e0, VEC, gbar);
+                lars_tile_out<GT, U, false>(s, gb, e0, VEC, gbar, sp, sg);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * VEC};
+                    float gbar[VEC];
+                    mean_tile_ct<GT, W, G, 1, false>(s, e, VEC, gbar);
+                    lars_tile_out<GT, 1, false>(s, gb, e, VEC, gbar, sp, sg);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            float gbar[VEC];
+            mean_tile_ct<GT, W, G, 1, true>(s, e, rem, gbar);
+            lars_tile_out<GT, 1, true>(s, gb, e, rem, gbar, sp, sg);
+        }
+        block_sum2(sp, sg, lds);
+        if (threadIdx.x == 0) {
+            la.partials[2 * static_cast<int64_t>(c)] = sp;
+            la.partials[2 * static_cast<int64_t>(c) + 1] = sg;
+        }
+    });
+}
+
+// Pass 1, runtime W and G (equal groups): one unit per lane.
+template <typename GT, int LV>
+__global__ __launch_bounds__(kBlock) void lars_norms_seg(LarsArgs la) {
+    constexpr int VEC = Unit<GT>::VEC;
+    __shared__ double lds[kBlock / 64][2];
+    const int W = la.pa.W;
+    auto gs = [&](int j) { return j * W; };
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t c) {
+        float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        double sp = 0.0, sg = 0.0;
+        const int64_t full = ch.len / VEC;
+        for (int64_t u = threadIdx.x; u < full; u += kBlock) {
+            const int64_t e[1] = {ch.start + u * VEC};
+            float gbar[VEC];
+            mean_unit_seg<GT, LV, false>(s, la.pa.n_workers, la.pa.n_groups, gs, false, e[0], VEC, gbar);
+            lars_tile_out<GT, 1, false>(s, gb, e, VEC, gbar, sp, sg);
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            float gbar[VEC];
+            mean_unit_seg<GT, LV, true>(s, la.pa.n_workers, la.pa.n_groups, gs, false, e[0], rem, gbar);
+            lars_tile_out<GT, 1, true>(s, gb, e, rem, gbar, sp, sg);
+        }
+        block_sum2(sp, sg, lds);
+        if (threadIdx.x == 0) {
+            la.partials[2 * static_cast<int64_t>(c)] = sp;
+            la.partials[2 * static_cast<int64_t>(c) + 1] = sg;
+        }
+    });
+}
+
+// Pass 2: one workgroup per tensor.
+static __global__ __launch_bounds__(kBlock) void lars_trust_kernel(LarsArgs la) {
+    __shared__ double lds[kBlock / 64][2];
+    const int32_t t = static_cast<int32_t>(blockIdx.x);
+    if (t >= la.n_tensors) return;
+    const int32_t c0 = la.tensor_chunks[t], c1 = la.tensor_chunks[t + 1];
+    double sp = 0.0, sg = 0.0;
+    for (int32_t c = c0 + static_cast<int32_t>(threadIdx.x); c < c1; c += kBlock) {
+        sp += la.partials[2 * static_cast<int64_t>(c)];
+        sg += la.partials[2 * static_cast<int64_t>(c) + 1];
+    }
+    block_sum2(sp, sg, lds);
+    if (threadIdx.x == 0) {
+        const double wn = sqrt(sp), gn = sqrt(sg);
+        const double wd = static_cast<double>(la.pa.h.wd);
+        const float tr = (wn == 0.0 || gn == 0.0)
+                             ? 1.0f
+                             : static_cast<float>((static_cast<double>(la.trust_coef) * wn) / (gn + wd * wn));
+        la.trust[t] = tr;
+        if (la.trust_out) la.trust_out[t] = tr;
+    }
+}
+
+// Pass 3: trust-scaled update of U binary32 units per lane.
+template <int VEC>
+__device__ __forceinline__ void lars_update(const Hyper& h, float trust, const float (&gbar)[VEC],
+                                            float (&p)[VEC], float (&m)[VEC]) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        const float decayed = gbar[v] + h.wd * p[v];
+        const float d = trust * decayed;
+        m[v] = h.mu * m[v] + d;
+        p[v] = p[v] - h.lr * m[v];
+    }
+}
+
+template <int U, bool TAIL>
+__device__ __forceinline__ void lars_update_tile(const PlanSrc& s, const float* gb, float trust,
+                                                 const int64_t (&e0)[U], int cnt) {
+    constexpr int T = U * 4;
+    float g[T], p[T], m[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(gb, e0[q], cnt, slice<4, T>(g, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(s.p(), e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(s.m(), e0[q], cnt, slice<4, T>(m, q));
+    lars_update<T>(s.hyper(), trust, g, p, m);
+    store_state<4, U, TAIL>(s, e0, cnt, p, m);
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void lars_update_kernel(LarsArgs la) {
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        const float trust = read_table(&la.trust[ch.tensor]);
+        const int64_t full = ch.len / 4;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * 4;
+                lars_update_tile<U, false>(s, gb, trust, e0, 4);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * 4};
+                    lars_update_tile<1, false>(s, gb, trust, e, 4);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * 4);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * 4};
+            lars_update_tile<1, true>(s, gb, trust, e, rem);
+        }
     });
 }
 

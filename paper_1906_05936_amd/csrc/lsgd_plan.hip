@@ -27,12 +27,23 @@ struct lsgd_plan {
     lsgd::PlanChunk* d_chunks;
     int32_t* d_bucket_begin;
     void** d_ptrs;
+    // LARS: per-tensor scratch offsets and chunk ranges, and every buffer's
+    // byte range (for the workspace aliasing check)
+    int64_t gbar_floats;
+    int64_t* d_gbar_off;
+    int32_t* d_tensor_chunks;
+    std::vector<lsgd::Range>* ranges;
 };
 
 namespace lsgd {
 namespace {
 
 using PlanKernel = void (*)(PlanArgs);
+using LarsKernel = void (*)(LarsArgs);
+
+// LARS scratch: each tensor's slice of the mean-gradient scratch starts on a
+// 64-float (256-byte) boundary.
+constexpr int64_t kGbarAlign = 64;
 
 // A kernel and the units per lane tile it processes.
 struct PlanPick {
@@ -74,11 +85,90 @@ PlanPick pick_plan(int W, int G) {
     return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>, 1};
 }
 
+lsgd_status check_device(const lsgd_plan* plan) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+        return fail(LSGD_ERR_HIP, "plan was created on device %d, current device is %d", plan->device, dev);
+    return LSGD_OK;
+}
+
+// Kernel arguments of a plan step and the launch shape over its buckets.
+PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, LaunchShape& ls) {
+    PlanArgs a;
+    memset(&a, 0, sizeof a);
+    a.chunks = plan->d_chunks;
+    a.bucket_begin = plan->d_bucket_begin;
+    a.ptrs = plan->d_ptrs;
+    a.stride = plan->stride;
+    a.n_workers = plan->n_workers;
+    a.n_groups = plan->n_groups;
+    a.W = plan->W;
+    a.n_replicas = plan->n_replicas;
+    a.rdt = static_cast<int32_t>(plan->rdt);
+    a.h = h;
+    a.lr_ptr = lr_device;
+    a.n_buckets = plan->n_buckets;
+    const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
+    ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
+    a.xcd_chunk = ls.xcd_chunk;
+    return a;
+}
+
+// LARS pass-1 kernels: compile-time (W, G) as for the step, else segmented.
+template <typename GT, int W>
+LarsKernel pick_lars_g(int G) {
+    constexpr int U = TileUnits<GT>::U;
+    switch (G) {
+        case 1: return lars_norms_kernel<GT, W, 1, U>;
+        case 2: return lars_norms_kernel<GT, W, 2, U>;
+        case 4: return lars_norms_kernel<GT, W, 4, U>;
+        case 8: return lars_norms_kernel<GT, W, 8, U>;
+        case 16:
+            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, U>;
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+template <typename GT>
+LarsKernel pick_lars(int W, int G) {
+    LarsKernel k = nullptr;
+    switch (W) {
+        case 1: k = pick_lars_g<GT, 1>(G); break;
+        case 2: k = pick_lars_g<GT, 2>(G); break;
+        case 4: k = pick_lars_g<GT, 4>(G); break;
+        case 8: k = pick_lars_g<GT, 8>(G); break;
+        case 16: k = pick_lars_g<GT, 16>(G); break;
+    }
+    if (k) return k;
+    return seg_levels(W > G ? W : G) == 5 ? lars_norms_seg<GT, 5> : lars_norms_seg<GT, 8>;
+}
+
+// LARS workspace layout: [gbar scratch | per-chunk partials | trust ratios],
+// each part starting on a 256-byte boundary.
+struct LarsLayout {
+    size_t gbar, partials, trust, total;
+};
+
+size_t round256(size_t x) { return (x + 255) / 256 * 256; }
+
+LarsLayout lars_layout(const lsgd_plan* plan) {
+    LarsLayout l;
+    l.gbar = 0;
+    l.partials = round256(static_cast<size_t>(plan->gbar_floats) * sizeof(float));
+    l.trust = l.partials + round256(static_cast<size_t>(plan->n_chunks) * 2 * sizeof(double));
+    l.total = l.trust + round256(static_cast<size_t>(plan->n_tensors) * sizeof(float));
+    return l;
+}
+
 void free_plan(lsgd_plan* p) {
     if (!p) return;
     if (p->d_chunks) (void)hipFree(p->d_chunks);
     if (p->d_bucket_begin) (void)hipFree(p->d_bucket_begin);
     if (p->d_ptrs) (void)hipFree(p->d_ptrs);
+    if (p->d_gbar_off) (void)hipFree(p->d_gbar_off);
+    if (p->d_tensor_chunks) (void)hipFree(p->d_tensor_chunks);
+    delete p->ranges;
     delete p;
 }
 
@@ -120,9 +210,15 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     const int64_t kPiece = (gdt == LSGD_BF16 ? piece_elems<uint16_t>(tile) : piece_elems<float>(tile)) *
                            launch_passes_per_block();
     int64_t bucket_fill = kPiece;  // forces a new bucket at the first piece
+    std::vector<int64_t> gbar_off(n_tensors, 0);
+    std::vector<int32_t> tensor_chunks(n_tensors + 1, 0);
+    int64_t gbar_floats = 0;
     for (int32_t t = 0; t < n_tensors; ++t) {
         const int64_t ne = numel[t];
         if (ne < 0) return fail(LSGD_ERR_SIZE, "numel[%d]=%lld < 0", t, static_cast<long long>(ne));
+        tensor_chunks[t] = static_cast<int32_t>(std::min<size_t>(chunks.size(), 0x7fffffff));
+        gbar_off[t] = gbar_floats;
+        gbar_floats += (ne + kGbarAlign - 1) / kGbarAlign * kGbarAlign;
         if (ne == 0) continue;
         void** row = &table[static_cast<size_t>(t) * stride];
         auto add = [&](void* p, size_t esz, bool written, const char* what, int idx) -> lsgd_status {
@@ -161,6 +257,7 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     if ((st = check_overlap(ranges)) != LSGD_OK) return st;
     if (chunks.size() > 0x7fffffff) return fail(LSGD_ERR_SIZE, "too many pieces");
     bucket_begin.push_back(static_cast<int32_t>(chunks.size()));
+    tensor_chunks[n_tensors] = static_cast<int32_t>(chunks.size());
 
     lsgd_plan* p = new lsgd_plan;
     memset(p, 0, sizeof *p);
@@ -179,6 +276,8 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     p->n_buckets = static_cast<int32_t>(bucket_begin.size()) - 1;
     p->stride = stride;
     p->piece = kPiece;
+    p->gbar_floats = gbar_floats;
+    p->ranges = new std::vector<Range>(ranges);
     hipError_t e = hipSuccess;
     const size_t chunk_bytes = std::max<size_t>(1, chunks.size()) * sizeof(PlanChunk);
     const size_t bucket_bytes = bucket_begin.size() * sizeof(int32_t);
@@ -191,6 +290,13 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     if (e == hipSuccess)
         e = hipMemcpy(p->d_bucket_begin, bucket_begin.data(), bucket_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(p->d_ptrs, table.data(), table_bytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMalloc(&p->d_gbar_off, gbar_off.size() * sizeof(int64_t));
+    if (e == hipSuccess) e = hipMalloc(&p->d_tensor_chunks, tensor_chunks.size() * sizeof(int32_t));
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_gbar_off, gbar_off.data(), gbar_off.size() * sizeof(int64_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_tensor_chunks, tensor_chunks.data(), tensor_chunks.size() * sizeof(int32_t),
+                      hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         free_plan(p);
         return fail(LSGD_ERR_HIP, "lsgd_plan_create: %s", hipGetErrorString(e));
@@ -212,26 +318,10 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
             return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
     }
     if (plan->n_buckets == 0) return LSGD_OK;
-    int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
-        return fail(LSGD_ERR_HIP, "plan was created on device %d, current device is %d", plan->device, dev);
-    PlanArgs a;
-    memset(&a, 0, sizeof a);
-    a.chunks = plan->d_chunks;
-    a.bucket_begin = plan->d_bucket_begin;
-    a.ptrs = plan->d_ptrs;
-    a.stride = plan->stride;
-    a.n_workers = plan->n_workers;
-    a.n_groups = plan->n_groups;
-    a.W = plan->W;
-    a.n_replicas = plan->n_replicas;
-    a.rdt = static_cast<int32_t>(plan->rdt);
-    a.h = Hyper{lr, momentum_coef, weight_decay};
-    a.lr_ptr = lr_device;
-    a.n_buckets = plan->n_buckets;
-    const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
-    const LaunchShape ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
-    a.xcd_chunk = ls.xcd_chunk;
+    lsgd_status st = check_device(plan);
+    if (st != LSGD_OK) return st;
+    LaunchShape ls;
+    const PlanArgs a = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
     const PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
                                                 : pick_plan<float>(plan->W, plan->n_groups).kernel;
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
@@ -241,6 +331,65 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                     float weight_decay, void* stream) {
     return lsgd_step_plan_ex(plan, lr, momentum_coef, weight_decay, nullptr, stream);
+}
+
+LSGD_API lsgd_status lsgd_lars_workspace_size(const lsgd_plan* plan, size_t* bytes) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    if (!bytes) return fail(LSGD_ERR_NULL, "bytes is NULL");
+    *bytes = lars_layout(plan).total;
+    return LSGD_OK;
+}
+
+LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
+                                         float weight_decay, float trust_coef, void* workspace,
+                                         size_t workspace_bytes, float* trust_out, void* stream) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    if (!workspace) return fail(LSGD_ERR_NULL, "workspace is NULL");
+    const LarsLayout l = lars_layout(plan);
+    if (workspace_bytes < l.total)
+        return fail(LSGD_ERR_SIZE, "workspace_bytes=%zu < %zu (lsgd_lars_workspace_size)", workspace_bytes, l.total);
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return fail(LSGD_ERR_ALIGN, "workspace is not 256-byte aligned");
+    if (trust_out && (reinterpret_cast<uintptr_t>(trust_out) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "trust_out is not 4-byte aligned");
+    std::vector<Range> ranges(*plan->ranges);
+    const uintptr_t wb = reinterpret_cast<uintptr_t>(workspace);
+    ranges.push_back(Range{wb, wb + l.total, true, "workspace"});
+    if (trust_out) {
+        const uintptr_t tb = reinterpret_cast<uintptr_t>(trust_out);
+        ranges.push_back(Range{tb, tb + static_cast<uintptr_t>(plan->n_tensors) * sizeof(float), true, "trust_out"});
+    }
+    lsgd_status st = check_overlap(ranges);
+    if (st != LSGD_OK) return st;
+    if ((st = check_device(plan)) != LSGD_OK) return st;
+
+    LarsArgs la;
+    memset(&la, 0, sizeof la);
+    LaunchShape ls;
+    la.pa = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, nullptr, ls);
+    la.gbar_off = plan->d_gbar_off;
+    la.tensor_chunks = plan->d_tensor_chunks;
+    char* ws = static_cast<char*>(workspace);
+    la.gbar = reinterpret_cast<float*>(ws + l.gbar);
+    la.partials = reinterpret_cast<double*>(ws + l.partials);
+    la.trust = reinterpret_cast<float*>(ws + l.trust);
+    la.trust_out = trust_out;
+    la.n_tensors = plan->n_tensors;
+    la.trust_coef = trust_coef;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (plan->n_buckets > 0) {
+        const LarsKernel k1 = plan->gdt == LSGD_BF16 ? pick_lars<uint16_t>(plan->W, plan->n_groups)
+                                                     : pick_lars<float>(plan->W, plan->n_groups);
+        hipLaunchKernelGGL(k1, dim3(ls.blocks), dim3(kBlock), 0, s, la);
+        if ((st = check_launch("lsgd_lars_step_plan (norms)")) != LSGD_OK) return st;
+    }
+    hipLaunchKernelGGL(lars_trust_kernel, dim3(plan->n_tensors), dim3(kBlock), 0, s, la);
+    if ((st = check_launch("lsgd_lars_step_plan (trust)")) != LSGD_OK) return st;
+    if (plan->n_buckets > 0) {
+        hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
+        if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK) return st;
+    }
+    return LSGD_OK;
 }
 
 LSGD_API void lsgd_plan_destroy(lsgd_plan* plan) { free_plan(plan); }

@@ -45,7 +45,8 @@ def test_header_declares_the_boundary():
             "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
             "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
-            "lsgd_lr_schedule_step", "lsgd_step_plan_ex"} == names
+            "lsgd_lr_schedule_step", "lsgd_step_plan_ex", "lsgd_lars_workspace_size",
+            "lsgd_lars_step_plan"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -268,6 +269,13 @@ def test_plan_ex_and_schedule_validation():
     assert f(ctypes.byref(sched), A, A + 4, None) == ALIAS
     bad = L.LrSchedule(0.1, 0.0, 16384.0, 390, 2340, 0.1)
     assert f(ctypes.byref(bad), A, A + 64, None) == SIZE
+
+
+def test_lars_validation():
+    n = ctypes.c_size_t()
+    assert lib.lsgd_lars_workspace_size(None, ctypes.byref(n)) == NULL
+    assert lib.lsgd_lars_step_plan(None, 0.1, 0.9, 1e-4, 1e-3, A, 1 << 30, None, None) == NULL
+    assert "plan is NULL" in lib.lsgd_last_error().decode()
 
 
 def test_last_error_is_per_thread():

@@ -1,0 +1,224 @@
+"""GPU parity of the LARS plan step (lsgd_lars_step_plan, through the C ABI)
+against the CPU oracle (oracle_lars_step, one tensor at a time).
+
+Bar: each tensor's trust ratio within one binary32 ulp of the oracle's (both
+evaluate the norms in binary64 and round once; the GPU sums in a blocked
+order, the oracle sequentially, so a ratio may differ in its last bit in rare
+cases). Where the trust ratios agree bit for bit, parameters, momentum and
+replicas are bit-exact; otherwise the contract tolerance
+|gpu - ref| <= 1e-6*|ref| + 1e-6*rms(ref) applies.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.device_count() > 0:
+    import paper_1906_05936_amd as lsgd
+else:  # collected but skipped on machines without a GPU
+    lsgd = None
+
+DEV = torch.device("cuda:0")
+TRUST_COEF = 1e-3   # eta of the LARS paper's experiments
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def to_host(t):
+    t = t.detach()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def rand_host(rng, n, std, dtype):
+    x = (rng.standard_normal(n) * std).astype(np.float32)
+    return oracle.f32_to_bf16(x) if dtype == "bf16" else x
+
+
+def close(gpu, ref, what):
+    assert gpu.shape == ref.shape, what
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(gpu), fin), what
+    rms = float(np.sqrt(np.mean(ref[fin].astype(np.float64) ** 2))) if fin.any() else 0.0
+    err = np.abs(gpu[fin].astype(np.float64) - ref[fin])
+    assert np.all(err <= 1e-6 * np.abs(ref[fin]) + 1e-6 * rms), "%s: max err %g" % (what, err.max())
+
+
+def ulps(a, b):
+    return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
+
+
+# Mixed sizes: ragged ends, single elements, several pieces, an empty tensor;
+# tensor ZERO_P starts at p = 0 and tensor ZERO_G gets zero gradients (trust 1).
+SIZES = [1, 3, 64, 1000, 8191, 8193, 0, 20_000, 5, 4096, 9408, 16_385, 70_001]
+ZERO_P, ZERO_G = 4, 9
+
+
+class Case:
+    def __init__(self, G, W, gdt, R, rdt, seed):
+        self.rng = np.random.default_rng(seed)
+        self.G, self.W, self.N, self.gdt, self.R, self.rdt = G, W, G * W, gdt, R, rdt
+        self.gow = workloads.shuffled_groups(G, W, seed)
+        self.ph = [(self.rng.standard_normal(s) * 0.05).astype(np.float32) for s in SIZES]
+        self.ph[ZERO_P][:] = 0.0
+        self.mh = [np.zeros(s, np.float32) for s in SIZES]
+        self.params = [to_dev(x) for x in self.ph]
+        self.mom = [to_dev(x) for x in self.mh]
+        self.grads = [[torch.empty(s, device=DEV, dtype=torch.bfloat16 if gdt == "bf16" else torch.float32)
+                       for s in SIZES] for _ in range(self.N)]
+        rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+        self.reps = [[torch.empty(s, device=DEV, dtype=rtd) for s in SIZES] for _ in range(R)]
+        self.plan = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps)
+
+    def new_grads(self):
+        self.gh = [[rand_host(self.rng, s, 1e-2 * self.rng.uniform(0.2, 5), self.gdt) for s in SIZES]
+                   for _ in range(self.N)]
+        for w in range(self.N):
+            self.gh[w][ZERO_G][:] = 0
+            for t in range(len(SIZES)):
+                self.grads[w][t].copy_(to_dev(self.gh[w][t]))
+
+    def check(self, lr, mu, wd, eta, step):
+        trust = torch.full((len(SIZES),), -1.0, device=DEV)
+        self.plan.lars_step(lr, mu, wd, eta, trust_out=trust)
+        torch.cuda.synchronize()
+        tg = to_host(trust)
+        exact = 0
+        for t, s in enumerate(SIZES):
+            rr = [np.zeros(s, np.uint16 if self.rdt == "bf16" else np.float32) for _ in range(self.R)]
+            tr = oracle.lars_step(self.ph[t], self.mh[t], [self.gh[w][t] for w in range(self.N)],
+                                  self.gow, self.G, lr, mu, wd, eta, rr,
+                                  oracle.BF16 if self.rdt == "bf16" else oracle.F32)
+            assert ulps(tg[t], tr) <= 1, "tensor %d step %d: trust %r vs %r" % (t, step, tg[t], tr)
+            if t == ZERO_G or s == 0 or (t == ZERO_P and step == 0):   # p = 0 only before the first update
+                assert tg[t] == 1.0, (t, tg[t])
+            pg, mg = to_host(self.params[t]), to_host(self.mom[t])
+            if np.float32(tg[t]) == np.float32(tr):
+                exact += 1
+                assert np.array_equal(pg, self.ph[t]), "params[%d] step %d differ in bits" % (t, step)
+                assert np.array_equal(mg, self.mh[t]), "momentum[%d] step %d differ in bits" % (t, step)
+                for r in range(self.R):
+                    assert np.array_equal(to_host(self.reps[r][t]), rr[r]), (t, r, step)
+            else:
+                close(pg, self.ph[t], "params[%d] step %d" % (t, step))
+                close(mg, self.mh[t], "momentum[%d] step %d" % (t, step))
+                # keep following the GPU's state so later steps compare like with like
+                self.ph[t][:] = pg
+                self.mh[t][:] = mg
+        log("  step %d: %d of %d trust ratios bit-equal" % (step, exact, len(SIZES)))
+
+
+@pytest.mark.parametrize("G,W,gdt,R,rdt", [(4, 4, "f32", 16, "f32"), (2, 2, "f32", 0, "f32"),
+                                           (8, 8, "bf16", 3, "bf16"), (3, 5, "f32", 1, "bf16"),
+                                           (1, 1, "f32", 1, "f32"), (5, 3, "bf16", 0, "f32")])
+def test_lars_plan_matches_oracle(G, W, gdt, R, rdt):
+    log("lars plan G=%d W=%d %s R=%d %s" % (G, W, gdt, R, rdt))
+    c = Case(G, W, gdt, R, rdt, seed=G * 10 + W)
+    for step in range(3):
+        c.new_grads()
+        c.check(0.1, 0.9, 1e-4, TRUST_COEF, step)
+    c.plan.close()
+
+
+def test_lars_special_coefficients():
+    """eta = 0 (trust 0: the momentum only decays) and wd = 0, on the same plan."""
+    c = Case(4, 4, "f32", 2, "f32", seed=77)
+    c.new_grads()
+    c.check(0.1, 0.9, 1e-4, 0.0, 0)
+    c.new_grads()
+    c.check(0.2, 0.5, 0.0, 0.02, 1)
+    c.plan.close()
+
+
+def test_lars_full_size_resnet50_tensors():
+    """The 161 ResNet-50 tensors (25,557,032 elements), 4 x 4 workers, two
+    steps, every element compared."""
+    wl = workloads.WORKLOADS["resnet50_tensors"]
+    G, W, N, R = wl.groups, wl.workers_per_group, wl.n_workers, 2
+    sizes = list(wl.tensor_sizes)
+    offs = np.cumsum([0] + sizes)
+    gow = workloads.contiguous_groups(G, W)
+    flat_p = workloads.init_params(wl, DEV)
+    params = workloads.split_tensors(flat_p, sizes)
+    ph = [to_host(x) for x in params]
+    del flat_p
+    mom = [torch.zeros_like(x) for x in params]
+    mh = [np.zeros(s, np.float32) for s in sizes]
+    grads = [[torch.empty(s, device=DEV) for s in sizes] for _ in range(N)]
+    reps = [[torch.empty(s, device=DEV) for s in sizes] for _ in range(R)]
+    plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+    tmp = torch.empty(wl.n, device=DEV)
+    trust = torch.empty(len(sizes), device=DEV)
+    for step in range(2):
+        gh = []
+        for w in range(N):
+            workloads.fill_worker_grad(wl, step, w, tmp)
+            for t in range(len(sizes)):
+                grads[w][t].copy_(tmp[offs[t]:offs[t + 1]])
+            gh.append(to_host(tmp))
+        plan.lars_step(wl.lr, wl.mu, wl.wd, TRUST_COEF, trust_out=trust)
+        torch.cuda.synchronize()
+        tg = to_host(trust)
+        exact = 0
+        for t, s in enumerate(sizes):
+            rr = [np.zeros(s, np.float32) for _ in range(R)]
+            tr = oracle.lars_step(ph[t], mh[t], [g[offs[t]:offs[t + 1]] for g in gh], gow, G,
+                                  wl.lr, wl.mu, wl.wd, TRUST_COEF, rr)
+            assert ulps(tg[t], tr) <= 1, (t, step, tg[t], tr)
+            pg, mg = to_host(params[t]), to_host(mom[t])
+            if np.float32(tg[t]) == np.float32(tr):
+                exact += 1
+                assert np.array_equal(pg, ph[t]) and np.array_equal(mg, mh[t]), (t, step)
+                assert np.array_equal(to_host(reps[R - 1][t]), rr[R - 1]), (t, step)
+            else:
+                close(pg, ph[t], "params[%d]" % t)
+                close(mg, mh[t], "momentum[%d]" % t)
+                ph[t][:] = pg
+                mh[t][:] = mg
+        log("  resnet50 step %d: %d of %d trust ratios bit-equal" % (step, exact, len(sizes)))
+    plan.close()
+
+
+def test_lars_argument_errors():
+    """Workspace too small, misaligned, or overlapping a plan buffer: the call
+    raises and launches nothing."""
+    n = 10_000
+    p = torch.zeros(n, device=DEV)
+    m = torch.zeros(n, device=DEV)
+    g = [[torch.ones(n, device=DEV)] for _ in range(2)]
+    plan = lsgd.Plan([p], [m], g, [0, 1], 2)
+    need = plan.lars_workspace_size()
+    assert need >= n * 4
+    ws = torch.empty(need + 512, dtype=torch.uint8, device=DEV)
+    for bad, status in [(ws[:need - 1], "LSGD_ERR_SIZE"), (ws[16:16 + need], "LSGD_ERR_ALIGN")]:
+        with pytest.raises(lsgd.LsgdError) as e:
+            plan.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, workspace=bad)
+        assert e.value.name == status
+    big = torch.zeros(need // 4 + 1024, device=DEV)
+    plan2 = lsgd.Plan([big[:n]], [m], g, [0, 1], 2)
+    with pytest.raises(lsgd.LsgdError) as e:
+        plan2.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, workspace=big.view(torch.uint8))
+    assert e.value.name == "LSGD_ERR_ALIAS"
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(p).item() == 0 and torch.count_nonzero(big[:n]).item() == 0
+    plan.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, workspace=ws)   # a valid call goes through
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(p).item() == n
+    plan.close()
+    plan2.close()
