@@ -56,6 +56,8 @@ def parse_args(argv=None):
     ap.add_argument("--lars", action="store_true",
                     help="LARS step (a trust ratio per tensor) on a multi-tensor workload's plan")
     ap.add_argument("--trust-coef", type=float, default=1e-3, help="LARS trust coefficient")
+    ap.add_argument("--copy-out", choices=("auto", "fused", "separate"), default="auto",
+                    help="replicas written inside the step kernel or by a copy-out pass of their own")
     ap.add_argument("--broadcast-grad", action="store_true",
                     help="fused step also writes the mean gradient into every worker buffer")
     ap.add_argument("--path", choices=("fused", "unfused"), default="fused",
@@ -406,6 +408,17 @@ def _calib_kib(rows, counter):
     return sum(vals.values()) / len(vals), len(vals)
 
 
+def separate_copy_out(wl, R, mode="auto"):
+    """The library's rule for the copy-out pass (lsgd_set_copy_out_mode), for
+    labels only."""
+    if R == 0 or mode == "fused":
+        return False
+    if mode == "separate":
+        return True
+    gb = wl.n_workers * wl.grad_bytes
+    return wl.replica_dtype == "f32" and (gb >= 256 or R * 4 > gb)
+
+
 def kernel_match(wl, reduction=None, lars=False):
     ct = (not wl.group_sizes and reduction != "literal" and wl.groups in (1, 2, 4, 8, 16)
           and wl.workers_per_group in (1, 2, 4, 8, 16) and wl.n_workers <= 128)
@@ -431,6 +444,10 @@ def derive_traffic(args):
     kname = kernel_match(wl)
     f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
     w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
+    if any("copy_out" in r.get("Kernel_Name", "") for r in fetch_rows):   # the step's copy-out pass
+        f_c2, _ = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", "copy_out")
+        w_c2, _ = _per_dispatch_kib(write_rows, "WRITE_SIZE", "copy_out")
+        f_k, w_k, kname = f_k + f_c2, w_k + w_c2, kname + " + copy_out"
     f_c, _ = _calib_kib(fetch_rows, "FETCH_SIZE")
     w_c, _ = _calib_kib(write_rows, "WRITE_SIZE")
     known = CALIB_ELEMS * 4 / 1024.0
@@ -527,6 +544,9 @@ def main(argv=None):
     print("bench: %s n=%d G=%d W=%d %s R=%d" % (wl.name, wl.n, wl.groups, wl.workers_per_group,
                                                wl.grad_dtype, R), file=sys.stderr, flush=True)
     ceiling = copy_ceiling(dev, args.calibrate_copy)
+    import paper_1906_05936_amd as lsgd
+    lsgd.set_copy_out_mode({"auto": lsgd.COPY_OUT_AUTO, "fused": lsgd.COPY_OUT_FUSED,
+                            "separate": lsgd.COPY_OUT_SEPARATE}[args.copy_out])
     if args.path == "unfused":
         setup = UnfusedSetup(wl, R, dev)
         ms = time_steps(setup, args.steps, args.warmup)
@@ -574,13 +594,17 @@ def main(argv=None):
                    "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1,
                    "reduction": setup.reduction, "broadcast_grad": setup.broadcast_grad,
                    **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {}),
-                   **({"lars": True, "trust_coef": args.trust_coef} if args.lars else {})},
+                   **({"lars": True, "trust_coef": args.trust_coef} if args.lars else {}),
+                   "copy_out": ("separate pass" if separate_copy_out(wl, R, args.copy_out) and not args.lars
+                                else "in the step kernel")},
         "steps_per_s": round(1e3 / ms, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": alg,
                      "kernel": kernel_match(wl, setup.reduction, args.lars)
-                               + (" + lars_trust_kernel + lars_update_kernel (whole step)" if args.lars else "")},
+                               + (" + lars_trust_kernel + lars_update_kernel (whole step)" if args.lars else "")
+                               + (" + copy_out (whole step)" if not args.lars and separate_copy_out(wl, R, args.copy_out)
+                                  else "")},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if R != 0 and not args.no_r0:

@@ -31,7 +31,8 @@ EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_get_launch_shape", "lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step",
            "lsgd_step", "lsgd_step_ex", "lsgd_lr_at", "lsgd_lr_schedule_step", "lsgd_plan_create",
            "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
-           "lsgd_lars_workspace_size", "lsgd_lars_step_plan")
+           "lsgd_lars_workspace_size", "lsgd_lars_step_plan", "lsgd_set_copy_out_mode",
+           "lsgd_get_copy_out_mode")
 
 
 class StepOptions(ctypes.Structure):
@@ -82,6 +83,8 @@ def _load():
     lib.lsgd_lr_at.argtypes, lib.lsgd_lr_at.restype = [ctypes.POINTER(LrSchedule), i64], f32
     lib.lsgd_lr_schedule_step.argtypes = [ctypes.POINTER(LrSchedule), P, P, P]
     lib.lsgd_lars_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.lsgd_set_copy_out_mode.argtypes = [i32]
+    lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
     lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
@@ -400,3 +403,15 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+
+COPY_OUT_AUTO, COPY_OUT_FUSED, COPY_OUT_SEPARATE = -1, 0, 1
+
+
+def set_copy_out_mode(mode):
+    """lsgd_set_copy_out_mode: COPY_OUT_AUTO, COPY_OUT_FUSED or COPY_OUT_SEPARATE."""
+    check(lib.lsgd_set_copy_out_mode(mode))
+
+
+def get_copy_out_mode():
+    return lib.lsgd_get_copy_out_mode()

@@ -23,6 +23,7 @@ std::atomic<int> g_cus[kMaxDevices];
 std::atomic<int32_t> g_xcd_chunk{kDefaultXcdChunk};
 std::atomic<int32_t> g_blocks_per_cu{kDefaultBlocksPerCu};
 std::atomic<int32_t> g_units_per_lane{kDefaultUnitsPerLane};
+std::atomic<int32_t> g_copy_out_mode{LSGD_COPY_OUT_AUTO};
 }  // namespace
 
 lsgd_status fail(lsgd_status st, const char* fmt, ...) {
@@ -150,6 +151,23 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
 
 int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_order_relaxed); }
 
+// Automatic rule, from same-process measurements of the fused pass against
+// step-then-copy-out over R = 8..128. Binary32 replicas: with 128 binary32
+// gradients (512 gradient bytes per element) the separate pass won at every R
+// (by 8-11%); with 16 (64 bytes) it won once the replica writes exceeded the
+// gradient reads (R = 32: +1-5%, R = 64: +5-8%, R = 128: +10%) and lost by
+// 2-4% below. bfloat16 replicas (64 bfloat16 gradients, R = 16, 64, 128):
+// the fused pass won every time (by 2-5%), so they always stay in it.
+bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz) {
+    if (n_replicas <= 0) return false;
+    const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
+    if (mode == LSGD_COPY_OUT_FUSED) return false;
+    if (mode == LSGD_COPY_OUT_SEPARATE) return true;
+    if (rsz != 4) return false;
+    const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
+    return grad_bytes >= 256 || static_cast<int64_t>(n_replicas) * 4 > grad_bytes;
+}
+
 LaunchShape launch_shape(int64_t units, int tile) {
     const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);
     const int64_t span = static_cast<int64_t>(kBlock) * upl * (tile < 1 ? 1 : tile);
@@ -198,6 +216,15 @@ LSGD_API lsgd_status lsgd_set_launch_shape(int32_t xcd_chunk, int32_t blocks_per
     lsgd::g_units_per_lane.store(units_per_lane, std::memory_order_relaxed);
     return LSGD_OK;
 }
+
+LSGD_API lsgd_status lsgd_set_copy_out_mode(int32_t mode) {
+    if (mode != LSGD_COPY_OUT_AUTO && mode != LSGD_COPY_OUT_FUSED && mode != LSGD_COPY_OUT_SEPARATE)
+        return lsgd::fail(LSGD_ERR_SIZE, "copy-out mode %d", mode);
+    lsgd::g_copy_out_mode.store(mode, std::memory_order_relaxed);
+    return LSGD_OK;
+}
+
+LSGD_API int32_t lsgd_get_copy_out_mode(void) { return lsgd::g_copy_out_mode.load(std::memory_order_relaxed); }
 
 LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_per_cu,
                                            int32_t* units_per_lane) {

@@ -94,6 +94,19 @@ MeanPick pick_global_mean(int G) {
 
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
 
+// The copy-out pass of a flat step: p (already updated on `stream`) to the
+// replicas in a.replicas[0 .. a.n_replicas).
+lsgd_status launch_copy_out(StepArgs& a, void* stream) {
+    const bool bf16 = a.rdt == static_cast<int32_t>(LSGD_BF16);
+    const int vec = bf16 ? 8 : 4, tile = bf16 ? 1 : 2;
+    const LaunchShape ls = launch_shape((a.n + vec - 1) / vec * (vec / 4), tile * (vec / 4));
+    a.xcd_chunk = ls.xcd_chunk;
+    a.upl = ls.upl;
+    const FlatKernel k = bf16 ? copy_out_kernel<8, 1> : copy_out_kernel<4, 2>;
+    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
+    return check_launch("lsgd_step (copy-out)");
+}
+
 // Name of gradient ranges in the aliasing check (compared by address).
 const char* const kGradRange = "grad";
 
@@ -219,8 +232,12 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
+    const bool split = separate_copy_out(n_workers, dtype_size(gdt), n_replicas, dtype_size(rdt));
+    if (split) a.n_replicas = 0;
     hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
-    return check_launch(literal ? "lsgd_step_ex" : "lsgd_step");
+    if ((st = check_launch(literal ? "lsgd_step_ex" : "lsgd_step")) != LSGD_OK || !split) return st;
+    a.n_replicas = n_replicas;
+    return launch_copy_out(a, stream);
 }
 
 LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,

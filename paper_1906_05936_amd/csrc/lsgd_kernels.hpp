@@ -888,6 +888,44 @@ __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
         });
 }
 
+// ------------------------------------------------------------- copy-out pass
+//
+// With many replicas the copy-out runs as a pass of its own after the step
+// kernel (which then writes no replica): a lane reads a tile of the new p once
+// and writes it to every replica. Measured: one read-heavy pass plus one
+// write-only pass beat the single mixed pass once the replica writes outweigh
+// the gradient reads, or when N is large (host rule in lsgd_common.hip).
+// Binary32 replicas use two 4-element units per lane; bfloat16 replicas one
+// 8-element unit, so that every store is 16 bytes.
+template <int VEC, int U, bool TAIL, typename Rep>
+__device__ __forceinline__ void copy_out_tile(const float* p, const Rep& rep, int R, int rdt,
+                                              const int64_t (&e0)[U], int cnt) {
+    constexpr int T = U * VEC;
+    float x[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(p, e0[q], cnt, slice<VEC, T>(x, q));
+    for (int r = 0; r < R; ++r) {
+        void* rp = rep(r);
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(x, q));
+    }
+}
+
+template <int VEC, int U>
+__global__ __launch_bounds__(kBlock) void copy_out_kernel(StepArgs a) {
+    const int64_t full = a.n / VEC;
+    const int rem = static_cast<int>(a.n - full * VEC);
+    auto rep = [&](int r) { return a.replicas[r]; };
+    for_tiles<U, VEC>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { copy_out_tile<VEC, U, false>(a.p, rep, a.n_replicas, a.rdt, e0, VEC); },
+        [&](int64_t u) {
+            const int64_t e[1] = {u * VEC};
+            if (u < full) copy_out_tile<VEC, 1, false>(a.p, rep, a.n_replicas, a.rdt, e, VEC);
+            else copy_out_tile<VEC, 1, true>(a.p, rep, a.n_replicas, a.rdt, e, rem);
+        });
+}
+
 // ------------------------------------------------------------- multi-tensor plan
 
 // One piece of one tensor: elements [start, start+len). Pieces start at
@@ -981,6 +1019,34 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0)
             fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, false, ch.start + full * VEC, rem);
+    });
+}
+
+// Copy-out pass over a plan's chunks (see copy_out_kernel).
+template <int VEC, int U>
+__global__ __launch_bounds__(kBlock) void copy_out_plan_kernel(PlanArgs a) {
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const float* p = s.p();
+        auto rep = [&](int r) { return s.replica(r); };
+        const int64_t full = ch.len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                copy_out_tile<VEC, U, false>(p, rep, a.n_replicas, a.rdt, e0, VEC);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * VEC};
+                    copy_out_tile<VEC, 1, false>(p, rep, a.n_replicas, a.rdt, e, VEC);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            copy_out_tile<VEC, 1, true>(p, rep, a.n_replicas, a.rdt, e, rem);
+        }
     });
 }
 

@@ -321,11 +321,19 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     lsgd_status st = check_device(plan);
     if (st != LSGD_OK) return st;
     LaunchShape ls;
-    const PlanArgs a = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
+    PlanArgs a = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
     const PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
                                                 : pick_plan<float>(plan->W, plan->n_groups).kernel;
-    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
-    return check_launch("lsgd_step_plan");
+    const bool split = separate_copy_out(plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4, plan->n_replicas,
+                                         plan->rdt == LSGD_BF16 ? 2 : 4);
+    if (split) a.n_replicas = 0;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, s, a);
+    if ((st = check_launch("lsgd_step_plan")) != LSGD_OK || !split) return st;
+    a.n_replicas = plan->n_replicas;
+    const PlanKernel kc = plan->rdt == LSGD_BF16 ? copy_out_plan_kernel<8, 1> : copy_out_plan_kernel<4, 2>;
+    hipLaunchKernelGGL(kc, dim3(ls.blocks), dim3(kBlock), 0, s, a);
+    return check_launch("lsgd_step_plan (copy-out)");
 }
 
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,

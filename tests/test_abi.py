@@ -46,7 +46,7 @@ def test_header_declares_the_boundary():
             "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
             "lsgd_lr_schedule_step", "lsgd_step_plan_ex", "lsgd_lars_workspace_size",
-            "lsgd_lars_step_plan"} == names
+            "lsgd_lars_step_plan", "lsgd_set_copy_out_mode", "lsgd_get_copy_out_mode"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -269,6 +269,16 @@ def test_plan_ex_and_schedule_validation():
     assert f(ctypes.byref(sched), A, A + 4, None) == ALIAS
     bad = L.LrSchedule(0.1, 0.0, 16384.0, 390, 2340, 0.1)
     assert f(ctypes.byref(bad), A, A + 64, None) == SIZE
+
+
+def test_copy_out_mode_setter():
+    assert lib.lsgd_get_copy_out_mode() == -1
+    for mode in (0, 1, -1):
+        assert lib.lsgd_set_copy_out_mode(mode) == OK
+        assert lib.lsgd_get_copy_out_mode() == mode
+    assert lib.lsgd_set_copy_out_mode(2) == SIZE
+    assert lib.lsgd_set_copy_out_mode(-2) == SIZE
+    assert lib.lsgd_get_copy_out_mode() == -1
 
 
 def test_lars_validation():

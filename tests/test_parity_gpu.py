@@ -647,3 +647,51 @@ def test_graph_captured_whole_step_follows_the_schedule():
         assert torch.equal(p, pe) and torch.equal(m, me), k
     assert it.item() == 12
     del graph
+
+
+# ---------------------------------------------------------------- copy-out pass
+
+@pytest.mark.parametrize("G,W,gdt,R,rdt,n", [(4, 4, "f32", 33, "f32", 100_003), (2, 2, "bf16", 9, "bf16", 77_777),
+                                             (8, 8, "f32", 3, "f32", 65_539), (3, 5, "f32", 20, "bf16", 4_099)])
+def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
+    """The replicas written in the step kernel, in a copy-out pass of their own,
+    and by the automatic choice: all bitwise equal to the oracle, flat and
+    through a plan (ragged sizes)."""
+    log("copy-out modes G=%d W=%d %s R=%d %s n=%d" % (G, W, gdt, R, rdt, n))
+    rng = np.random.default_rng(n)
+    N = G * W
+    gow = groups_for(G, W, "shuffled", seed=3)
+    gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(N)]
+    grads = [to_dev(x) for x in gh]
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    ph, mh = p0.copy(), np.zeros(n, np.float32)
+    rr = [np.zeros(n, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+    oracle.lsgd_step(ph, mh, gh, gow, G, 0.1, 0.9, 1e-4, rr, oracle.BF16 if rdt == "bf16" else oracle.F32)
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    sizes = [n // 3, 1, n - n // 3 - 1]
+    try:
+        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO):
+            lsgd.set_copy_out_mode(mode)
+            p, m = to_dev(p0), torch.zeros(n, device=DEV)
+            reps = [torch.full((n,), 7, device=DEV, dtype=rtd) for _ in range(R)]
+            lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
+            torch.cuda.synchronize()
+            assert_close(to_host(p), ph, "params mode %d" % mode)
+            for r in range(R):
+                assert np.array_equal(to_host(reps[r]), rr[r]), (mode, r)
+            # the same step through a three-tensor plan
+            offs = np.cumsum([0] + sizes)
+            pt = [to_dev(p0[offs[t]:offs[t + 1]].copy()) for t in range(3)]
+            mt = [torch.zeros(s, device=DEV) for s in sizes]
+            gt = [[g[offs[t]:offs[t + 1]].clone() for t in range(3)] for g in grads]
+            rt = [[torch.full((s,), 7, device=DEV, dtype=rtd) for s in sizes] for _ in range(R)]
+            plan = lsgd.Plan(pt, mt, gt, gow, G, rt)
+            plan.step(0.1, 0.9, 1e-4)
+            torch.cuda.synchronize()
+            for t in range(3):
+                assert_close(to_host(pt[t]), ph[offs[t]:offs[t + 1]], "plan params %d mode %d" % (t, mode))
+                for r in range(R):
+                    assert np.array_equal(to_host(rt[r][t]), rr[r][offs[t]:offs[t + 1]]), (mode, t, r)
+            plan.close()
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
