@@ -115,7 +115,7 @@ class Setup:
                 self.workspace = torch.empty(self.plan.lars_workspace_size(), dtype=torch.uint8, device=dev)
                 fn = lib.lsgd_lars_step_plan
                 extra = (ctypes.c_float(trust_coef), ctypes.c_void_p(self.workspace.data_ptr()),
-                         ctypes.c_size_t(self.workspace.numel()), None)
+                         ctypes.c_size_t(self.workspace.numel()), None, None)
 
                 def step():
                     check(fn(h, *hyper, *extra, s))

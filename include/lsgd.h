@@ -332,7 +332,10 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
  * element), the partial norms and the trust ratios, and its contents are not
  * needed between calls. Calls sharing a workspace must be ordered on one
  * stream. trust_out (optional, device, n_tensors floats, 4-byte aligned)
- * receives the trust ratios. Errors: LSGD_ERR_NULL (plan or workspace NULL),
+ * receives the trust ratios. lr_device (optional, device, 4-byte aligned):
+ * when non-NULL the update reads the global rate there when it runs and `lr`
+ * is ignored, as in lsgd_step_ex (so a captured graph can follow
+ * lsgd_lr_schedule_step). Errors: LSGD_ERR_NULL (plan or workspace NULL),
  * LSGD_ERR_SIZE (workspace too small), LSGD_ERR_ALIGN, LSGD_ERR_ALIAS,
  * LSGD_ERR_HIP (wrong device or launch failure); nothing is launched on an
  * argument error. */
@@ -340,7 +343,8 @@ LSGD_API lsgd_status lsgd_lars_workspace_size(const lsgd_plan* plan, size_t* byt
 
 LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                          float weight_decay, float trust_coef, void* workspace,
-                                         size_t workspace_bytes, float* trust_out, void* stream);
+                                         size_t workspace_bytes, float* trust_out,
+                                         const float* lr_device, void* stream);
 
 /* Frees the plan's device tables. NULL-safe. The caller synchronizes every
  * stream that ran lsgd_step_plan or lsgd_lars_step_plan with this plan first. */

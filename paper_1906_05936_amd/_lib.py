@@ -85,7 +85,7 @@ def _load():
     lib.lsgd_lars_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
     lib.lsgd_set_copy_out_mode.argtypes = [i32]
     lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
-    lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P]
+    lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
                  "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_step_plan_ex",
@@ -367,12 +367,14 @@ class Plan:
         return n.value
 
     def lars_step(self, lr, momentum_coef, weight_decay, trust_coef, trust_out=None, workspace=None,
-                  stream=None):
+                  stream=None, lr_device=None):
         """lsgd_lars_step_plan: one LARS step (a trust ratio per tensor).
         workspace: a uint8 device tensor of at least lars_workspace_size()
         bytes, 256-byte aligned; by default one is allocated on first use and
         kept with the plan. trust_out: optional float32 device tensor of
-        n_tensors elements that receives the trust ratios."""
+        n_tensors elements that receives the trust ratios. lr_device: optional
+        one-element float32 device tensor read for the rate when the update
+        runs (lr is then ignored)."""
         if self._handle is None:
             raise RuntimeError("plan is closed")
         if workspace is None:
@@ -386,10 +388,14 @@ class Plan:
         if trust_out is not None:
             _dev_tensor(trust_out, "trust_out", torch.float32, len(self._keep[0]), self.device)
             tp = trust_out.data_ptr()
+        lp = None
+        if lr_device is not None:
+            _dev_tensor(lr_device, "lr_device", torch.float32, 1, self.device)
+            lp = lr_device.data_ptr()
         with torch.cuda.device(self.device):
             st = lib.lsgd_lars_step_plan(self._handle, lr, momentum_coef, weight_decay, trust_coef,
                                          workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-                                         tp, _stream(stream, self.device))
+                                         tp, lp, _stream(stream, self.device))
         check(st)
 
     def close(self):

@@ -350,7 +350,8 @@ LSGD_API lsgd_status lsgd_lars_workspace_size(const lsgd_plan* plan, size_t* byt
 
 LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                          float weight_decay, float trust_coef, void* workspace,
-                                         size_t workspace_bytes, float* trust_out, void* stream) {
+                                         size_t workspace_bytes, float* trust_out,
+                                         const float* lr_device, void* stream) {
     if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
     if (!workspace) return fail(LSGD_ERR_NULL, "workspace is NULL");
     const LarsLayout l = lars_layout(plan);
@@ -360,12 +361,18 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
         return fail(LSGD_ERR_ALIGN, "workspace is not 256-byte aligned");
     if (trust_out && (reinterpret_cast<uintptr_t>(trust_out) & 3u) != 0)
         return fail(LSGD_ERR_ALIGN, "trust_out is not 4-byte aligned");
+    if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
     std::vector<Range> ranges(*plan->ranges);
     const uintptr_t wb = reinterpret_cast<uintptr_t>(workspace);
     ranges.push_back(Range{wb, wb + l.total, true, "workspace"});
     if (trust_out) {
         const uintptr_t tb = reinterpret_cast<uintptr_t>(trust_out);
         ranges.push_back(Range{tb, tb + static_cast<uintptr_t>(plan->n_tensors) * sizeof(float), true, "trust_out"});
+    }
+    if (lr_device) {
+        const uintptr_t lb = reinterpret_cast<uintptr_t>(lr_device);
+        ranges.push_back(Range{lb, lb + sizeof(float), false, "lr_device"});
     }
     lsgd_status st = check_overlap(ranges);
     if (st != LSGD_OK) return st;
@@ -374,7 +381,7 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
     LarsArgs la;
     memset(&la, 0, sizeof la);
     LaunchShape ls;
-    la.pa = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, nullptr, ls);
+    la.pa = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
     la.gbar_off = plan->d_gbar_off;
     la.tensor_chunks = plan->d_tensor_chunks;
     char* ws = static_cast<char*>(workspace);

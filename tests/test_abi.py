@@ -284,7 +284,7 @@ def test_copy_out_mode_setter():
 def test_lars_validation():
     n = ctypes.c_size_t()
     assert lib.lsgd_lars_workspace_size(None, ctypes.byref(n)) == NULL
-    assert lib.lsgd_lars_step_plan(None, 0.1, 0.9, 1e-4, 1e-3, A, 1 << 30, None, None) == NULL
+    assert lib.lsgd_lars_step_plan(None, 0.1, 0.9, 1e-4, 1e-3, A, 1 << 30, None, None, None) == NULL
     assert "plan is NULL" in lib.lsgd_last_error().decode()
 
 

@@ -222,3 +222,50 @@ def test_lars_argument_errors():
     assert torch.count_nonzero(p).item() == n
     plan.close()
     plan2.close()
+
+
+def test_lars_graph_follows_the_device_schedule():
+    """A HIP graph holding the device-side learning-rate schedule step and a
+    LARS plan step that reads the rate from device memory: every replay equals
+    an eager LARS step run with the oracle's rate for that iteration, bit for
+    bit (three launches per step, no host work, no allocation in the graph)."""
+    rng = np.random.default_rng(12)
+    sizes = [1000, 4097, 65_536, 3]
+    G, W = 2, 2
+    gow = workloads.contiguous_groups(G, W)
+    p0 = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in sizes]
+    gh = [[rand_host(rng, s, 1e-2, "f32") for s in sizes] for _ in range(G * W)]
+
+    def make():
+        params = [to_dev(x) for x in p0]
+        mom = [torch.zeros(s, device=DEV) for s in sizes]
+        grads = [[to_dev(x) for x in row] for row in gh]
+        reps = [[torch.empty(s, device=DEV) for s in sizes]]
+        return params, mom, grads, reps, lsgd.Plan(params, mom, grads, gow, G, reps)
+
+    pg, mg, gg, rg, plan_g = make()
+    pe, me, ge, re_, plan_e = make()
+    ws = torch.empty(plan_g.lars_workspace_size(), dtype=torch.uint8, device=DEV)
+    sched = (0.1, 256.0, 1024.0, 3, 5, 0.5)
+    s = lsgd.lr_schedule(*sched)
+    it = torch.zeros(1, device=DEV, dtype=torch.int64)
+    lr_t = torch.zeros(1, device=DEV)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            lsgd.lr_schedule_step(s, it, lr_t, stream=stream)
+            plan_g.lars_step(0.0, 0.9, 1e-4, TRUST_COEF, workspace=ws, stream=stream, lr_device=lr_t)
+    torch.cuda.synchronize()
+    for k in range(8):
+        graph.replay()
+        plan_e.lars_step(float(oracle.lr_at(k, *sched)), 0.9, 1e-4, TRUST_COEF)
+        torch.cuda.synchronize()
+        for t in range(len(sizes)):
+            assert torch.equal(pg[t], pe[t]) and torch.equal(mg[t], me[t]), (k, t)
+            assert torch.equal(rg[0][t], re_[0][t]), (k, t)
+    assert it.item() == 8
+    del graph
+    plan_g.close()
+    plan_e.close()

@@ -695,3 +695,36 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
             plan.close()
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+
+
+def test_graph_with_separate_copy_out_matches_eager():
+    """The step kernel and its copy-out pass captured in one graph: every
+    replay equals eager steps, bit for bit."""
+    n, G, W, R = 50_021, 4, 4, 40
+    rng = np.random.default_rng(8)
+    gow = groups_for(G, W, "contiguous")
+    grads = [to_dev(rand_host(rng, n, 1e-2, "f32")) for _ in range(G * W)]
+    p0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+    p, m = p0.clone(), torch.zeros(n, device=DEV)
+    reps = [torch.empty(n, device=DEV) for _ in range(R)]
+    pe, me = p0.clone(), torch.zeros(n, device=DEV)
+    reps_e = [torch.empty(n, device=DEV) for _ in range(R)]
+    try:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_SEPARATE)
+        stream = torch.cuda.Stream()
+        stream.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(graph, stream=stream):
+                lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps, stream=stream)
+        torch.cuda.synchronize()
+        for k in range(5):
+            graph.replay()
+            lsgd.step(pe, me, grads, gow, G, 0.1, 0.9, 1e-4, reps_e)
+            torch.cuda.synchronize()
+            assert torch.equal(p, pe) and torch.equal(m, me), k
+            for r in (0, R // 2, R - 1):
+                assert torch.equal(reps[r], reps_e[r]) and torch.equal(reps[r], p), (k, r)
+        del graph
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
