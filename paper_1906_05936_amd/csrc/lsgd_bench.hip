@@ -3,6 +3,21 @@
 #include "lsgd_host.hpp"
 #include "lsgd_kernels.hpp"
 
+namespace lsgd {
+namespace {
+
+// Plain streaming copy: one 16-byte unit per lane, in the kernels' XCD-chunked
+// block order.
+__global__ __launch_bounds__(kBlock) void stream_copy_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
+                                                            int64_t units, uint32_t chunk) {
+    for_units(units, chunk, 1, [&](int64_t u) {
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
+    });
+}
+
+}  // namespace
+}  // namespace lsgd
+
 using namespace lsgd;
 
 extern "C" {

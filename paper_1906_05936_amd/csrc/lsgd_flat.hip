@@ -6,6 +6,7 @@
 
 #include "lsgd_host.hpp"
 #include "lsgd_kernels.hpp"
+#include "lsgd_schedule.hpp"
 
 namespace lsgd {
 namespace {

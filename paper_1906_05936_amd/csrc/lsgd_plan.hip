@@ -16,7 +16,7 @@
 #include <algorithm>
 
 #include "lsgd_host.hpp"
-#include "lsgd_kernels.hpp"
+#include "lsgd_plan_kernels.hpp"
 
 struct lsgd_plan {
     int device;

@@ -1,0 +1,371 @@
+// Device code of liblsgd's multi-tensor plans: the fused step over a list of
+// tensors in one launch (chunk and bucket tables built by lsgd_plan_create),
+// its copy-out pass, and the LARS step. Included by lsgd_plan.hip only.
+#pragma once
+
+#include "lsgd_kernels.hpp"
+
+#pragma clang fp contract(off)
+
+namespace lsgd {
+
+// ------------------------------------------------------------- multi-tensor plan
+
+// One piece of one tensor: elements [start, start+len). Pieces start at
+// multiples of the unit size; only a tensor's last piece can end ragged.
+struct PlanChunk {
+    int32_t tensor;
+    int32_t pad_;
+    int64_t start;
+    int64_t len;
+};
+
+// Per tensor the device pointer table holds `stride` entries:
+// [p, m, grads in member order (N), replicas (R)].
+struct PlanArgs {
+    const PlanChunk* chunks;
+    const int32_t* bucket_begin;  // [n_buckets + 1]: workgroup b runs chunks [begin[b], begin[b+1])
+    void* const* ptrs;
+    int32_t stride, n_workers, n_groups, W;
+    int32_t n_replicas, rdt;
+    int32_t n_buckets;
+    uint32_t xcd_chunk;
+    const float* lr_ptr;
+    Hyper h;
+};
+
+struct PlanSrc {
+    void* const* t;  // this tensor's row of the pointer table
+    const PlanArgs& a;
+    Hyper h;
+    __device__ const void* grad(int k) const { return read_table(&t[2 + k]); }
+    __device__ float* p() const { return static_cast<float*>(read_table(&t[0])); }
+    __device__ float* m() const { return static_cast<float*>(read_table(&t[1])); }
+    __device__ void* replica(int r) const { return read_table(&t[2 + a.n_workers + r]); }
+    __device__ int n_replicas() const { return a.n_replicas; }
+    __device__ int rdt() const { return a.rdt; }
+    __device__ Hyper hyper() const { return h; }
+    __device__ int bcast_grad() const { return 0; }
+    __device__ int n_workers() const { return a.n_workers; }
+};
+
+// One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
+// (one large piece, or several small tensors). Chunk and pointer-table reads
+// are uniform per workgroup. chunk(s, ch, c) processes chunk c.
+template <typename ChunkFn>
+__device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn& chunk) {
+    const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
+    if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
+    const Hyper h = resolve_hyper(a.h, a.lr_ptr);
+    const int32_t c_end = read_table(&a.bucket_begin[b + 1]);
+    for (int32_t c = read_table(&a.bucket_begin[b]); c < c_end; ++c) {
+        const PlanChunk* cp = &a.chunks[c];
+        const PlanChunk ch{read_table(&cp->tensor), 0, read_table(&cp->start), read_table(&cp->len)};
+        const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
+        chunk(s, ch, c);
+    }
+}
+
+// Compile-time (W, G): tiles of U units kBlock apart, then the units of a
+// partial last tile, then the ragged end (thread 0).
+template <typename GT, int W, int G, int U>
+__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const int64_t full = ch.len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                fused_tile_ct<GT, W, G, U, false>(s, e0, VEC);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock)
+                    fused_unit_ct<GT, W, G, false>(s, ch.start + u * VEC, VEC);
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) fused_unit_ct<GT, W, G, true>(s, ch.start + full * VEC, rem);
+    });
+}
+
+// Runtime W and G (any equal-size grouping): one unit per lane.
+template <typename GT, int LV>
+__global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
+    constexpr int VEC = Unit<GT>::VEC;
+    const int W = a.W;
+    auto gs = [&](int j) { return j * W; };
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const int64_t full = ch.len / VEC;
+        for (int64_t u = threadIdx.x; u < full; u += kBlock)
+            fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, false, ch.start + u * VEC, VEC);
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0)
+            fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, false, ch.start + full * VEC, rem);
+    });
+}
+
+// Copy-out pass over a plan's chunks (see copy_out_kernel).
+template <int VEC, int U>
+__global__ __launch_bounds__(kBlock) void copy_out_plan_kernel(PlanArgs a) {
+    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const float* p = s.p();
+        auto rep = [&](int r) { return s.replica(r); };
+        const int64_t full = ch.len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                copy_out_tile<VEC, U, false>(p, rep, a.n_replicas, a.rdt, e0, VEC);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * VEC};
+                    copy_out_tile<VEC, 1, false>(p, rep, a.n_replicas, a.rdt, e, VEC);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            copy_out_tile<VEC, 1, true>(p, rep, a.n_replicas, a.rdt, e, rem);
+        }
+    });
+}
+
+}  // namespace lsgd
+
+namespace lsgd {
+
+// ------------------------------------------------------------- LARS on a plan
+//
+// Layer-wise trust ratios (LARS, which the paper names in Sec. 2 and Sec. 6;
+// definition of You, Gitman and Ginsburg, eq. 6 and Alg. 1) need each tensor's
+// ||p|| and ||gbar|| before any of its elements is updated, so a step takes
+// three launches over the plan:
+//   1. lars_norms_*: the mean gradient of every element (the same pairwise
+//      aggregation as the fused step), stored to a scratch slice per tensor,
+//      and per-chunk binary64 sums of p^2 and gbar^2 (one workgroup-level
+//      reduction per chunk, fixed order);
+//   2. lars_trust_kernel: one workgroup per tensor sums its chunks' partials
+//      (fixed order) and forms trust = eta*||p|| / (||gbar|| + wd*||p||) in
+//      binary64, rounded once to binary32; 1 when a norm is zero;
+//   3. lars_update_kernel: d = trust*(gbar + wd*p), the heavy-ball update and
+//      the copy-out, reading gbar back from the scratch.
+
+struct LarsArgs {
+    PlanArgs pa;                   // the plan's tables and counts
+    const int64_t* gbar_off;       // [n_tensors]: tensor t's slice of `gbar` starts here (floats)
+    const int32_t* tensor_chunks;  // [n_tensors + 1]: tensor t owns chunks [tc[t], tc[t+1])
+    float* gbar;                   // scratch: aggregated gradient, one slice per tensor
+    double* partials;              // [n_chunks][2]: sums of p^2 and gbar^2 over a chunk
+    float* trust;                  // [n_tensors]
+    float* trust_out;              // optional copy of the trust ratios
+    int32_t n_tensors;
+    float trust_coef;
+};
+
+// Workgroup sums of two doubles per lane, valid in thread 0. Within a wave an
+// xor butterfly: partners add the same two values, and addition is
+// commutative, so every lane holds the same bits after each round; then the
+// four wave sums in a fixed order. Every thread of the block calls it.
+__device__ __forceinline__ void block_sum2(double& a, double& b, double (*lds)[2]) {
+    static_assert(kBlock == 256, "four waves per workgroup");
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        lds[wave][0] = a;
+        lds[wave][1] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a = (lds[0][0] + lds[1][0]) + (lds[2][0] + lds[3][0]);
+        b = (lds[0][1] + lds[1][1]) + (lds[2][1] + lds[3][1]);
+    }
+    __syncthreads();
+}
+
+// Mean gradient of a tile stored to the scratch slice, squares accumulated.
+template <int T>
+__device__ __forceinline__ void lars_accumulate(const float (&p)[T], const float (&g)[T], int cnt_total,
+                                                double& sp, double& sg) {
+#pragma unroll
+    for (int v = 0; v < T; ++v) {
+        if (v < cnt_total) {
+            sp += static_cast<double>(p[v]) * static_cast<double>(p[v]);
+            sg += static_cast<double>(g[v]) * static_cast<double>(g[v]);
+        }
+    }
+}
+
+template <typename GT, int U, bool TAIL>
+__device__ __forceinline__ void lars_tile_out(const PlanSrc& s, float* gb, const int64_t (&e)[U], int cnt,
+                                              const float (&gbar)[U * Unit<GT>::VEC], double& sp, double& sg) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    float p[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        store_f32_cached<VEC, TAIL>(gb, e[q], cnt, slice<VEC, T>(gbar, q));
+        load_f32_cached<VEC, TAIL>(s.p(), e[q], cnt, slice<VEC, T>(p, q));
+    }
+    // zero-filled tail elements add nothing, but skip them anyway
+    lars_accumulate<T>(p, gbar, TAIL ? cnt : T, sp, sg);
+}
+
+// Pass 1, compile-time (W, G).
+template <typename GT, int W, int G, int U>
+__global__ __launch_bounds__(kBlock) void lars_norms_kernel(LarsArgs la) {
+    constexpr int VEC = Unit<GT>::VEC;
+    __shared__ double lds[kBlock / 64][2];
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t c) {
+        float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        double sp = 0.0, sg = 0.0;
+        const int64_t full = ch.len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                float gbar[U * VEC];
+                mean_tile_ct<GT, W, G, U, false>(s, e0, VEC, gbar);
+                lars_tile_out<GT, U, false>(s, gb, e0, VEC, gbar, sp, sg);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * VEC};
+                    float gbar[VEC];
+                    mean_tile_ct<GT, W, G, 1, false>(s, e, VEC, gbar);
+                    lars_tile_out<GT, 1, false>(s, gb, e, VEC, gbar, sp, sg);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            float gbar[VEC];
+            mean_tile_ct<GT, W, G, 1, true>(s, e, rem, gbar);
+            lars_tile_out<GT, 1, true>(s, gb, e, rem, gbar, sp, sg);
+        }
+        block_sum2(sp, sg, lds);
+        if (threadIdx.x == 0) {
+            la.partials[2 * static_cast<int64_t>(c)] = sp;
+            la.partials[2 * static_cast<int64_t>(c) + 1] = sg;
+        }
+    });
+}
+
+// Pass 1, runtime W and G (equal groups): one unit per lane.
+template <typename GT, int LV>
+__global__ __launch_bounds__(kBlock) void lars_norms_seg(LarsArgs la) {
+    constexpr int VEC = Unit<GT>::VEC;
+    __shared__ double lds[kBlock / 64][2];
+    const int W = la.pa.W;
+    auto gs = [&](int j) { return j * W; };
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t c) {
+        float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        double sp = 0.0, sg = 0.0;
+        const int64_t full = ch.len / VEC;
+        for (int64_t u = threadIdx.x; u < full; u += kBlock) {
+            const int64_t e[1] = {ch.start + u * VEC};
+            float gbar[VEC];
+            mean_unit_seg<GT, LV, false>(s, la.pa.n_workers, la.pa.n_groups, gs, false, e[0], VEC, gbar);
+            lars_tile_out<GT, 1, false>(s, gb, e, VEC, gbar, sp, sg);
+        }
+        const int rem = static_cast<int>(ch.len - full * VEC);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * VEC};
+            float gbar[VEC];
+            mean_unit_seg<GT, LV, true>(s, la.pa.n_workers, la.pa.n_groups, gs, false, e[0], rem, gbar);
+            lars_tile_out<GT, 1, true>(s, gb, e, rem, gbar, sp, sg);
+        }
+        block_sum2(sp, sg, lds);
+        if (threadIdx.x == 0) {
+            la.partials[2 * static_cast<int64_t>(c)] = sp;
+            la.partials[2 * static_cast<int64_t>(c) + 1] = sg;
+        }
+    });
+}
+
+// Pass 2: one workgroup per tensor.
+static __global__ __launch_bounds__(kBlock) void lars_trust_kernel(LarsArgs la) {
+    __shared__ double lds[kBlock / 64][2];
+    const int32_t t = static_cast<int32_t>(blockIdx.x);
+    if (t >= la.n_tensors) return;
+    const int32_t c0 = la.tensor_chunks[t], c1 = la.tensor_chunks[t + 1];
+    double sp = 0.0, sg = 0.0;
+    for (int32_t c = c0 + static_cast<int32_t>(threadIdx.x); c < c1; c += kBlock) {
+        sp += la.partials[2 * static_cast<int64_t>(c)];
+        sg += la.partials[2 * static_cast<int64_t>(c) + 1];
+    }
+    block_sum2(sp, sg, lds);
+    if (threadIdx.x == 0) {
+        const double wn = sqrt(sp), gn = sqrt(sg);
+        const double wd = static_cast<double>(la.pa.h.wd);
+        const float tr = (wn == 0.0 || gn == 0.0)
+                             ? 1.0f
+                             : static_cast<float>((static_cast<double>(la.trust_coef) * wn) / (gn + wd * wn));
+        la.trust[t] = tr;
+        if (la.trust_out) la.trust_out[t] = tr;
+    }
+}
+
+// Pass 3: trust-scaled update of U binary32 units per lane.
+template <int VEC>
+__device__ __forceinline__ void lars_update(const Hyper& h, float trust, const float (&gbar)[VEC],
+                                            float (&p)[VEC], float (&m)[VEC]) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        const float decayed = gbar[v] + h.wd * p[v];
+        const float d = trust * decayed;
+        m[v] = h.mu * m[v] + d;
+        p[v] = p[v] - h.lr * m[v];
+    }
+}
+
+template <int U, bool TAIL>
+__device__ __forceinline__ void lars_update_tile(const PlanSrc& s, const float* gb, float trust,
+                                                 const int64_t (&e0)[U], int cnt) {
+    constexpr int T = U * 4;
+    float g[T], p[T], m[T];
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(gb, e0[q], cnt, slice<4, T>(g, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(s.p(), e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(s.m(), e0[q], cnt, slice<4, T>(m, q));
+    lars_update<T>(s.hyper(), trust, g, p, m);
+    store_state<4, U, TAIL>(s, e0, cnt, p, m);
+}
+
+template <int U>
+__global__ __launch_bounds__(kBlock) void lars_update_kernel(LarsArgs la) {
+    for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+        const float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
+        const float trust = read_table(&la.trust[ch.tensor]);
+        const int64_t full = ch.len / 4;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * 4;
+                lars_update_tile<U, false>(s, gb, trust, e0, 4);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock) {
+                    const int64_t e[1] = {ch.start + u * 4};
+                    lars_update_tile<1, false>(s, gb, trust, e, 4);
+                }
+            }
+        }
+        const int rem = static_cast<int>(ch.len - full * 4);
+        if (rem != 0 && threadIdx.x == 0) {
+            const int64_t e[1] = {ch.start + full * 4};
+            lars_update_tile<1, true>(s, gb, trust, e, rem);
+        }
+    });
+}
+
+}  // namespace lsgd
