@@ -282,8 +282,12 @@ LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int
  *             when n_replicas == 0.
  * The plan holds the pointers: the tensors must stay allocated, unmoved, while
  * the plan is used. Counts: n_tensors >= 1, 1 <= n_workers <= LSGD_MAX_WORKERS,
- * 0 <= n_replicas <= LSGD_MAX_REPLICAS. The plan is bound to the device current
- * at creation.
+ * 0 <= n_replicas <= LSGD_MAX_REPLICAS. group_of_worker may be any partition
+ * into n_groups non-empty groups (LSGD_ERR_GROUPS otherwise); the default
+ * mean-of-means step and the LARS step need equal group sizes and return
+ * LSGD_ERR_GROUPS on a plan whose groups differ, which takes the paper-literal
+ * reduction (lsgd_step_plan_ex). The plan is bound to the device current at
+ * creation.
  * lsgd_plan_create allocates device memory (LSGD_ERR_HIP if that fails) and
  * synchronizes the null stream once; lsgd_step_plan allocates nothing.
  */
@@ -299,8 +303,12 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                     float weight_decay, void* stream);
 
-/* lsgd_step_plan with options: only lr_device is taken (reduction must be
- * LSGD_REDUCE_MEAN_OF_MEANS and broadcast_grad zero, else LSGD_ERR_UNSUPPORTED). */
+/* lsgd_step_plan with options, as lsgd_step_ex: the paper-literal reduction
+ * (any partition), the gradient broadcast (binary32 gradients only, else
+ * LSGD_ERR_DTYPE; every worker's gradient tensors are then written, so none
+ * may overlap another buffer of the plan: LSGD_ERR_ALIAS) and lr_device.
+ * Errors as lsgd_step_plan, plus LSGD_ERR_UNSUPPORTED (unknown reduction),
+ * LSGD_ERR_GROUPS (mean of means on unequal groups), LSGD_ERR_ALIGN. */
 LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float momentum_coef,
                                        float weight_decay, const lsgd_step_options* options,
                                        void* stream);

@@ -347,15 +347,19 @@ class Plan:
         check(st)
         self._handle = handle
 
-    def step(self, lr, momentum_coef, weight_decay, stream=None, lr_device=None):
+    def step(self, lr, momentum_coef, weight_decay, stream=None, lr_device=None,
+             reduction="mean_of_means", broadcast_grad=False):
+        """lsgd_step_plan, or lsgd_step_plan_ex with the paper-literal
+        reduction, the gradient broadcast or a device learning rate."""
         if self._handle is None:
             raise RuntimeError("plan is closed")
+        plain = reduction in ("mean_of_means", REDUCE_MEAN_OF_MEANS) and not broadcast_grad and lr_device is None
         with torch.cuda.device(self.device):
-            if lr_device is None:
+            if plain:
                 st = lib.lsgd_step_plan(self._handle, lr, momentum_coef, weight_decay,
                                         _stream(stream, self.device))
             else:
-                opts = _options("mean_of_means", False, lr_device, self.device)
+                opts = _options(reduction, broadcast_grad, lr_device, self.device)
                 st = lib.lsgd_step_plan_ex(self._handle, lr, momentum_coef, weight_decay,
                                            ctypes.byref(opts), _stream(stream, self.device))
         check(st)

@@ -33,6 +33,10 @@ struct lsgd_plan {
     int64_t* d_gbar_off;
     int32_t* d_tensor_chunks;
     std::vector<lsgd::Range>* ranges;
+    // the partition: groups of equal size W (W = 0 otherwise), group j is
+    // members [group_start[j], group_start[j+1]) of the member order
+    int32_t max_group;
+    int32_t group_start[lsgd::kMaxWorkers + 1];
 };
 
 namespace lsgd {
@@ -108,6 +112,7 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     a.h = h;
     a.lr_ptr = lr_device;
     a.n_buckets = plan->n_buckets;
+    for (int32_t j = 0; j <= plan->n_groups; ++j) a.group_start[j] = static_cast<uint8_t>(plan->group_start[j]);
     const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
     ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
     a.xcd_chunk = ls.xcd_chunk;
@@ -188,9 +193,17 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     *out = nullptr;
     if (n_tensors < 1) return fail(LSGD_ERR_SIZE, "n_tensors=%d < 1", n_tensors);
     if (!numel) return fail(LSGD_ERR_NULL, "numel is NULL");
-    std::vector<int32_t> order;
-    lsgd_status st = member_order(n_workers, group_of_worker, n_groups, order);
+    std::vector<int32_t> order, gstart;
+    lsgd_status st = partition_order(n_workers, group_of_worker, n_groups, order, gstart);
     if (st != LSGD_OK) return st;
+    // equal group sizes (the mean-of-means step needs them) give W > 0
+    int32_t max_group = 0;
+    bool equal = true;
+    for (int32_t j = 0; j < n_groups; ++j) {
+        const int32_t c = gstart[j + 1] - gstart[j];
+        max_group = std::max(max_group, c);
+        equal = equal && c == gstart[1] - gstart[0];
+    }
     if (gdt != LSGD_F32 && gdt != LSGD_BF16) return fail(LSGD_ERR_DTYPE, "gradient dtype %d", (int)gdt);
     if (rdt != LSGD_F32 && rdt != LSGD_BF16) return fail(LSGD_ERR_DTYPE, "replica dtype %d", (int)rdt);
     if (n_replicas < 0 || n_replicas > kMaxReplicas)
@@ -205,7 +218,7 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     std::vector<PlanChunk> chunks;
     std::vector<int32_t> bucket_begin;
     // one tile pass of the kernel, times the launch shape's passes per workgroup
-    const int32_t W = n_workers / n_groups;
+    const int32_t W = equal ? n_workers / n_groups : 0;
     const int tile = gdt == LSGD_BF16 ? pick_plan<uint16_t>(W, n_groups).tile : pick_plan<float>(W, n_groups).tile;
     const int64_t kPiece = (gdt == LSGD_BF16 ? piece_elems<uint16_t>(tile) : piece_elems<float>(tile)) *
                            launch_passes_per_block();
@@ -268,7 +281,9 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     p->n_tensors = n_tensors;
     p->n_workers = n_workers;
     p->n_groups = n_groups;
-    p->W = n_workers / n_groups;
+    p->W = W;
+    p->max_group = max_group;
+    for (int32_t j = 0; j <= n_groups; ++j) p->group_start[j] = gstart[j];
     p->n_replicas = n_replicas;
     p->gdt = gdt;
     p->rdt = rdt;
@@ -309,21 +324,47 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
                                        float weight_decay, const lsgd_step_options* options,
                                        void* stream) {
     if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
-    const float* lr_device = nullptr;
-    if (options) {
-        if (options->reduction != LSGD_REDUCE_MEAN_OF_MEANS || options->broadcast_grad != 0)
-            return fail(LSGD_ERR_UNSUPPORTED, "plans take only lr_device among the step options");
-        lr_device = options->lr_device;
-        if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
-            return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
+    const lsgd_step_options none = {LSGD_REDUCE_MEAN_OF_MEANS, 0, nullptr};
+    const lsgd_step_options& o = options ? *options : none;
+    if (o.reduction != LSGD_REDUCE_MEAN_OF_MEANS && o.reduction != LSGD_REDUCE_LITERAL)
+        return fail(LSGD_ERR_UNSUPPORTED, "reduction %d", o.reduction);
+    const bool literal = o.reduction == LSGD_REDUCE_LITERAL;
+    const bool bcast = o.broadcast_grad != 0;
+    const float* lr_device = o.lr_device;
+    if (!literal && plan->W == 0)
+        return fail(LSGD_ERR_GROUPS, "the mean-of-means step needs equal group sizes; this plan's differ");
+    if (bcast && plan->gdt != LSGD_F32)
+        return fail(LSGD_ERR_DTYPE, "broadcast_grad needs binary32 gradients");
+    if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
+    if (bcast || lr_device) {
+        std::vector<Range> ranges(*plan->ranges);
+        if (bcast)   // the gradient buffers are written too
+            for (Range& r : ranges)
+                if (strcmp(r.what, "grads") == 0) r.written = true;
+        if (lr_device) {
+            const uintptr_t lb = reinterpret_cast<uintptr_t>(lr_device);
+            ranges.push_back(Range{lb, lb + sizeof(float), false, "lr_device"});
+        }
+        lsgd_status st = check_overlap(ranges);
+        if (st != LSGD_OK) return st;
     }
     if (plan->n_buckets == 0) return LSGD_OK;
     lsgd_status st = check_device(plan);
     if (st != LSGD_OK) return st;
     LaunchShape ls;
     PlanArgs a = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
-    const PlanKernel k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
-                                                : pick_plan<float>(plan->W, plan->n_groups).kernel;
+    a.literal = literal ? 1 : 0;
+    a.bcast_grad = bcast ? 1 : 0;
+    PlanKernel k;
+    if (literal || plan->W == 0) {
+        const int32_t max_count = std::max(plan->max_group, plan->n_groups);
+        k = seg_levels(max_count) == 5 ? (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 5> : step_plan_seg<float, 5>)
+                                       : (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 8> : step_plan_seg<float, 8>);
+    } else {
+        k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
+                                   : pick_plan<float>(plan->W, plan->n_groups).kernel;
+    }
     const bool split = separate_copy_out(plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4, plan->n_replicas,
                                          plan->rdt == LSGD_BF16 ? 2 : 4);
     if (split) a.n_replicas = 0;
@@ -376,6 +417,7 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
     }
     lsgd_status st = check_overlap(ranges);
     if (st != LSGD_OK) return st;
+    if (plan->W == 0) return fail(LSGD_ERR_GROUPS, "the LARS step needs equal group sizes; this plan's differ");
     if ((st = check_device(plan)) != LSGD_OK) return st;
 
     LarsArgs la;

@@ -32,6 +32,9 @@ struct PlanArgs {
     uint32_t xcd_chunk;
     const float* lr_ptr;
     Hyper h;
+    int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
+    int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
+    uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
 };
 
 struct PlanSrc {
@@ -45,7 +48,7 @@ struct PlanSrc {
     __device__ int n_replicas() const { return a.n_replicas; }
     __device__ int rdt() const { return a.rdt; }
     __device__ Hyper hyper() const { return h; }
-    __device__ int bcast_grad() const { return 0; }
+    __device__ int bcast_grad() const { return a.bcast_grad; }
     __device__ int n_workers() const { return a.n_workers; }
 };
 
@@ -89,19 +92,20 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     });
 }
 
-// Runtime W and G (any equal-size grouping): one unit per lane.
+// Runtime group layouts (non-power-of-two or large counts, and the
+// paper-literal reduction over any partition): one unit per lane.
 template <typename GT, int LV>
 __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const int W = a.W;
-    auto gs = [&](int j) { return j * W; };
+    const bool literal = a.literal != 0;
+    auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
     for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t u = threadIdx.x; u < full; u += kBlock)
-            fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, false, ch.start + u * VEC, VEC);
+            fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, ch.start + u * VEC, VEC);
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0)
-            fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, false, ch.start + full * VEC, rem);
+            fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, literal, ch.start + full * VEC, rem);
     });
 }
 

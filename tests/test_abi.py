@@ -181,7 +181,8 @@ def plan_create(numel=(100, 64), G=2, gow=(0, 0, 1, 1), R=0, gdt=0, rdt=0, param
 def test_plan_validation_errors():
     assert plan_create(numel=()) == SIZE
     assert plan_create(numel=(100, -1)) == SIZE
-    assert plan_create(gow=(0, 0, 0, 1)) == GROUPS
+    assert plan_create(gow=(0, 0, 0, 3)) == GROUPS          # group id out of range
+    assert plan_create(gow=(0, 0, 0, 0)) == GROUPS          # group 1 empty
     assert plan_create(gdt=4) == DTYPE
     assert plan_create(R=1, replicas=None) == NULL
     assert plan_create(R=200, replicas=[A] * 400) == SIZE

@@ -728,3 +728,81 @@ def test_graph_with_separate_copy_out_matches_eager():
         del graph
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+
+
+# ---------------------------------------------------------------- plans: literal reduction, broadcast
+
+@pytest.mark.parametrize("gow,G,gdt,R,bcast", [
+    ([0, 0, 1, 1, 1, 2, 2, 2, 2, 2, 3, 3, 3, 3, 3, 3], 4, "f32", 3, False),   # node sizes 2, 3, 5, 6
+    ([2, 0, 1, 1, 0, 2, 1], 3, "bf16", 2, False),
+    ([0, 0, 1, 1, 1, 2, 2, 2, 2, 2, 3, 3, 3, 3, 3, 3], 4, "f32", 1, True),
+    (workloads.contiguous_groups(4, 4), 4, "f32", 16, True),
+])
+def test_plan_literal_reduction_and_broadcast_match_oracle(gow, G, gdt, R, bcast):
+    """Plans over any partition take the paper-literal reduction, optionally
+    broadcasting the mean gradient into every worker's tensors; every tensor
+    bit-exact against the oracle's literal step."""
+    log("plan literal gow=%s G=%d %s R=%d bcast=%d" % (gow, G, gdt, R, bcast))
+    rng = np.random.default_rng(len(gow) * 7 + R)
+    N = len(gow)
+    T = len(PLAN_SIZES)
+    ph = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in PLAN_SIZES]
+    mh = [np.zeros(s, np.float32) for s in PLAN_SIZES]
+    params = [to_dev(x) for x in ph]
+    mom = [to_dev(x) for x in mh]
+    gh = [[rand_host(rng, s, 1e-2, gdt) for s in PLAN_SIZES] for _ in range(N)]
+    grads = [[to_dev(x) for x in row] for row in gh]
+    reps = [[torch.empty(s, device=DEV) for s in PLAN_SIZES] for _ in range(R)]
+    plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+    equal = len(set(gow.count(j) for j in range(G))) == 1
+    if not equal:
+        with pytest.raises(lsgd.LsgdError) as e:
+            plan.step(0.1, 0.9, 1e-4)
+        assert e.value.name == "LSGD_ERR_GROUPS"
+        with pytest.raises(lsgd.LsgdError) as e:
+            plan.lars_step(0.1, 0.9, 1e-4, 1e-3)
+        assert e.value.name == "LSGD_ERR_GROUPS"
+    for step in range(2):
+        if step:
+            gh = [[rand_host(rng, s, 1e-2, gdt) for s in PLAN_SIZES] for _ in range(N)]
+            for w in range(N):
+                for t in range(T):
+                    grads[w][t].copy_(to_dev(gh[w][t]))
+        plan.step(0.1, 0.9, 1e-4, reduction="literal", broadcast_grad=bcast)
+        torch.cuda.synchronize()
+        for t in range(T):
+            rr = [np.zeros(PLAN_SIZES[t], np.float32) for _ in range(R)]
+            gt = [gh[w][t].copy() for w in range(N)]
+            oracle.lsgd_step_literal(ph[t], mh[t], gt, gow, G, 0.1, 0.9, 1e-4, rr, oracle.F32,
+                                     broadcast_grad=bcast)
+            assert_close(to_host(params[t]), ph[t], "params[%d] step %d" % (t, step))
+            assert_close(to_host(mom[t]), mh[t], "momentum[%d] step %d" % (t, step))
+            for r in range(R):
+                assert np.array_equal(to_host(reps[r][t]), rr[r]), (t, r)
+            if bcast:
+                for w in (0, N - 1):
+                    assert np.array_equal(to_host(grads[w][t]), gt[w]), (t, w)
+    plan.close()
+
+
+def test_plan_broadcast_rejects_shared_gradient_tensors():
+    """With the broadcast every gradient tensor is written: two workers
+    sharing one tensor are rejected (LSGD_ERR_ALIAS), bf16 gradients too
+    (LSGD_ERR_DTYPE); the plain step on the same plan still runs."""
+    n = 4096
+    p, m = torch.zeros(n, device=DEV), torch.zeros(n, device=DEV)
+    g = torch.ones(n, device=DEV)
+    plan = lsgd.Plan([p], [m], [[g], [g]], [0, 1], 2)
+    with pytest.raises(lsgd.LsgdError) as e:
+        plan.step(0.1, 0.9, 1e-4, broadcast_grad=True)
+    assert e.value.name == "LSGD_ERR_ALIAS"
+    plan.step(0.1, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(p).item() == n
+    gb = [torch.ones(n, device=DEV, dtype=torch.bfloat16) for _ in range(2)]
+    plan2 = lsgd.Plan([p], [m], [[gb[0]], [gb[1]]], [0, 1], 2)
+    with pytest.raises(lsgd.LsgdError) as e:
+        plan2.step(0.1, 0.9, 1e-4, broadcast_grad=True)
+    assert e.value.name == "LSGD_ERR_DTYPE"
+    plan.close()
+    plan2.close()
