@@ -56,6 +56,8 @@ def parse_args(argv=None):
     ap.add_argument("--lars", action="store_true",
                     help="LARS step (a trust ratio per tensor) on a multi-tensor workload's plan")
     ap.add_argument("--trust-coef", type=float, default=1e-3, help="LARS trust coefficient")
+    ap.add_argument("--lars-exclude-vectors", action="store_true",
+                    help="LARS: one-dimensional tensors (batch norm, biases) take trust 1")
     ap.add_argument("--copy-out", choices=("auto", "fused", "separate"), default="auto",
                     help="replicas written inside the step kernel or by a copy-out pass of their own")
     ap.add_argument("--broadcast-grad", action="store_true",
@@ -74,7 +76,8 @@ def parse_args(argv=None):
 class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
-    def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3):
+    def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3,
+                 lars_exclude=None):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
@@ -90,7 +93,7 @@ class Setup:
             raise SystemExit("plans run the mean-of-means step without broadcast")
         if lars and not wl.tensor_sizes:
             raise SystemExit("--lars needs a workload with per-tensor sizes (a plan)")
-        self.lars, self.trust_coef = lars, trust_coef
+        self.lars, self.trust_coef, self.lars_exclude = lars, trust_coef, lars_exclude
         rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
         stream = torch.cuda.current_stream(dev)
         flat_p = workloads.init_params(wl, dev)
@@ -112,6 +115,8 @@ class Setup:
             hyper = (ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd))
             s = ctypes.c_void_p(stream.cuda_stream)
             if lars:
+                if lars_exclude is not None:
+                    self.plan.set_lars_exclude(lars_exclude)
                 self.workspace = torch.empty(self.plan.lars_workspace_size(), dtype=torch.uint8, device=dev)
                 fn = lib.lsgd_lars_step_plan
                 extra = (ctypes.c_float(trust_coef), ctypes.c_void_p(self.workspace.data_ptr()),
@@ -343,19 +348,23 @@ def _cpu_baseline_lars(setup, seconds, S):
 
     wl, R = setup.wl, setup.R
     host = lambda t: t.detach().cpu().numpy().copy()
+    excl = setup.lars_exclude or [False] * len(setup.params)
     tensors, got = [], 0
     for t in range(len(setup.params)):
         if got >= S:
             break
         ne = setup.params[t].numel()
         tensors.append((host(setup.params[t]), host(setup.mom[t]),
-                        [host(g[t]) for g in setup.grads], [np.zeros(ne, np.float32) for _ in range(R)]))
+                        [host(g[t]) for g in setup.grads], [np.zeros(ne, np.float32) for _ in range(R)], excl[t]))
         got += ne
     steps = 0
     t0 = time.perf_counter()
     while True:
-        for p, m, grads, reps in tensors:
-            oracle.lars_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, setup.trust_coef, reps)
+        for p, m, grads, reps, ex in tensors:
+            if ex:   # trust 1: the plain step
+                oracle.lsgd_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, reps)
+            else:
+                oracle.lars_step(p, m, grads, setup.gow, wl.groups, wl.lr, wl.mu, wl.wd, setup.trust_coef, reps)
         steps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -577,7 +586,12 @@ def main(argv=None):
         # writes and re-reads the mean gradient
         return (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0) + (12 * wl.n if args.lars else 0)
 
-    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef)
+    lars_excl = None
+    if args.lars_exclude_vectors:
+        if wl.tensor_sizes != tuple(workloads.resnet50_param_sizes()):
+            raise SystemExit("--lars-exclude-vectors knows the ResNet-50 tensor list only")
+        lars_excl = workloads.resnet50_vector_params()
+    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl)
     ms = time_steps(setup, args.steps, args.warmup)
     alg = wl.algorithmic_bytes(R) + extra_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
@@ -594,7 +608,8 @@ def main(argv=None):
                    "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1,
                    "reduction": setup.reduction, "broadcast_grad": setup.broadcast_grad,
                    **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {}),
-                   **({"lars": True, "trust_coef": args.trust_coef} if args.lars else {}),
+                   **({"lars": True, "trust_coef": args.trust_coef,
+                       "lars_excluded_tensors": sum(lars_excl) if lars_excl else 0} if args.lars else {}),
                    "copy_out": ("separate pass" if separate_copy_out(wl, R, args.copy_out) and not args.lars
                                 else "in the step kernel")},
         "steps_per_s": round(1e3 / ms, 2),
@@ -611,7 +626,7 @@ def main(argv=None):
         setup.close()
         del setup
         torch.cuda.empty_cache()
-        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef)
+        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl)
         ms0 = time_steps(setup, args.steps, args.warmup)
         alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),

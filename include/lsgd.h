@@ -354,6 +354,16 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
                                          size_t workspace_bytes, float* trust_out,
                                          const float* lr_device, void* stream);
 
+/* Tensors excluded from the layer-wise rates: exclude[t] != 0 gives tensor t
+ * trust 1 in every later lsgd_lars_step_plan (so its update is the plain
+ * step of lsgd_step_plan); NULL clears every exclusion. Implementations
+ * commonly exclude biases and batch-normalisation parameters; the paper names
+ * no exclusions, and a new plan excludes nothing. exclude is a host array of
+ * n_tensors bytes. Copies to device memory synchronously: call it between
+ * steps, not inside a captured graph. Errors: LSGD_ERR_NULL (plan),
+ * LSGD_ERR_HIP (wrong device or copy failure). */
+LSGD_API lsgd_status lsgd_plan_set_lars_exclude(lsgd_plan* plan, const uint8_t* exclude);
+
 /* Frees the plan's device tables. NULL-safe. The caller synchronizes every
  * stream that ran lsgd_step_plan or lsgd_lars_step_plan with this plan first. */
 LSGD_API void lsgd_plan_destroy(lsgd_plan* plan);

@@ -32,7 +32,7 @@ EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_step", "lsgd_step_ex", "lsgd_lr_at", "lsgd_lr_schedule_step", "lsgd_plan_create",
            "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
            "lsgd_lars_workspace_size", "lsgd_lars_step_plan", "lsgd_set_copy_out_mode",
-           "lsgd_get_copy_out_mode")
+           "lsgd_get_copy_out_mode", "lsgd_plan_set_lars_exclude")
 
 
 class StepOptions(ctypes.Structure):
@@ -84,6 +84,7 @@ def _load():
     lib.lsgd_lr_schedule_step.argtypes = [ctypes.POINTER(LrSchedule), P, P, P]
     lib.lsgd_lars_workspace_size.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
     lib.lsgd_set_copy_out_mode.argtypes = [i32]
+    lib.lsgd_plan_set_lars_exclude.argtypes = [P, P]
     lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
     lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
@@ -363,6 +364,19 @@ class Plan:
                 st = lib.lsgd_step_plan_ex(self._handle, lr, momentum_coef, weight_decay,
                                            ctypes.byref(opts), _stream(stream, self.device))
         check(st)
+
+    def set_lars_exclude(self, exclude=None):
+        """lsgd_plan_set_lars_exclude: tensors whose flag is true take trust 1
+        in later LARS steps; None clears every exclusion."""
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        arr = None
+        if exclude is not None:
+            if len(exclude) != len(self._keep[0]):
+                raise ValueError("exclude needs one flag per tensor")
+            arr = (ctypes.c_uint8 * len(exclude))(*[1 if x else 0 for x in exclude])
+        with torch.cuda.device(self.device):
+            check(lib.lsgd_plan_set_lars_exclude(self._handle, arr))
 
     def lars_workspace_size(self):
         """Bytes of device workspace lsgd_lars_step_plan needs for this plan."""

@@ -32,6 +32,7 @@ struct lsgd_plan {
     int64_t gbar_floats;
     int64_t* d_gbar_off;
     int32_t* d_tensor_chunks;
+    uint8_t* d_lars_exclude;   // [n_tensors], zero until lsgd_plan_set_lars_exclude
     std::vector<lsgd::Range>* ranges;
     // the partition: groups of equal size W (W = 0 otherwise), group j is
     // members [group_start[j], group_start[j+1]) of the member order
@@ -173,6 +174,7 @@ void free_plan(lsgd_plan* p) {
     if (p->d_ptrs) (void)hipFree(p->d_ptrs);
     if (p->d_gbar_off) (void)hipFree(p->d_gbar_off);
     if (p->d_tensor_chunks) (void)hipFree(p->d_tensor_chunks);
+    if (p->d_lars_exclude) (void)hipFree(p->d_lars_exclude);
     delete p->ranges;
     delete p;
 }
@@ -306,6 +308,11 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
         e = hipMemcpy(p->d_bucket_begin, bucket_begin.data(), bucket_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(p->d_ptrs, table.data(), table_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMalloc(&p->d_gbar_off, gbar_off.size() * sizeof(int64_t));
+    if (e == hipSuccess) e = hipMalloc(&p->d_lars_exclude, static_cast<size_t>(n_tensors));
+    if (e == hipSuccess) {
+        const std::vector<uint8_t> none(static_cast<size_t>(n_tensors), 0);
+        e = hipMemcpy(p->d_lars_exclude, none.data(), none.size(), hipMemcpyHostToDevice);
+    }
     if (e == hipSuccess) e = hipMalloc(&p->d_tensor_chunks, tensor_chunks.size() * sizeof(int32_t));
     if (e == hipSuccess)
         e = hipMemcpy(p->d_gbar_off, gbar_off.data(), gbar_off.size() * sizeof(int64_t), hipMemcpyHostToDevice);
@@ -431,6 +438,7 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
     la.partials = reinterpret_cast<double*>(ws + l.partials);
     la.trust = reinterpret_cast<float*>(ws + l.trust);
     la.trust_out = trust_out;
+    la.exclude = plan->d_lars_exclude;
     la.n_tensors = plan->n_tensors;
     la.trust_coef = trust_coef;
     const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -446,6 +454,18 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
         hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
         if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK) return st;
     }
+    return LSGD_OK;
+}
+
+LSGD_API lsgd_status lsgd_plan_set_lars_exclude(lsgd_plan* plan, const uint8_t* exclude) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    std::vector<uint8_t> flags(static_cast<size_t>(plan->n_tensors), 0);
+    if (exclude)
+        for (int32_t t = 0; t < plan->n_tensors; ++t) flags[t] = exclude[t] ? 1 : 0;
+    lsgd_status st = check_device(plan);
+    if (st != LSGD_OK) return st;
+    const hipError_t e = hipMemcpy(plan->d_lars_exclude, flags.data(), flags.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(LSGD_ERR_HIP, "lsgd_plan_set_lars_exclude: %s", hipGetErrorString(e));
     return LSGD_OK;
 }
 

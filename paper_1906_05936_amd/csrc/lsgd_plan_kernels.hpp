@@ -153,7 +153,8 @@ namespace lsgd {
 //      reduction per chunk, fixed order);
 //   2. lars_trust_kernel: one workgroup per tensor sums its chunks' partials
 //      (fixed order) and forms trust = eta*||p|| / (||gbar|| + wd*||p||) in
-//      binary64, rounded once to binary32; 1 when a norm is zero;
+//      binary64, rounded once to binary32; 1 when a norm is zero or the
+//      tensor is excluded from the layer-wise rates;
 //   3. lars_update_kernel: d = trust*(gbar + wd*p), the heavy-ball update and
 //      the copy-out, reading gbar back from the scratch.
 
@@ -165,6 +166,7 @@ struct LarsArgs {
     double* partials;              // [n_chunks][2]: sums of p^2 and gbar^2 over a chunk
     float* trust;                  // [n_tensors]
     float* trust_out;              // optional copy of the trust ratios
+    const uint8_t* exclude;        // [n_tensors]: nonzero = the tensor takes trust 1
     int32_t n_tensors;
     float trust_coef;
 };
@@ -309,7 +311,7 @@ static __global__ __launch_bounds__(kBlock) void lars_trust_kernel(LarsArgs la) 
     if (threadIdx.x == 0) {
         const double wn = sqrt(sp), gn = sqrt(sg);
         const double wd = static_cast<double>(la.pa.h.wd);
-        const float tr = (wn == 0.0 || gn == 0.0)
+        const float tr = (wn == 0.0 || gn == 0.0 || la.exclude[t] != 0)
                              ? 1.0f
                              : static_cast<float>((static_cast<double>(la.trust_coef) * wn) / (gn + wd * wn));
         la.trust[t] = tr;

@@ -46,7 +46,8 @@ def test_header_declares_the_boundary():
             "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
             "lsgd_lr_schedule_step", "lsgd_step_plan_ex", "lsgd_lars_workspace_size",
-            "lsgd_lars_step_plan", "lsgd_set_copy_out_mode", "lsgd_get_copy_out_mode"} == names
+            "lsgd_lars_step_plan", "lsgd_set_copy_out_mode", "lsgd_get_copy_out_mode",
+            "lsgd_plan_set_lars_exclude"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -287,6 +288,7 @@ def test_lars_validation():
     assert lib.lsgd_lars_workspace_size(None, ctypes.byref(n)) == NULL
     assert lib.lsgd_lars_step_plan(None, 0.1, 0.9, 1e-4, 1e-3, A, 1 << 30, None, None, None) == NULL
     assert "plan is NULL" in lib.lsgd_last_error().decode()
+    assert lib.lsgd_plan_set_lars_exclude(None, None) == NULL
 
 
 def test_last_error_is_per_thread():

@@ -269,3 +269,35 @@ def test_lars_graph_follows_the_device_schedule():
     del graph
     plan_g.close()
     plan_e.close()
+
+
+def test_lars_excluded_tensors_take_the_plain_step():
+    """Tensors flagged with lsgd_plan_set_lars_exclude take trust 1: their step
+    is the oracle's plain step bit for bit, the others' the LARS step; clearing
+    the flags brings every tensor back to LARS."""
+    c = Case(4, 4, "f32", 2, "f32", seed=91)
+    excl = [s < 100 or t == 7 for t, s in enumerate(SIZES)]   # the small vectors and one large tensor
+    c.plan.set_lars_exclude(excl)
+    for step in range(2):
+        c.new_grads()
+        trust = torch.full((len(SIZES),), -1.0, device=DEV)
+        c.plan.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, trust_out=trust)
+        torch.cuda.synchronize()
+        tg = to_host(trust)
+        for t, s in enumerate(SIZES):
+            rr = [np.zeros(s, np.float32) for _ in range(c.R)]
+            g = [c.gh[w][t] for w in range(c.N)]
+            if excl[t]:
+                oracle.lsgd_step(c.ph[t], c.mh[t], g, c.gow, c.G, 0.1, 0.9, 1e-4, rr)
+                assert tg[t] == 1.0, (t, tg[t])
+            else:
+                tr = oracle.lars_step(c.ph[t], c.mh[t], g, c.gow, c.G, 0.1, 0.9, 1e-4, TRUST_COEF, rr)
+                assert np.float32(tg[t]) == np.float32(tr), (t, tg[t], tr)
+            assert np.array_equal(to_host(c.params[t]), c.ph[t]), (t, step)
+            assert np.array_equal(to_host(c.mom[t]), c.mh[t]), (t, step)
+            for r in range(c.R):
+                assert np.array_equal(to_host(c.reps[r][t]), rr[r]), (t, r, step)
+    c.plan.set_lars_exclude(None)
+    c.new_grads()
+    c.check(0.1, 0.9, 1e-4, TRUST_COEF, 2)
+    c.plan.close()

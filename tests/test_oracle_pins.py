@@ -458,6 +458,9 @@ def test_non_finite_values_propagate():
 def test_workload_shapes():
     sizes = workloads.resnet50_param_sizes()
     assert len(sizes) == 161 and sum(sizes) == workloads.RESNET50_NUMEL
+    vec = workloads.resnet50_vector_params()
+    assert len(vec) == 161 and sum(vec) == 107                     # 53 BN pairs + the classifier bias
+    assert all(s in (64, 128, 256, 512, 1024, 2048, 1000) for s, v in zip(sizes, vec) if v)
     for wl in workloads.WORKLOADS.values():
         if wl.tensor_sizes:
             assert sum(wl.tensor_sizes) == wl.n

@@ -48,6 +48,18 @@ def resnet50_param_sizes() -> List[int]:
     return sizes
 
 
+def resnet50_vector_params() -> List[bool]:
+    """For each of resnet50_param_sizes(): True for the one-dimensional tensors
+    (batch-norm scales and shifts, the classifier bias), which LARS
+    implementations commonly exclude from the layer-wise rates."""
+    flags = [False, True, True]
+    for width, blocks in ((64, 3), (128, 4), (256, 6), (512, 3)):
+        for b in range(blocks):
+            flags += [False, True, True] * (4 if b == 0 else 3)
+    flags += [False, True]
+    return flags
+
+
 RESNET50_NUMEL = 25_557_032
 
 
