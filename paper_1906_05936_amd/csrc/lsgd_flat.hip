@@ -20,8 +20,8 @@ struct FlatPick {
 };
 
 // Compile-time (W, G) kernels for power-of-two counts up to 16 each (and
-// N <= 128); every other grouping takes the runtime-count kernel. Both give
-// the same bits.
+// N <= 128); every other grouping takes the segmented runtime-layout kernel.
+// Both give the same bits.
 template <typename GT, int W>
 FlatKernel pick_flat_g(int G) {
     constexpr int U = TileUnits<GT>::U;

@@ -26,7 +26,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kMaxWorkers = 128;   // == LSGD_MAX_WORKERS
 constexpr int kMaxReplicas = 128;  // == LSGD_MAX_REPLICAS
 constexpr int kBlock = 256;        // threads per workgroup (4 wave64)
-constexpr int kAccLevels = 8;      // runtime pairwise accumulator: counts up to 255
 
 enum : int { kF32 = 0, kBF16 = 1 };
 
@@ -326,7 +325,7 @@ __device__ __forceinline__ void pw_tree(const Leaf& leaf, float (&out)[VEC]) {
 // (which would move the slots to scratch memory). `levels` (uniform, <= LEVELS)
 // bounds the levels a push visits: pushes beyond 2^levels - 1 terms are not
 // supported.
-template <int VEC, int LEVELS = kAccLevels>
+template <int VEC, int LEVELS>
 struct PwAcc {
     float slot[LEVELS][VEC];
     uint32_t count = 0;
