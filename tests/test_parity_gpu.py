@@ -806,3 +806,36 @@ def test_plan_broadcast_rejects_shared_gradient_tensors():
     assert e.value.name == "LSGD_ERR_DTYPE"
     plan.close()
     plan2.close()
+
+
+def test_vector_longer_than_2_to_31_elements():
+    """n = 2^31 + 13 (8.6 GB per fp32 buffer, five buffers): the 64-bit
+    element offsets of the fused step, the copy-out pass and the ragged tail,
+    checked on sampled elements (including the last 64) against the oracle."""
+    n = (1 << 31) + 13
+    G, W, R = 1, 2, 1
+    log("n = %d (%.1f GB per buffer)" % (n, n * 4 / 1e9))
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(2 ** 31)
+    p = torch.randn(n, generator=gen, device=DEV).mul_(0.05)
+    m = torch.zeros(n, device=DEV)
+    grads = [torch.randn(n, generator=gen, device=DEV).mul_(0.01) for _ in range(G * W)]
+    rep = torch.empty(n, device=DEV)
+    idx = workloads.sample_indices(n, 4096, seed=31)
+    ti = torch.from_numpy(idx).to(DEV)
+    ph, mh = to_host(p.index_select(0, ti)), np.zeros(idx.size, np.float32)
+    gh = [to_host(g.index_select(0, ti)) for g in grads]
+    try:
+        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE):
+            lsgd.set_copy_out_mode(mode)
+            lsgd.step(p, m, grads, [0, 0], G, 0.1, 0.9, 1e-4, [rep])
+            rr = [np.zeros(idx.size, np.float32)]
+            oracle.lsgd_step(ph, mh, gh, [0, 0], G, 0.1, 0.9, 1e-4, rr)
+            torch.cuda.synchronize()
+            assert_close(to_host(p.index_select(0, ti)), ph, "params mode %d" % mode)
+            assert_close(to_host(m.index_select(0, ti)), mh, "momentum mode %d" % mode)
+            assert np.array_equal(to_host(rep.index_select(0, ti)), rr[0]), mode
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+    del p, m, grads, rep
+    torch.cuda.empty_cache()
