@@ -54,20 +54,31 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and with whitespace runs collapsed, so that
+    a comment-only edit keeps the digest (string literals are kept as they are;
+    the sources hold no comment markers inside strings)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_digest() -> str:
-    """SHA-256 over the kernel sources, the public header and the build flags:
-    identifies the kernels a stored profile was taken from."""
+    """SHA-256 over the kernel sources and public headers (comments and layout
+    stripped) and the build flags: identifies the kernels a stored profile was
+    taken from."""
     import hashlib
     h = hashlib.sha256()
     h.update(" ".join(CFLAGS).replace(ROOT, "").encode())
     files = sorted(os.listdir(CSRC))
     for name in files:
         if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+            with open(os.path.join(CSRC, name)) as f:
+                h.update(name.encode() + b"\0" + _code_only(f.read()).encode())
     for name in ("lsgd.h", "lsgd_bench.h"):
-        with open(os.path.join(INCLUDE, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(INCLUDE, name)) as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 
