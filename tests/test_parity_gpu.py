@@ -839,3 +839,68 @@ def test_vector_longer_than_2_to_31_elements():
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
     del p, m, grads, rep
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------- tail sizes
+
+TAIL_SIZES = list(range(1, 68)) + [2 ** k + d for k in (7, 10, 11, 12, 13, 17) for d in (-1, 1)]
+
+
+@pytest.mark.parametrize("gdt,G,W,R,rdt", [("f32", 2, 2, 1, "f32"), ("bf16", 4, 4, 2, "bf16"), ("f32", 3, 5, 1, "f32")])
+def test_every_tail_size_flat(gdt, G, W, R, rdt):
+    """n = 1..67 and 2^k +- 1: every ragged end of the 4- and 8-element units,
+    flat step bit-exact against the oracle."""
+    rng = np.random.default_rng(67)
+    gow = groups_for(G, W, "shuffled", seed=2)
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    for n in TAIL_SIZES:
+        gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(G * W)]
+        p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+        ph, mh = p0.copy(), np.zeros(n, np.float32)
+        rr = [np.zeros(n, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+        oracle.lsgd_step(ph, mh, gh, gow, G, 0.1, 0.9, 1e-4, rr, oracle.BF16 if rdt == "bf16" else oracle.F32)
+        p, m = to_dev(p0), torch.zeros(n, device=DEV)
+        reps = [torch.empty(n, device=DEV, dtype=rtd) for _ in range(R)]
+        lsgd.step(p, m, [to_dev(g) for g in gh], gow, G, 0.1, 0.9, 1e-4, reps)
+        torch.cuda.synchronize()
+        assert_close(to_host(p), ph, "params n=%d" % n)
+        assert_close(to_host(m), mh, "momentum n=%d" % n)
+        for r in range(R):
+            assert np.array_equal(to_host(reps[r]), rr[r]), (n, r)
+
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+def test_every_tail_size_as_plan_tensors(gdt):
+    """The same sizes as the tensors of one plan (many small tensors share a
+    bucket): plain step, then a LARS step, each tensor bit-exact against the
+    oracle."""
+    rng = np.random.default_rng(68)
+    G, W = 2, 4
+    N = G * W
+    gow = groups_for(G, W, "shuffled", seed=4)
+    sizes = TAIL_SIZES
+    ph = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in sizes]
+    mh = [np.zeros(s, np.float32) for s in sizes]
+    params = [to_dev(x) for x in ph]
+    mom = [to_dev(x) for x in mh]
+    gh = [[rand_host(rng, s, 1e-2, gdt) for s in sizes] for _ in range(N)]
+    grads = [[to_dev(x) for x in row] for row in gh]
+    reps = [[torch.empty(s, device=DEV) for s in sizes]]
+    plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+    plan.step(0.1, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    for t, s in enumerate(sizes):
+        rr = [np.zeros(s, np.float32)]
+        oracle.lsgd_step(ph[t], mh[t], [gh[w][t] for w in range(N)], gow, G, 0.1, 0.9, 1e-4, rr)
+        assert_close(to_host(params[t]), ph[t], "plan params size %d" % s)
+        assert np.array_equal(to_host(reps[0][t]), rr[0]), s
+    trust = torch.empty(len(sizes), device=DEV)
+    plan.lars_step(0.1, 0.9, 1e-4, 1e-3, trust_out=trust)
+    torch.cuda.synchronize()
+    tg = to_host(trust)
+    for t, s in enumerate(sizes):
+        tr = oracle.lars_step(ph[t], mh[t], [gh[w][t] for w in range(N)], gow, G, 0.1, 0.9, 1e-4, 1e-3)
+        assert np.float32(tg[t]) == np.float32(tr), (s, tg[t], tr)
+        assert_close(to_host(params[t]), ph[t], "LARS params size %d" % s)
+        assert_close(to_host(mom[t]), mh[t], "LARS momentum size %d" % s)
+    plan.close()
