@@ -41,7 +41,10 @@
  *    launched and no output is touched. n == 0 is a no-op that returns LSGD_OK
  *    after the counts, dtypes and membership are validated (pointers may then
  *    be NULL).
- *  - Alignment. Every buffer must be 16-byte aligned (LSGD_ERR_ALIGN).
+ *  - Alignment. Every buffer must be 16-byte aligned (LSGD_ERR_ALIGN). For
+ *    bandwidth, give all buffers of a call the same offset modulo 2 MB (as
+ *    separate large allocations have): buffers packed back to back at
+ *    arbitrary offsets measured up to 13% slower on MI355X.
  *  - Aliasing. Written buffers may not overlap each other or any read buffer
  *    (LSGD_ERR_ALIAS). Read buffers may overlap each other (several workers may
  *    pass the same gradient buffer).
