@@ -58,6 +58,9 @@ def parse_args(argv=None):
     ap.add_argument("--trust-coef", type=float, default=1e-3, help="LARS trust coefficient")
     ap.add_argument("--lars-exclude-vectors", action="store_true",
                     help="LARS: one-dimensional tensors (batch norm, biases) take trust 1")
+    ap.add_argument("--tensor-layout", choices=("separate", "arena"), default="separate",
+                    help="multi-tensor workloads: every tensor its own allocation, or each worker's (and "
+                         "replica's, p's, m's) tensors as views into one allocation")
     ap.add_argument("--copy-out", choices=("auto", "fused", "separate"), default="auto",
                     help="replicas written inside the step kernel or by a copy-out pass of their own")
     ap.add_argument("--broadcast-grad", action="store_true",
@@ -77,7 +80,7 @@ class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
     def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3,
-                 lars_exclude=None):
+                 lars_exclude=None, tensor_layout="separate"):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
@@ -100,16 +103,29 @@ class Setup:
         scratch = torch.empty(wl.n, device=dev) if wl.grad_dtype == "bf16" else None
         if wl.tensor_sizes:
             sizes = wl.tensor_sizes
-            self.params = workloads.split_tensors(flat_p, sizes)
-            del flat_p
-            self.mom = [torch.zeros_like(x) for x in self.params]
             self.grads = []
-            tmp = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
-            for w in range(N):
-                workloads.fill_worker_grad(wl, 0, w, tmp, scratch)
-                self.grads.append(workloads.split_tensors(tmp, sizes))
-            del tmp
-            self.reps = [[torch.empty(s, device=dev, dtype=rtd) for s in sizes] for _ in range(R)]
+            if tensor_layout == "arena":   # one allocation per worker, tensors as views into it
+                self._arenas = [flat_p, torch.zeros_like(flat_p)]
+                self.params = workloads.view_tensors(flat_p, sizes)
+                self.mom = workloads.view_tensors(self._arenas[1], sizes)
+                for w in range(N):
+                    g = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
+                    workloads.fill_worker_grad(wl, 0, w, g, scratch)
+                    self._arenas.append(g)
+                    self.grads.append(workloads.view_tensors(g, sizes))
+                reps = [torch.empty(wl.n, device=dev, dtype=rtd) for _ in range(R)]
+                self._arenas += reps
+                self.reps = [workloads.view_tensors(x, sizes) for x in reps]
+            else:
+                self.params = workloads.split_tensors(flat_p, sizes)
+                del flat_p
+                self.mom = [torch.zeros_like(x) for x in self.params]
+                tmp = torch.empty(wl.n, device=dev, dtype=wl.torch_grad_dtype)
+                for w in range(N):
+                    workloads.fill_worker_grad(wl, 0, w, tmp, scratch)
+                    self.grads.append(workloads.split_tensors(tmp, sizes))
+                del tmp
+                self.reps = [[torch.empty(s, device=dev, dtype=rtd) for s in sizes] for _ in range(R)]
             self.plan = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps)
             h = self.plan._handle
             hyper = (ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd))
@@ -591,7 +607,8 @@ def main(argv=None):
         if wl.tensor_sizes != tuple(workloads.resnet50_param_sizes()):
             raise SystemExit("--lars-exclude-vectors knows the ResNet-50 tensor list only")
         lars_excl = workloads.resnet50_vector_params()
-    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl)
+    setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
+                  args.tensor_layout)
     ms = time_steps(setup, args.steps, args.warmup)
     alg = wl.algorithmic_bytes(R) + extra_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
@@ -606,6 +623,7 @@ def main(argv=None):
                    "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                    "replicas": R, "replica_dtype": wl.replica_dtype,
                    "tensors": len(wl.tensor_sizes) if wl.tensor_sizes else 1,
+                   **({"tensor_layout": args.tensor_layout} if wl.tensor_sizes else {}),
                    "reduction": setup.reduction, "broadcast_grad": setup.broadcast_grad,
                    **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {}),
                    **({"lars": True, "trust_coef": args.trust_coef,
@@ -626,7 +644,8 @@ def main(argv=None):
         setup.close()
         del setup
         torch.cuda.empty_cache()
-        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl)
+        setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
+                      args.tensor_layout)
         ms0 = time_steps(setup, args.steps, args.warmup)
         alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),

@@ -224,6 +224,15 @@ def split_tensors(flat: torch.Tensor, sizes) -> List[torch.Tensor]:
     return out
 
 
+def view_tensors(flat: torch.Tensor, sizes) -> List[torch.Tensor]:
+    """Consecutive pieces of `flat` as views (one allocation for all tensors)."""
+    out, off = [], 0
+    for s in sizes:
+        out.append(flat[off:off + s])
+        off += s
+    return out
+
+
 def sample_indices(n: int, count: int, seed: int) -> np.ndarray:
     """Sorted, unique element indices: the first and last 64 elements, the
     ragged end, and `count` seeded uniform draws."""
