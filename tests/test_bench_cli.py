@@ -1,0 +1,57 @@
+"""bench.py's host logic without a GPU: the one-GPU contract, and the counter
+arithmetic that turns rocprofv3 FETCH_SIZE / WRITE_SIZE rows into traffic."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import workloads  # noqa: E402
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def _write_rows(path, counter, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for d, (kernel, grid, value) in enumerate(rows):
+            w.writerow({"Dispatch_Id": d, "Kernel_Name": kernel, "Grid_Size": grid, "Counter_Name": counter,
+                        "Counter_Value": value})
+
+
+def test_derive_traffic_scales_by_the_calibration_copy(tmp_path, monkeypatch):
+    """Synthetic counter rows: the 1 GiB copy reads FETCH_SIZE = half its bytes
+    and WRITE_SIZE = all of them, so the step's rows are scaled by 2 and 1;
+    two dispatches of the step kernel average; the ceiling copy (a larger grid)
+    is ignored."""
+    wl = workloads.WORKLOADS["resnet50_flat"]
+    alg = wl.algorithmic_bytes(16)
+    read_b, write_b = wl.n * (16 * 4 + 8), wl.n * (8 + 16 * 4)
+    gib_kib = (1 << 30) / 1024
+    step = "void lsgd::step_flat_ct<float, 4, 4, 2>(lsgd::StepArgs)"
+    copy = "lsgd::stream_copy_kernel(unsigned int __vector(4)*)"
+    calib_grid = (1 << 28) // 4          # one lane per 16 bytes of the 1 GiB copy
+    fetch = [(copy, calib_grid, gib_kib / 2), (copy, calib_grid * 2, 999.0),
+             (step, 1, read_b / 1024 / 2), (step, 1, read_b / 1024 / 2)]
+    write = [(copy, calib_grid, gib_kib), (step, 1, write_b / 1024), (step, 1, write_b / 1024)]
+    fcsv, wcsv = tmp_path / "f.csv", tmp_path / "w.csv"
+    _write_rows(fcsv, "FETCH_SIZE", fetch)
+    _write_rows(wcsv, "WRITE_SIZE", write)
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    args = bench.parse_args(["--derive-traffic", "--workload", "resnet50_flat", "--fetch-csv", str(fcsv),
+                             "--write-csv", str(wcsv)])
+    bench.derive_traffic(args)
+    out = json.load(open(tmp_path / "traffic_resnet50_flat_R16.json"))
+    assert abs(out["fetch_scale"] - 2.0) < 1e-12 and abs(out["write_scale"] - 1.0) < 1e-12
+    assert abs(out["traffic_over_algorithmic"] - 1.0) < 1e-9
+    assert out["algorithmic_bytes"] == alg and out["dispatches"] == [2, 2]
