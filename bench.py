@@ -356,6 +356,48 @@ def cpu_baseline(setup, seconds):
                                                                           steps, el)}
 
 
+def cpu_baseline_unfused(setup, seconds):
+    """The oracle's three unfused steps (group means, global mean, update and
+    copy-out) on the first 2^20 elements, one host thread, scaled by the
+    unfused path's bytes per element."""
+    import numpy as np
+    import oracle
+
+    wl, R = setup.wl, setup.R
+    S = min(wl.n, 1 << 20)
+    host = lambda t: t[:S].detach().cpu()
+    grads = []
+    for g in setup.grads:
+        x = host(g[0])
+        grads.append(x.view(torch_int16()).numpy().view(np.uint16).copy() if wl.grad_dtype == "bf16" else x.numpy().copy())
+    p = host(setup.params[0]).numpy().copy()
+    m = host(setup.mom[0]).numpy().copy()
+    rdt = oracle.BF16 if wl.replica_dtype == "bf16" else oracle.F32
+    reps = [np.zeros(S, np.uint16 if rdt == oracle.BF16 else np.float32) for _ in range(R)]
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        means = oracle.group_means(grads, setup.gow, wl.groups)
+        gbar = oracle.global_mean(means)
+        oracle.sgd_step(p, m, gbar, wl.lr, wl.mu, wl.wd, reps, rdt)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    elem_per_s = S * steps / el
+    per_elem = sum(setup.bytes_per_call()) / wl.n
+    return {"value": round(elem_per_s * per_elem / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "steps_per_s": round(elem_per_s / wl.n, 6),
+            "sample": "first %d of %d elements, all %d worker gradients and %d replicas, %d oracle unfused "
+                      "steps (group means, global mean, update) in %.1f s on one host thread"
+                      % (S, wl.n, wl.n_workers, R, steps, el)}
+
+
+def torch_int16():
+    import torch
+    return torch.int16
+
+
 def _cpu_baseline_lars(setup, seconds, S):
     """The oracle's LARS step, tensor by tensor, over the leading tensors that
     hold about S elements (whole tensors: the trust ratio needs each one)."""
@@ -595,6 +637,14 @@ def main(argv=None):
             "fused_equivalent_bytes": wl.algorithmic_bytes(R),
             "copy_ceiling_GBps": round(ceiling, 1),
         }
+        # the dominant call (most time) against the HBM roofline, per launch
+        k = max(range(3), key=lambda i: per_call[i])
+        kb = nbytes[k] / (per_call[k] * 1e-3) / 1e9
+        result["roofline"] = {"bound": "hbm", "achieved": round(kb, 2), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                              "frac": round(kb / PEAK_HBM_GBPS, 4), "traffic": None,
+                              "algorithmic_bytes": nbytes[k], "kernel": names[k]}
+        if not args.no_cpu_baseline:
+            result["cpu_baseline"] = cpu_baseline_unfused(setup, args.cpu_seconds)
         print(json.dumps(result), flush=True)
         return
     def extra_bytes():
