@@ -168,6 +168,18 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
     return grad_bytes >= 256 || static_cast<int64_t>(n_replicas) * 4 > grad_bytes;
 }
 
+// The same choice for lsgd_sgd_step (reads 12 bytes per element, writes 8 plus
+// the replicas). Measured: the separate pass won once the replicas take 64
+// bytes per element or more (binary32 R = 16: +2%, R = 64: +4%; bfloat16
+// R = 64: +5%) and lost below (binary32 R = 1, 4: -13%, -10%; bfloat16 R = 16).
+bool separate_copy_out_update(int32_t n_replicas, size_t rsz) {
+    if (n_replicas <= 0) return false;
+    const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
+    if (mode == LSGD_COPY_OUT_FUSED) return false;
+    if (mode == LSGD_COPY_OUT_SEPARATE) return true;
+    return static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz) >= 64;
+}
+
 LaunchShape launch_shape(int64_t units, int tile) {
     const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);
     const int64_t span = static_cast<int64_t>(kBlock) * upl * (tile < 1 ? 1 : tile);

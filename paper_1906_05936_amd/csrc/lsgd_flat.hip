@@ -347,9 +347,13 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     const LaunchShape ls = launch_shape((n + 3) / 4, kSgdTile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
+    const bool split = separate_copy_out_update(n_replicas, dtype_size(rdt));
+    if (split) a.n_replicas = 0;
     hipLaunchKernelGGL(sgd_kernel<kSgdTile>, dim3(ls.blocks), dim3(kBlock), 0,
                        static_cast<hipStream_t>(stream), a);
-    return check_launch("lsgd_sgd_step");
+    if ((st = check_launch("lsgd_sgd_step")) != LSGD_OK || !split) return st;
+    a.n_replicas = n_replicas;
+    return launch_copy_out(a, stream);
 }
 
 namespace {

@@ -71,6 +71,8 @@ int32_t launch_passes_per_block();
 // Whether a step with N gradients of gsz bytes and R replicas of rsz bytes
 // writes its replicas in a copy-out pass of its own (lsgd_set_copy_out_mode).
 bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz);
+// The same for lsgd_sgd_step.
+bool separate_copy_out_update(int32_t n_replicas, size_t rsz);
 
 // Grid of exactly `blocks` logical workgroups, each covering `block_bytes` of
 // every buffer, padded for the XCD chunking (kernels skip logical blocks

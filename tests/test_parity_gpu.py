@@ -199,17 +199,22 @@ def test_unfused_calls_match_oracle_and_fused(G, W, gdt, n, R, rdt):
     p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
     m0 = (rng.standard_normal(n) * 0.01).astype(np.float32)
     rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
-    p, m = to_dev(p0), to_dev(m0)
-    reps = [torch.empty(n, device=DEV, dtype=rtd) for _ in range(R)]
-    lsgd.sgd_step(p, m, gbar, 0.1, 0.9, 1e-4, reps)
     p_ref, m_ref = p0.copy(), m0.copy()
     ref_reps = [np.zeros(n, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
     oracle.sgd_step(p_ref, m_ref, gbar_ref, 0.1, 0.9, 1e-4, ref_reps,
                     oracle.BF16 if rdt == "bf16" else oracle.F32)
-    assert_close(to_host(p), p_ref, "params")
-    assert_close(to_host(m), m_ref, "momentum")
-    for r in range(R):
-        assert np.array_equal(to_host(reps[r]), ref_reps[r])
+    try:   # replicas written by the update kernel, then by a copy-out pass of their own
+        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO):
+            lsgd.set_copy_out_mode(mode)
+            p, m = to_dev(p0), to_dev(m0)
+            reps = [torch.empty(n, device=DEV, dtype=rtd) for _ in range(R)]
+            lsgd.sgd_step(p, m, gbar, 0.1, 0.9, 1e-4, reps)
+            assert_close(to_host(p), p_ref, "params mode %d" % mode)
+            assert_close(to_host(m), m_ref, "momentum mode %d" % mode)
+            for r in range(R):
+                assert np.array_equal(to_host(reps[r]), ref_reps[r]), (mode, r)
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
 
     pf, mf = to_dev(p0), to_dev(m0)
     lsgd.step(pf, mf, grads, gow, G, 0.1, 0.9, 1e-4)
