@@ -54,7 +54,8 @@ FlatPick pick_flat(int W, int G) {
 // Runtime group layouts: accumulator levels for the largest count.
 template <typename GT>
 FlatPick pick_flat_seg(int max_count) {
-    return FlatPick{seg_levels(max_count) == 5 ? step_flat_seg<GT, 5> : step_flat_seg<GT, 8>, 1};
+    constexpr int U = SegTileUnits<GT>::U;
+    return FlatPick{seg_levels(max_count) == 5 ? step_flat_seg<GT, 5, U> : step_flat_seg<GT, 8, U>, U};
 }
 
 using MeanKernel = void (*)(MeanArgs);

@@ -368,41 +368,50 @@ __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x
 // Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
 
-// Member gradients a lane holds in one register batch of the segmented sum.
+// Member gradient loads a lane holds in one register batch of the segmented sum.
 constexpr int kSegBatch = 8;
 
-// Pairwise sums of consecutive runs of the N member-ordered gradient units of
-// one lane, for group layouts known only at run time: group j holds members
-// [gs(j), gs(j+1)), j < G, and done(j, sum) receives PW over them. Loads run
-// ahead of the additions in two alternating register batches of kSegBatch
-// members that ignore group boundaries, so a lane keeps between one and two
+// Pairwise sums of consecutive runs of the N member-ordered gradients of one
+// lane tile (U units, stream-major), for group layouts known only at run time:
+// group j holds members [gs(j), gs(j+1)), j < G, and done(j, sum) receives PW
+// over them for every element of the tile. Loads run ahead of the additions
+// in two alternating register batches of kSegBatch loads (kSegBatch / U
+// members) that ignore group boundaries, so a lane keeps between one and two
 // batches of 128-bit loads in flight whatever the group sizes. Each group is
 // folded through a binary-counter accumulator (LV levels: sizes below 2^LV).
 // N, G and gs are uniform, so every branch here is uniform.
-template <typename GT, int LV, bool TAIL, typename Ptr, typename Start, typename Done>
-__device__ __forceinline__ void pw_segments(int N, int G, const Ptr& ptr, const Start& gs, int64_t e0,
+template <typename GT, int LV, int U, bool TAIL, typename Ptr, typename Start, typename Done>
+__device__ __forceinline__ void pw_segments(int N, int G, const Ptr& ptr, const Start& gs, const int64_t (&e0)[U],
                                             int cnt, const Done& done) {
     constexpr int VEC = Unit<GT>::VEC;
-    constexpr int B = kSegBatch;
-    u32x4 xa[B], xb[B];
-    PwAcc<VEC, LV> acc;
+    constexpr int T = U * VEC;
+    constexpr int B = kSegBatch / U;
+    static_assert(B >= 1 && B * U == kSegBatch, "the batch holds whole members");
+    u32x4 xa[B][U], xb[B][U];
+    PwAcc<T, LV> acc;
     int j = 0;
     int gend = gs(1);
     int lv = acc_levels(gend - gs(0));
-    auto fetch = [&](int k0, u32x4 (&x)[B]) {
-#pragma unroll
-        for (int q = 0; q < B; ++q)
-            if (k0 + q < N) x[q] = load_raw<GT, TAIL>(ptr(k0 + q), e0, cnt);
-    };
-    auto consume = [&](int k0, const u32x4 (&x)[B]) {
+    auto fetch = [&](int k0, u32x4 (&x)[B][U]) {
 #pragma unroll
         for (int q = 0; q < B; ++q) {
             if (k0 + q < N) {
-                float v[VEC];
-                widen<GT>(x[q], v);
+                const void* g = ptr(k0 + q);
+#pragma unroll
+                for (int u = 0; u < U; ++u) x[q][u] = load_raw<GT, TAIL>(g, e0[u], cnt);
+            }
+        }
+    };
+    auto consume = [&](int k0, const u32x4 (&x)[B][U]) {
+#pragma unroll
+        for (int q = 0; q < B; ++q) {
+            if (k0 + q < N) {
+                float v[T];
+#pragma unroll
+                for (int u = 0; u < U; ++u) widen<GT>(x[q][u], slice<VEC, T>(v, u));
                 acc.push(v, lv);
                 if (k0 + q + 1 == gend) {
-                    float sum[VEC];
+                    float sum[T];
                     acc.result(sum, lv);
                     acc.count = 0;
                     done(j, sum);
@@ -494,6 +503,14 @@ struct MeanArgs {
 template <typename GT> struct TileUnits;
 template <> struct TileUnits<float> { static constexpr int U = 2; };
 template <> struct TileUnits<uint16_t> { static constexpr int U = 1; };
+
+// Units per lane tile in the flat runtime-layout (segmented) kernel
+// (measured: two binary32 units per lane, stream-major, +2-5% over one on
+// 3x5, 4x6, 2x64 and 32x4 groupings, -1% on the literal 4x4 step; bf16 stays
+// at one unit for registers).
+template <typename GT> struct SegTileUnits;
+template <> struct SegTileUnits<float> { static constexpr int U = 2; };
+template <> struct SegTileUnits<uint16_t> { static constexpr int U = 1; };
 
 // Widened gradient values one lane may hold at once: up to kUnrollFloats the
 // whole two-level tree is unrolled with every load issued up front (32 fp32
@@ -639,45 +656,61 @@ __device__ __forceinline__ void fused_unit_ct(const Src& s, int64_t e0, int cnt)
     fused_tile_ct<GT, W, G, 1, TAIL>(s, e, cnt);
 }
 
-// The mean gradient of one unit for group layouts known only at run time.
-// Group j is members [gs(j), gs(j+1)) of the member-ordered gradients. Mean of
-// means (literal = false, equal groups of W): each group's PW sum / W, PW over
-// the G results, / G. Paper-literal (any partition): each group's PW sum / N,
-// PW over the G results, no further division.
-template <typename GT, int LV, bool TAIL, typename Src, typename Start>
-__device__ __forceinline__ void mean_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
-                                              int64_t e0, int cnt, float (&gbar)[Unit<GT>::VEC]) {
-    constexpr int VEC = Unit<GT>::VEC;
+// The mean gradient of a lane tile (U units) for group layouts known only at
+// run time. Group j is members [gs(j), gs(j+1)) of the member-ordered
+// gradients. Mean of means (literal = false, equal groups of W): each group's
+// PW sum / W, PW over the G results, / G. Paper-literal (any partition): each
+// group's PW sum / N, PW over the G results, no further division.
+template <typename GT, int LV, int U, bool TAIL, typename Src, typename Start>
+__device__ __forceinline__ void mean_tile_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                              const int64_t (&e0)[U], int cnt,
+                                              float (&gbar)[U * Unit<GT>::VEC]) {
+    constexpr int T = U * Unit<GT>::VEC;
     const float dg = static_cast<float>(literal ? N : gs(1) - gs(0));
-    PwAcc<VEC, LV> groups;
+    PwAcc<T, LV> groups;
     const int glevels = acc_levels(G);
-    pw_segments<GT, LV, TAIL>(N, G, [&](int k) { return s.grad(k); }, gs, e0, cnt,
-                              [&](int, float (&sum)[VEC]) {
+    pw_segments<GT, LV, U, TAIL>(N, G, [&](int k) { return s.grad(k); }, gs, e0, cnt,
+                                 [&](int, float (&sum)[T]) {
 #pragma unroll
-                                  for (int v = 0; v < VEC; ++v) sum[v] = sum[v] / dg;
-                                  groups.push(sum, glevels);
-                              });
+                                     for (int v = 0; v < T; ++v) sum[v] = sum[v] / dg;
+                                     groups.push(sum, glevels);
+                                 });
     groups.result(gbar, glevels);
     if (!literal) {
         const float gf = static_cast<float>(G);
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) gbar[v] = gbar[v] / gf;
+        for (int v = 0; v < T; ++v) gbar[v] = gbar[v] / gf;
     }
 }
 
-// Fused step on one unit for runtime group layouts. Parameters and momentum
-// are loaded first so that their latency overlaps the gradient stream.
+template <typename GT, int LV, bool TAIL, typename Src, typename Start>
+__device__ __forceinline__ void mean_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                              int64_t e0, int cnt, float (&gbar)[Unit<GT>::VEC]) {
+    const int64_t e[1] = {e0};
+    mean_tile_seg<GT, LV, 1, TAIL>(s, N, G, gs, literal, e, cnt, gbar);
+}
+
+// Fused step on a lane tile for runtime group layouts. Parameters and
+// momentum are loaded first so that their latency overlaps the gradient
+// stream.
+template <typename GT, int LV, int U, bool TAIL, typename Src, typename Start>
+__device__ __forceinline__ void fused_tile_seg(const Src& s, int N, int G, const Start& gs, bool literal,
+                                               const int64_t (&e0)[U], int cnt) {
+    constexpr int VEC = Unit<GT>::VEC;
+    constexpr int T = U * VEC;
+    float p[T], m[T];
+    load_state<VEC, U, TAIL>(s, e0, cnt, p, m);
+    float gbar[T];
+    mean_tile_seg<GT, LV, U, TAIL>(s, N, G, gs, literal, e0, cnt, gbar);
+    broadcast_mean<GT, U, TAIL>(s, e0, cnt, gbar);
+    update_and_store<VEC, U, TAIL>(s, e0, cnt, gbar, p, m);
+}
+
 template <typename GT, int LV, bool TAIL, typename Src, typename Start>
 __device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const Start& gs, bool literal,
                                                int64_t e0, int cnt) {
-    constexpr int VEC = Unit<GT>::VEC;
     const int64_t e[1] = {e0};
-    float p[VEC], m[VEC];
-    load_state<VEC, 1, TAIL>(s, e, cnt, p, m);
-    float gbar[VEC];
-    mean_unit_seg<GT, LV, TAIL>(s, N, G, gs, literal, e0, cnt, gbar);
-    broadcast_mean<GT, 1, TAIL>(s, e, cnt, gbar);
-    update_and_store<VEC, 1, TAIL>(s, e, cnt, gbar, p, m);
+    fused_tile_seg<GT, LV, 1, TAIL>(s, N, G, gs, literal, e, cnt);
 }
 
 // Pointer source for the planless fused step: everything from StepArgs.
@@ -719,7 +752,7 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
 // Runtime group layouts (non-power-of-two or large counts, and the
 // paper-literal reduction): group j is members [group_start[j],
 // group_start[j+1]) of the member-ordered pointer table.
-template <typename GT, int LV>
+template <typename GT, int LV, int U>
 __global__ __launch_bounds__(kBlock) void step_flat_seg(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
@@ -727,10 +760,13 @@ __global__ __launch_bounds__(kBlock) void step_flat_seg(StepArgs a) {
     const int rem = static_cast<int>(a.n - full * VEC);
     const bool literal = a.literal != 0;
     auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
-    for_units(full + (rem != 0), a.xcd_chunk, a.upl, [&](int64_t u) {
-        if (u < full) fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, VEC);
-        else fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, rem);
-    });
+    for_tiles<U, VEC>(
+        full, full + (rem != 0), a.xcd_chunk, a.upl,
+        [&](const int64_t (&e0)[U]) { fused_tile_seg<GT, LV, U, false>(s, a.n_workers, a.n_groups, gs, literal, e0, VEC); },
+        [&](int64_t u) {
+            if (u < full) fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, VEC);
+            else fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, literal, u * VEC, rem);
+        });
 }
 
 // lsgd_group_mean, compile-time W (a power of two): every group's mean of its
@@ -774,8 +810,9 @@ __device__ __forceinline__ void group_mean_unit(const MeanArgs& a, int64_t e0, i
     constexpr int VEC = Unit<GT>::VEC;
     const int W = a.W;
     const float wf = static_cast<float>(W);
-    pw_segments<GT, LV, TAIL>(a.n_workers, a.n_groups, [&](int k) { return a.in[k]; },
-                              [&](int j) { return j * W; }, e0, cnt, [&](int j, float (&sum)[VEC]) {
+    const int64_t e[1] = {e0};
+    pw_segments<GT, LV, 1, TAIL>(a.n_workers, a.n_groups, [&](int k) { return a.in[k]; },
+                                 [&](int j) { return j * W; }, e, cnt, [&](int j, float (&sum)[VEC]) {
 #pragma unroll
                                   for (int v = 0; v < VEC; ++v) sum[v] = sum[v] / wf;
                                   store_f32<VEC, TAIL>(a.out[j], e0, cnt, sum);
@@ -829,8 +866,9 @@ template <int LV, bool TAIL>
 __device__ __forceinline__ void global_mean_unit(const MeanArgs& a, int64_t e0, int cnt) {
     const int G = a.n_groups;
     const float gf = static_cast<float>(G);
-    pw_segments<float, LV, TAIL>(G, 1, [&](int j) { return a.in[j]; }, [&](int j) { return j * G; },
-                                 e0, cnt, [&](int, float (&sum)[4]) {
+    const int64_t e[1] = {e0};
+    pw_segments<float, LV, 1, TAIL>(G, 1, [&](int j) { return a.in[j]; }, [&](int j) { return j * G; },
+                                    e, cnt, [&](int, float (&sum)[4]) {
 #pragma unroll
                                      for (int v = 0; v < 4; ++v) sum[v] = sum[v] / gf;
                                      store_f32<4, TAIL>(a.out[0], e0, cnt, sum);
