@@ -3,10 +3,9 @@
 //
 // lsgd_plan_create cuts every tensor into pieces of P workgroup tile passes
 // (256 lanes x the kernel's lane tile: 2048 elements for binary32 and bf16
-// gradients alike with the compile-time kernels, 1024 (binary32) or 2048
-// (bf16) with the runtime-layout kernel, times P = the launch shape's passes
-// per workgroup at plan creation, 1 by default), starting on unit boundaries, then packs consecutive pieces
-// into buckets of at most one piece: a large tensor yields one bucket per piece
+// gradients alike, times P = the launch shape's passes per workgroup at plan
+// creation, 1 by default), starting on unit boundaries, then packs consecutive
+// pieces into buckets of at most one piece: a large tensor yields one bucket per piece
 // (so it is walked exactly like the flat kernel walks a vector), while runs of
 // small tensors (ResNet-50's 64..1024-element batch-norm and bias vectors)
 // share a bucket. One workgroup runs one bucket; buckets are taken in the
@@ -87,7 +86,8 @@ PlanPick pick_plan(int W, int G) {
         case 16: k = pick_plan_g<GT, 16>(G); break;
     }
     if (k) return PlanPick{k, TileUnits<GT>::U};
-    return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>, 1};
+    return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>,
+                    SegTileUnits<GT>::U};
 }
 
 lsgd_status check_device(const lsgd_plan* plan) {

@@ -97,12 +97,22 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
 template <typename GT, int LV>
 __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
+    constexpr int U = SegTileUnits<GT>::U;
     const bool literal = a.literal != 0;
     auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
     for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
-        for (int64_t u = threadIdx.x; u < full; u += kBlock)
-            fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, ch.start + u * VEC, VEC);
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
+                int64_t e0[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
+                fused_tile_seg<GT, LV, U, false>(s, a.n_workers, a.n_groups, gs, literal, e0, VEC);
+            } else {
+                for (int64_t u = t0; u < full; u += kBlock)
+                    fused_unit_seg<GT, LV, false>(s, a.n_workers, a.n_groups, gs, literal, ch.start + u * VEC, VEC);
+            }
+        }
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0)
             fused_unit_seg<GT, LV, true>(s, a.n_workers, a.n_groups, gs, literal, ch.start + full * VEC, rem);
