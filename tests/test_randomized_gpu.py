@@ -1,0 +1,149 @@
+"""Seeded randomized parity over the option space of the library: partition
+(equal or unequal groups), reduction, gradient broadcast, gradient and
+replica dtypes, replica count, copy-out mode, flat vector or plan (a random
+split into tensors), and the LARS step where it applies. Every case is
+checked against the oracle bit for bit; each draw is logged before it runs."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.device_count() > 0:
+    import paper_1906_05936_amd as lsgd
+else:  # collected but skipped on machines without a GPU
+    lsgd = None
+
+DEV = torch.device("cuda:0")
+N_CASES = 48
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def to_host(t):
+    t = t.detach()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def draw(k):
+    rng = np.random.default_rng(workloads.stream_seed(77, k))
+    equal = rng.random() < 0.6
+    if equal:
+        G = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+        W = int(rng.choice([1, 2, 3, 4, 6, 8]))
+        while G * W > 128:
+            W = max(1, W // 2)
+        gow = workloads.shuffled_groups(G, W, int(rng.integers(1 << 30)))
+    else:
+        G = int(rng.integers(2, 7))
+        N = int(rng.integers(G, 40))
+        gow = list(range(G)) + [int(x) for x in rng.integers(0, G, size=N - G)]
+        rng.shuffle(gow)
+    gdt = "bf16" if rng.random() < 0.35 else "f32"
+    rdt = "bf16" if rng.random() < 0.3 else "f32"
+    R = int(rng.choice([0, 1, 2, 5, 17, 40]))
+    literal = (not equal) or rng.random() < 0.25
+    bcast = gdt == "f32" and rng.random() < 0.25
+    plan = rng.random() < 0.45
+    n = int(rng.integers(1, 120_000))
+    mode = int(rng.choice([-1, 0, 1]))
+    lars = plan and equal and not literal and not bcast and rng.random() < 0.5
+    cuts = sorted(set(int(x) for x in rng.integers(0, n, size=int(rng.integers(0, 6))))) if plan else []
+    sizes = [b - a for a, b in zip([0] + cuts, cuts + [n])]
+    return dict(gow=gow, G=G, gdt=gdt, rdt=rdt, R=R, literal=literal, bcast=bcast, plan=plan, n=n, mode=mode,
+                lars=lars, sizes=sizes, seed=k)
+
+
+def rand_host(rng, n, std, dtype):
+    x = (rng.standard_normal(n) * std).astype(np.float32)
+    return oracle.f32_to_bf16(x) if dtype == "bf16" else x
+
+
+@pytest.mark.parametrize("k", range(N_CASES))
+def test_random_case_matches_oracle(k):
+    c = draw(k)
+    log("case %d: %s" % (k, {x: c[x] for x in c if x != "gow"}) + " N=%d" % len(c["gow"]))
+    rng = np.random.default_rng(1000 + k)
+    N, G, n = len(c["gow"]), c["G"], c["n"]
+    sizes = c["sizes"]
+    offs = np.cumsum([0] + sizes)
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    gh = [rand_host(rng, n, 1e-2, c["gdt"]) for _ in range(N)]
+    rtd = torch.bfloat16 if c["rdt"] == "bf16" else torch.float32
+    rr = [np.zeros(n, np.uint16 if c["rdt"] == "bf16" else np.float32) for _ in range(c["R"])]
+    ph, mh = p0.copy(), np.zeros(n, np.float32)
+    ghc = [g.copy() for g in gh]
+    rdt_o = oracle.BF16 if c["rdt"] == "bf16" else oracle.F32
+    trusts = []
+    if c["lars"]:
+        for t in range(len(sizes)):
+            sl = slice(offs[t], offs[t + 1])
+            rt = [np.zeros(sizes[t], rr[0].dtype) for _ in range(c["R"])]
+            p_t, m_t = ph[sl].copy(), mh[sl].copy()
+            trusts.append(oracle.lars_step(p_t, m_t, [g[sl] for g in gh], c["gow"], G, 0.1, 0.9, 1e-4, 1e-3, rt, rdt_o))
+            ph[sl], mh[sl] = p_t, m_t
+            for r in range(c["R"]):
+                rr[r][sl] = rt[r]
+    elif c["literal"] or c["bcast"]:
+        oracle.lsgd_step_literal(ph, mh, ghc, c["gow"], G, 0.1, 0.9, 1e-4, rr, rdt_o, broadcast_grad=c["bcast"])
+    else:
+        oracle.lsgd_step(ph, mh, gh, c["gow"], G, 0.1, 0.9, 1e-4, rr, rdt_o)
+    # with the broadcast, mean of means and literal give the same bits only for power-of-two
+    # groups; such draws use the literal reduction on the GPU too
+    reduction = "literal" if (c["literal"] or c["bcast"]) else "mean_of_means"
+    try:
+        lsgd.set_copy_out_mode(c["mode"])
+        if c["plan"]:
+            params = [to_dev(p0[offs[t]:offs[t + 1]].copy()) for t in range(len(sizes))]
+            mom = [torch.zeros(s, device=DEV) for s in sizes]
+            grads = [[to_dev(g[offs[t]:offs[t + 1]].copy()) for t in range(len(sizes))] for g in gh]
+            reps = [[torch.empty(s, device=DEV, dtype=rtd) for s in sizes] for _ in range(c["R"])]
+            plan = lsgd.Plan(params, mom, grads, c["gow"], G, reps)
+            if c["lars"]:
+                tr = torch.empty(len(sizes), device=DEV)
+                plan.lars_step(0.1, 0.9, 1e-4, 1e-3, trust_out=tr)
+            else:
+                plan.step(0.1, 0.9, 1e-4, reduction=reduction, broadcast_grad=c["bcast"])
+            torch.cuda.synchronize()
+            pg = np.concatenate([to_host(x) for x in params]) if n else np.zeros(0, np.float32)
+            mg = np.concatenate([to_host(x) for x in mom])
+            rg = [np.concatenate([to_host(x) for x in row]) for row in reps]
+            gg = [np.concatenate([to_host(x) for x in row]) for row in grads]
+            if c["lars"]:
+                tg = to_host(tr)
+                assert all(np.float32(a) == np.float32(b) for a, b in zip(tg, trusts)), (tg, trusts)
+            plan.close()
+        else:
+            p, m = to_dev(p0), torch.zeros(n, device=DEV)
+            grads = [to_dev(g) for g in gh]
+            reps = [torch.empty(n, device=DEV, dtype=rtd) for _ in range(c["R"])]
+            lsgd.step(p, m, grads, c["gow"], G, 0.1, 0.9, 1e-4, reps, reduction=reduction, broadcast_grad=c["bcast"])
+            torch.cuda.synchronize()
+            pg, mg = to_host(p), to_host(m)
+            rg = [to_host(x) for x in reps]
+            gg = [to_host(x) for x in grads]
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+    assert np.array_equal(pg.view(np.uint32), ph.view(np.uint32)), "params differ"
+    assert np.array_equal(mg.view(np.uint32), mh.view(np.uint32)), "momentum differs"
+    for r in range(c["R"]):
+        assert np.array_equal(rg[r], rr[r]), "replica %d differs" % r
+    if c["bcast"]:
+        for w in range(N):
+            assert np.array_equal(gg[w], ghc[w]), "broadcast gradient %d differs" % w
