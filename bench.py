@@ -482,8 +482,8 @@ def separate_copy_out(wl, R, mode="auto"):
         return False
     if mode == "separate":
         return True
-    gb = wl.n_workers * wl.grad_bytes
-    return wl.replica_dtype == "f32" and (gb >= 256 or R * 4 > gb)
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    return R * rb >= 32 or wl.n_workers * wl.grad_bytes >= 256
 
 
 def kernel_match(wl, reduction=None, lars=False):
@@ -535,17 +535,30 @@ def derive_traffic(args):
     print(json.dumps(out))
 
 
-def lars_kernel_bytes(wl, R):
-    """Algorithmic bytes of the three LARS kernels (per launch): the norms pass
-    reads the N gradients and p and writes the mean gradient; the trust pass
-    reads two binary64 partials per chunk (2048-element pieces) and writes one
-    float per tensor; the update reads the mean gradient, p and m and writes p,
-    m and the R replicas."""
+def lars_separate_copy_out(wl, R, mode="auto"):
+    """The library's copy-out rule for the LARS update (that of lsgd_sgd_step),
+    for labels and per-kernel accounting."""
+    if R == 0 or mode == "fused":
+        return False
+    return mode == "separate" or (wl.replica_dtype == "f32" and R >= 4)
+
+
+def lars_kernel_bytes(wl, R, mode="auto"):
+    """Algorithmic bytes of the LARS kernels (per launch): the norms pass reads
+    the N gradients and p and writes the mean gradient; the trust pass reads
+    two binary64 partials per chunk (2048-element pieces) and writes one float
+    per tensor; the update reads the mean gradient, p and m and writes p, m and
+    the R replicas, or, with a copy-out pass, p and m only, and the copy-out
+    pass reads p and writes the replicas."""
     rb = 2 if wl.replica_dtype == "bf16" else 4
     chunks = sum((s + 2047) // 2048 for s in wl.tensor_sizes)
-    return {"lars_norms": wl.n * (wl.n_workers * wl.grad_bytes + 8),
-            "lars_trust": chunks * 16 + len(wl.tensor_sizes) * 4,
-            "lars_update": wl.n * (4 + 16 + R * rb)}
+    out = {"lars_norms": wl.n * (wl.n_workers * wl.grad_bytes + 8),
+           "lars_trust": chunks * 16 + len(wl.tensor_sizes) * 4,
+           "lars_update": wl.n * (4 + 16 + R * rb)}
+    if lars_separate_copy_out(wl, R, mode):
+        out["lars_update"] = wl.n * 20
+        out["copy_out"] = wl.n * (4 + R * rb)
+    return out
 
 
 def _derive_traffic_lars(args, wl, R, fetch_rows, write_rows):
@@ -554,9 +567,9 @@ def _derive_traffic_lars(args, wl, R, fetch_rows, write_rows):
     w_c, _ = _calib_kib(write_rows, "WRITE_SIZE")
     known = CALIB_ELEMS * 4 / 1024.0
     f_scale, w_scale = known / f_c, known / w_c
-    alg = lars_kernel_bytes(wl, R)
+    alg = lars_kernel_bytes(wl, R, args.copy_out)
     per = {}
-    for kname in ("lars_norms", "lars_trust", "lars_update"):
+    for kname in alg:
         f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
         w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
         rb, wb = f_k * f_scale * 1024, w_k * w_scale * 1024
@@ -678,16 +691,18 @@ def main(argv=None):
                    **({"group_sizes": list(wl.group_sizes)} if wl.group_sizes else {}),
                    **({"lars": True, "trust_coef": args.trust_coef,
                        "lars_excluded_tensors": sum(lars_excl) if lars_excl else 0} if args.lars else {}),
-                   "copy_out": ("separate pass" if separate_copy_out(wl, R, args.copy_out) and not args.lars
+                   "copy_out": ("separate pass" if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
+                                                     else separate_copy_out(wl, R, args.copy_out))
                                 else "in the step kernel")},
         "steps_per_s": round(1e3 / ms, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": alg,
                      "kernel": kernel_match(wl, setup.reduction, args.lars)
-                               + (" + lars_trust_kernel + lars_update_kernel (whole step)" if args.lars else "")
-                               + (" + copy_out (whole step)" if not args.lars and separate_copy_out(wl, R, args.copy_out)
-                                  else "")},
+                               + (" + lars_trust_kernel + lars_update_kernel" if args.lars else "")
+                               + (" + copy_out" if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
+                                                    else separate_copy_out(wl, R, args.copy_out)) else "")
+                               + (" (whole step)" if args.lars or separate_copy_out(wl, R, args.copy_out) else "")},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if R != 0 and not args.no_r0:

@@ -129,14 +129,14 @@ LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_p
 /* Where the steps (lsgd_step, lsgd_step_ex, lsgd_step_plan*, lsgd_sgd_step)
  * write their replicas (the copy-out, Alg. 3 broadcast step): inside the step
  * kernel, or in a copy-out pass of their own launched right after it on the
- * same stream, which reads the new parameters once more (4 bytes per element)
- * and writes every replica. Results are identical either way.
- * LSGD_COPY_OUT_AUTO (the default) takes the separate pass where it measured
- * faster: for the fused steps with binary32 replicas when the gradient bytes
- * N*s_g per element are at least 256 or the replica bytes 4R exceed them
- * (bfloat16 replicas stay in the step kernel); for lsgd_sgd_step when the
- * replica bytes R*s_r per element are at least 64. Process-wide, for launches after the call returns. Errors:
- * LSGD_ERR_SIZE (unknown mode). A tuning and measurement knob. */
+ * same stream, which reads the new parameters once more (4 bytes per element,
+ * mostly from cache) and writes the replicas one window of the vector at a
+ * time. Results are identical either way. LSGD_COPY_OUT_AUTO (the default)
+ * takes the separate pass where it measured faster: for the fused steps when
+ * the replica bytes R*s_r per element are at least 32 or the gradient bytes
+ * N*s_g at least 256; for lsgd_sgd_step with binary32 replicas and R >= 4.
+ * Process-wide, for launches after the call returns. Errors: LSGD_ERR_SIZE
+ * (unknown mode). A tuning and measurement knob. */
 #define LSGD_COPY_OUT_AUTO (-1)
 #define LSGD_COPY_OUT_FUSED 0
 #define LSGD_COPY_OUT_SEPARATE 1

@@ -134,15 +134,15 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
     int64_t need = blocks < 1 ? 1 : blocks;
     int64_t chunk = g_xcd_chunk.load(std::memory_order_relaxed);
     if (chunk == kXcdChunkAuto) chunk = std::max<int64_t>(1, kAutoChunkBytes / block_bytes);
-    if (chunk > 0 && need >= 8 * chunk && need <= 0x7fffffff - 8 * chunk) {
-        const int64_t group = 8 * chunk;
+    const int64_t group = 8 * std::max<int64_t>(chunk, 1);
+    if (chunk > 0 && need >= group && (need + group - 1) / group * group <= kMaxGridBlocks) {
         need = (need + group - 1) / group * group;
     } else {
         chunk = 0;
     }
     // The kernels grid-stride, so a capped grid still covers the work (the
     // renumbering is off in that case, so it stays a bijection).
-    if (need > 0x7fffffff) need = 0x7fffffff;
+    if (need > kMaxGridBlocks) need = kMaxGridBlocks;
     ls.blocks = static_cast<unsigned>(need);
     ls.xcd_chunk = static_cast<uint32_t>(chunk);
     ls.upl = 1;
@@ -152,32 +152,41 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
 int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_order_relaxed); }
 
 // Automatic rule, from same-process measurements of the fused pass against
-// step-then-copy-out over R = 8..128. Binary32 replicas: with 128 binary32
-// gradients (512 gradient bytes per element) the separate pass won at every R
-// (by 8-11%); with 16 (64 bytes) it won once the replica writes exceeded the
-// gradient reads (R = 32: +1-5%, R = 64: +5-8%, R = 128: +10%) and lost by
-// 2-4% below. bfloat16 replicas (64 bfloat16 gradients, R = 16, 64, 128):
-// the fused pass won every time (by 2-5%), so they always stay in it.
+// step-then-copy-out (the replica-major pass) at N = 16, 64, 128 gradients
+// and R = 1..128 replicas, flat steps and plans, binary32 and bfloat16. The
+// separate pass won once the replicas take 32 bytes per element or more
+// (R = 16 with 16 gradients: +7-9%; R = 64: +18-20%; 64 bfloat16 gradients:
+// even) or the gradients 256 bytes (128 binary32 gradients, R = 2: +6%,
+// R = 128: +20%), and was within 3% either way below that.
 bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz) {
     if (n_replicas <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
-    if (rsz != 4) return false;
     const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
-    return grad_bytes >= 256 || static_cast<int64_t>(n_replicas) * 4 > grad_bytes;
+    return static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz) >= 32 || grad_bytes >= 256;
+}
+
+// 8 MB of p per window: 1 MB in each of the eight XCD L2 caches (4 MB each),
+// re-read there for every replica. Windows of 4-20 MB measured alike; from
+// 24 MB the window no longer stays in L2 and the pass slows by a third.
+constexpr int64_t kCopyWindowBytes = 8 << 20;
+
+int64_t copy_window_blocks(int64_t block_p_bytes) {
+    const int64_t blocks = kCopyWindowBytes / block_p_bytes;
+    return std::max<int64_t>(8, blocks / 8 * 8);
 }
 
 // The same choice for lsgd_sgd_step (reads 12 bytes per element, writes 8 plus
-// the replicas). Measured: the separate pass won once the replicas take 64
-// bytes per element or more (binary32 R = 16: +2%, R = 64: +4%; bfloat16
-// R = 64: +5%) and lost below (binary32 R = 1, 4: -13%, -10%; bfloat16 R = 16).
+// the replicas). Measured: with binary32 replicas the separate pass won from
+// R = 4 (+2%; R = 8: +4%, R = 16: +15%, R = 64: +10%) and lost below (R = 1:
+// -11%); with bfloat16 replicas the fused pass won or tied at every R up to 64.
 bool separate_copy_out_update(int32_t n_replicas, size_t rsz) {
     if (n_replicas <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
-    return static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz) >= 64;
+    return rsz == 4 && n_replicas >= 4;
 }
 
 LaunchShape launch_shape(int64_t units, int tile) {

@@ -74,6 +74,11 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
 // The same for lsgd_sgd_step.
 bool separate_copy_out_update(int32_t n_replicas, size_t rsz);
 
+// Workgroups per window of the replica-major copy-out pass whose workgroups
+// each read `block_p_bytes` of p: a multiple of 8, so that each XCD reads the
+// same part of the window for every replica.
+int64_t copy_window_blocks(int64_t block_p_bytes);
+
 // Grid of exactly `blocks` logical workgroups, each covering `block_bytes` of
 // every buffer, padded for the XCD chunking (kernels skip logical blocks
 // >= `blocks`).

@@ -26,6 +26,9 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kMaxWorkers = 128;   // == LSGD_MAX_WORKERS
 constexpr int kMaxReplicas = 128;  // == LSGD_MAX_REPLICAS
 constexpr int kBlock = 256;        // threads per workgroup (4 wave64)
+// A dispatch holds at most 2^32 - 1 work-items; grids stay at or below this
+// many workgroups (a multiple of 8, the XCD count).
+constexpr int64_t kMaxGridBlocks = (0xffffffffLL / kBlock) / 8 * 8;
 
 enum : int { kF32 = 0, kBF16 = 1 };
 
@@ -474,6 +477,8 @@ struct StepArgs {
     const float* lr_ptr;   // non-null: the learning rate is read here when the kernel runs
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
     int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
+    int32_t win_blocks;    // replica-major copy-out: workgroups per window and replica group (a multiple of 8)
+    int64_t block0;        // replica-major copy-out: workgroup number of this launch's first workgroup
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
     const void* grads[kMaxWorkers];
     void* replicas[kMaxReplicas];
@@ -927,40 +932,51 @@ __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
 
 // ------------------------------------------------------------- copy-out pass
 //
-// With many replicas the copy-out runs as a pass of its own after the step
-// kernel (which then writes no replica): a lane reads a tile of the new p once
-// and writes it to every replica. Measured: one read-heavy pass plus one
-// write-only pass beat the single mixed pass once the replica writes outweigh
-// the gradient reads, or when N is large (host rule in lsgd_common.hip).
-// Binary32 replicas use two 4-element units per lane; bfloat16 replicas one
-// 8-element unit, so that every store is 16 bytes.
-template <int VEC, int U, bool TAIL, typename Rep>
-__device__ __forceinline__ void copy_out_tile(const float* p, const Rep& rep, int R, int rdt,
-                                              const int64_t (&e0)[U], int cnt) {
-    constexpr int T = U * VEC;
-    float x[T];
-#pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(p, e0[q], cnt, slice<VEC, T>(x, q));
-    for (int r = 0; r < R; ++r) {
-        void* rp = rep(r);
-#pragma unroll
-        for (int q = 0; q < U; ++q) store_replica<VEC, TAIL>(rp, rdt, e0[q], cnt, slice<VEC, T>(x, q));
-    }
-}
-
-template <int VEC, int U>
-__global__ __launch_bounds__(kBlock) void copy_out_kernel(StepArgs a) {
+// With several replicas the copy-out runs as a pass of its own after the step
+// kernel (which then writes no replica). It runs replica-major over windows of
+// the parameter vector: workgroup b writes block s of window w to replica
+// group q (RK consecutive replicas), b = (w*ceil(R/RK) + q)*win_blocks + s, so
+// at any time the chip writes a few replica streams instead of all R. With
+// win_blocks a multiple of 8 each XCD (workgroups go to XCD b % 8) reads the
+// same eighth of the window for every replica group: after the first group the
+// window comes from that XCD's L2 (p is read with cache-allocating loads; a
+// window is 8 MB, 1 MB per XCD). A lane loads U units of p and stores them to
+// each of its group's replicas: several loads in flight and several stores per
+// load keep the pass at the write bandwidth (one unit and one replica per lane
+// left the bfloat16 pass at about half of it). Binary32 replicas take
+// 4-element units, bfloat16 replicas 8-element units, so every store is 16
+// bytes. The host splits grids above kMaxGridBlocks into several launches.
+template <int VEC, int U, int RK>
+__global__ __launch_bounds__(kBlock) void copy_out_rmajor_kernel(StepArgs a) {
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
-    auto rep = [&](int r) { return a.replicas[r]; };
-    for_tiles<U, VEC>(
-        full, full + (rem != 0), a.xcd_chunk, a.upl,
-        [&](const int64_t (&e0)[U]) { copy_out_tile<VEC, U, false>(a.p, rep, a.n_replicas, a.rdt, e0, VEC); },
-        [&](int64_t u) {
-            const int64_t e[1] = {u * VEC};
-            if (u < full) copy_out_tile<VEC, 1, false>(a.p, rep, a.n_replicas, a.rdt, e, VEC);
-            else copy_out_tile<VEC, 1, true>(a.p, rep, a.n_replicas, a.rdt, e, rem);
-        });
+    const int n_rg = (a.n_replicas + RK - 1) / RK;
+    const int64_t per_win = static_cast<int64_t>(a.win_blocks) * n_rg;
+    const int64_t b = a.block0 + blockIdx.x;
+    const int64_t w = b / per_win;
+    const int64_t rb = b - w * per_win;
+    const int q = static_cast<int>(rb / a.win_blocks);
+    const int64_t sblk = rb - static_cast<int64_t>(q) * a.win_blocks;
+    const int64_t u0 = (w * a.win_blocks + sblk) * kBlock * U + threadIdx.x;
+    const int r0 = q * RK;
+    float x[U][VEC];
+#pragma unroll
+    for (int t = 0; t < U; ++t) {
+        const int64_t u = u0 + static_cast<int64_t>(t) * kBlock;
+        if (u < full) load_f32_cached<VEC, false>(a.p, u * VEC, VEC, x[t]);
+        else if (u == full && rem != 0) load_f32_cached<VEC, true>(a.p, u * VEC, rem, x[t]);
+    }
+#pragma unroll
+    for (int k = 0; k < RK; ++k) {
+        if (r0 + k >= a.n_replicas) break;
+        void* dst = a.replicas[r0 + k];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+            const int64_t u = u0 + static_cast<int64_t>(t) * kBlock;
+            if (u < full) store_replica<VEC, false>(dst, a.rdt, u * VEC, VEC, x[t]);
+            else if (u == full && rem != 0) store_replica<VEC, true>(dst, a.rdt, u * VEC, rem, x[t]);
+        }
+    }
 }
 
 }  // namespace lsgd

@@ -120,6 +120,31 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     return a;
 }
 
+// Replicas per workgroup of the plan's copy-out pass (as for flat steps: a
+// lane loads 32 bytes of p and stores 32 bytes per tile).
+constexpr int kPlanCopyRKF32 = 1, kPlanCopyRKBF16 = 2;
+
+// The copy-out pass of a plan step: one workgroup per bucket and replica
+// group; a lane tile covers a 2048-element piece (the usual piece size).
+template <int VEC, int RK>
+lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t s) {
+    constexpr int U = 2048 / (VEC * kBlock);
+    static_assert(U >= 1, "at least one unit per lane");
+    const int64_t win = std::min<int64_t>(copy_window_blocks(4 * plan->piece),
+                                          (static_cast<int64_t>(plan->n_buckets) + 7) / 8 * 8);
+    const int64_t blocks = (plan->n_buckets + win - 1) / win * ((plan->n_replicas + RK - 1) / RK) * win;
+    a.win_blocks = static_cast<int32_t>(win);
+    for (int64_t b0 = 0; b0 < blocks; b0 += kMaxGridBlocks) {   // b0 stays a multiple of 8
+        a.block0 = b0;
+        const int64_t nb = std::min<int64_t>(kMaxGridBlocks, blocks - b0);
+        hipLaunchKernelGGL((copy_out_plan_rmajor<VEC, U, RK>), dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, s,
+                           a);
+        const lsgd_status st = check_launch("lsgd_step_plan (copy-out)");
+        if (st != LSGD_OK) return st;
+    }
+    return LSGD_OK;
+}
+
 // LARS pass-1 kernels: compile-time (W, G) as for the step, else segmented.
 template <typename GT, int W>
 LarsKernel pick_lars_g(int G) {
@@ -271,6 +296,9 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     }
     if ((st = check_overlap(ranges)) != LSGD_OK) return st;
     if (chunks.size() > 0x7fffffff) return fail(LSGD_ERR_SIZE, "too many pieces");
+    // one workgroup per bucket (and per tensor in the LARS trust kernel), in one launch
+    if (static_cast<int64_t>(bucket_begin.size()) > kMaxGridBlocks || n_tensors > kMaxGridBlocks)
+        return fail(LSGD_ERR_SIZE, "more than %lld buckets or tensors", static_cast<long long>(kMaxGridBlocks));
     bucket_begin.push_back(static_cast<int32_t>(chunks.size()));
     tensor_chunks[n_tensors] = static_cast<int32_t>(chunks.size());
 
@@ -379,9 +407,8 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, s, a);
     if ((st = check_launch("lsgd_step_plan")) != LSGD_OK || !split) return st;
     a.n_replicas = plan->n_replicas;
-    const PlanKernel kc = plan->rdt == LSGD_BF16 ? copy_out_plan_kernel<8, 1> : copy_out_plan_kernel<4, 2>;
-    hipLaunchKernelGGL(kc, dim3(ls.blocks), dim3(kBlock), 0, s, a);
-    return check_launch("lsgd_step_plan (copy-out)");
+    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, a, s)
+                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
 }
 
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
@@ -450,11 +477,15 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
     }
     hipLaunchKernelGGL(lars_trust_kernel, dim3(plan->n_tensors), dim3(kBlock), 0, s, la);
     if ((st = check_launch("lsgd_lars_step_plan (trust)")) != LSGD_OK) return st;
-    if (plan->n_buckets > 0) {
-        hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
-        if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK) return st;
-    }
-    return LSGD_OK;
+    if (plan->n_buckets == 0) return LSGD_OK;
+    // the update reads and writes as lsgd_sgd_step does: the same copy-out rule
+    const bool split = separate_copy_out_update(plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4);
+    if (split) la.pa.n_replicas = 0;
+    hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
+    if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK || !split) return st;
+    la.pa.n_replicas = plan->n_replicas;
+    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, la.pa, s)
+                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, la.pa, s);
 }
 
 LSGD_API lsgd_status lsgd_plan_set_lars_exclude(lsgd_plan* plan, const uint8_t* exclude) {

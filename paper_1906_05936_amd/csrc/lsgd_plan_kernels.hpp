@@ -34,6 +34,8 @@ struct PlanArgs {
     Hyper h;
     int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
+    int32_t win_blocks;    // replica-major copy-out: buckets per window (a multiple of 8)
+    int64_t block0;        // replica-major copy-out: workgroup number of this launch's first workgroup
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
 };
 
@@ -119,32 +121,57 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     });
 }
 
-// Copy-out pass over a plan's chunks (see copy_out_kernel).
-template <int VEC, int U>
-__global__ __launch_bounds__(kBlock) void copy_out_plan_kernel(PlanArgs a) {
-    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
-        const float* p = s.p();
-        auto rep = [&](int r) { return s.replica(r); };
-        const int64_t full = ch.len / VEC;
-        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
-            if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
-                int64_t e0[U];
+// Replica-major copy-out pass over a plan's buckets (the layout of
+// copy_out_rmajor_kernel with buckets in place of fixed-size blocks): workgroup
+// b copies bucket w*win_blocks + s to replica group q (RK consecutive
+// replicas), b = (w*ceil(R/RK) + q)*win_blocks + s; a lane loads U units of
+// p, then stores them to each replica of the group.
+template <int VEC, int U, int RK>
+__global__ __launch_bounds__(kBlock) void copy_out_plan_rmajor(PlanArgs a) {
+    const int n_rg = (a.n_replicas + RK - 1) / RK;
+    const int64_t per_win = static_cast<int64_t>(a.win_blocks) * n_rg;
+    const int64_t b = a.block0 + blockIdx.x;
+    const int64_t w = b / per_win;
+    const int64_t rb = b - w * per_win;
+    const int q = static_cast<int>(rb / a.win_blocks);
+    const int64_t bucket = w * a.win_blocks + (rb - static_cast<int64_t>(q) * a.win_blocks);
+    if (bucket >= a.n_buckets) return;   // padding of the last window
+    const int r0 = q * RK;
+    const int nr = min(RK, a.n_replicas - r0);
+    const int32_t c_end = read_table(&a.bucket_begin[bucket + 1]);
+    for (int32_t c = read_table(&a.bucket_begin[bucket]); c < c_end; ++c) {
+        const PlanChunk* cp = &a.chunks[c];
+        const int64_t start = read_table(&cp->start), len = read_table(&cp->len);
+        void* const* t = a.ptrs + static_cast<int64_t>(read_table(&cp->tensor)) * a.stride;
+        const float* p = static_cast<const float*>(read_table(&t[0]));
+        void* dst[RK];
 #pragma unroll
-                for (int q = 0; q < U; ++q) e0[q] = ch.start + (t0 + static_cast<int64_t>(q) * kBlock) * VEC;
-                copy_out_tile<VEC, U, false>(p, rep, a.n_replicas, a.rdt, e0, VEC);
-            } else {
-                for (int64_t u = t0; u < full; u += kBlock) {
-                    const int64_t e[1] = {ch.start + u * VEC};
-                    copy_out_tile<VEC, 1, false>(p, rep, a.n_replicas, a.rdt, e, VEC);
+        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[2 + a.n_workers + r0 + k]) : nullptr;
+        const int64_t full = len / VEC;
+        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+            float x[U][VEC];
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
+                if (u < full) load_f32_cached<VEC, false>(p, start + u * VEC, VEC, x[i]);
+            }
+#pragma unroll
+            for (int k = 0; k < RK; ++k) {
+                if (k >= nr) break;
+#pragma unroll
+                for (int i = 0; i < U; ++i) {
+                    const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
+                    if (u < full) store_replica<VEC, false>(dst[k], a.rdt, start + u * VEC, VEC, x[i]);
                 }
             }
         }
-        const int rem = static_cast<int>(ch.len - full * VEC);
+        const int rem = static_cast<int>(len - full * VEC);
         if (rem != 0 && threadIdx.x == 0) {
-            const int64_t e[1] = {ch.start + full * VEC};
-            copy_out_tile<VEC, 1, true>(p, rep, a.n_replicas, a.rdt, e, rem);
+            float x[VEC];
+            load_f32_cached<VEC, true>(p, start + full * VEC, rem, x);
+            for (int k = 0; k < nr; ++k) store_replica<VEC, true>(dst[k], a.rdt, start + full * VEC, rem, x);
         }
-    });
+    }
 }
 
 }  // namespace lsgd

@@ -136,6 +136,23 @@ def test_lars_plan_matches_oracle(G, W, gdt, R, rdt):
     c.plan.close()
 
 
+@pytest.mark.parametrize("mode", ["fused", "separate"])
+@pytest.mark.parametrize("R,rdt", [(5, "f32"), (6, "bf16")])
+def test_lars_copy_out_modes(mode, R, rdt):
+    """The replicas written inside the update kernel and by the copy-out pass
+    (replica groups that do not divide R) both match the oracle."""
+    log("lars copy-out %s R=%d %s" % (mode, R, rdt))
+    lsgd.set_copy_out_mode(lsgd.COPY_OUT_FUSED if mode == "fused" else lsgd.COPY_OUT_SEPARATE)
+    try:
+        c = Case(2, 2, "f32", R, rdt, seed=31 + R)
+        for step in range(2):
+            c.new_grads()
+            c.check(0.1, 0.9, 1e-4, TRUST_COEF, step)
+        c.plan.close()
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+
+
 def test_lars_special_coefficients():
     """eta = 0 (trust 0: the momentum only decays) and wd = 0, on the same plan."""
     c = Case(4, 4, "f32", 2, "f32", seed=77)

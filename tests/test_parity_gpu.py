@@ -657,11 +657,14 @@ def test_graph_captured_whole_step_follows_the_schedule():
 # ---------------------------------------------------------------- copy-out pass
 
 @pytest.mark.parametrize("G,W,gdt,R,rdt,n", [(4, 4, "f32", 33, "f32", 100_003), (2, 2, "bf16", 9, "bf16", 77_777),
-                                             (8, 8, "f32", 3, "f32", 65_539), (3, 5, "f32", 20, "bf16", 4_099)])
+                                             (8, 8, "f32", 3, "f32", 65_539), (3, 5, "f32", 20, "bf16", 4_099),
+                                             (2, 2, "f32", 5, "f32", 4_500_007), (2, 1, "bf16", 7, "bf16", 4_500_011)])
 def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
     """The replicas written in the step kernel, in a copy-out pass of their own,
     and by the automatic choice: all bitwise equal to the oracle, flat and
-    through a plan (ragged sizes)."""
+    through a plan (ragged sizes; the last two cases span three 8 MB windows of
+    the copy-out pass, the last one partial, and replica counts that the
+    replicas-per-workgroup grouping does not divide)."""
     log("copy-out modes G=%d W=%d %s R=%d %s n=%d" % (G, W, gdt, R, rdt, n))
     rng = np.random.default_rng(n)
     N = G * W
