@@ -339,7 +339,8 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
  *
  * The step runs three kernels on `stream`: the mean gradient plus per-chunk
  * binary64 partial norms, the per-tensor trust ratios, then the update and
- * copy-out. The workspace is caller-owned device memory of at least
+ * copy-out (the copy-out as a fourth kernel where lsgd_set_copy_out_mode's
+ * rule for lsgd_sgd_step picks the separate pass). The workspace is caller-owned device memory of at least
  * lsgd_lars_workspace_size bytes, 256-byte aligned, that must not overlap any
  * buffer of the plan or trust_out; it holds the mean gradient (4 bytes per
  * element), the partial norms and the trust ratios, and its contents are not
