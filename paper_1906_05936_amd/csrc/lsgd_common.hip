@@ -189,6 +189,13 @@ bool separate_copy_out_update(int32_t n_replicas, size_t rsz) {
     return rsz == 4 && n_replicas >= 4;
 }
 
+int64_t stride_grid_cap() {
+    const int32_t bpc = g_blocks_per_cu.load(std::memory_order_relaxed);
+    if (bpc <= 0) return kMaxGridBlocks;
+    const int64_t cap = static_cast<int64_t>(device_cus()) * bpc / 8 * 8;
+    return std::min<int64_t>(kMaxGridBlocks, std::max<int64_t>(8, cap));
+}
+
 LaunchShape launch_shape(int64_t units, int tile) {
     const int64_t upl = g_units_per_lane.load(std::memory_order_relaxed);
     const int64_t span = static_cast<int64_t>(kBlock) * upl * (tile < 1 ? 1 : tile);

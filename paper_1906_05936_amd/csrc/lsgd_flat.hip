@@ -112,15 +112,12 @@ lsgd_status launch_copy_out_rmajor(StepArgs& a, hipStream_t stream) {
     const int64_t win = std::min<int64_t>(copy_window_blocks(4 * VEC * span), (need + 7) / 8 * 8);
     const int64_t blocks = (need + win - 1) / win * ((a.n_replicas + RK - 1) / RK) * win;
     a.win_blocks = static_cast<int32_t>(win);
-    for (int64_t b0 = 0; b0 < blocks; b0 += kMaxGridBlocks) {   // b0 stays a multiple of 8
-        a.block0 = b0;
-        const int64_t nb = std::min<int64_t>(kMaxGridBlocks, blocks - b0);
-        hipLaunchKernelGGL((copy_out_rmajor_kernel<VEC, U, RK>), dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0,
-                           stream, a);
-        const lsgd_status st = check_launch("lsgd_step (copy-out)");
-        if (st != LSGD_OK) return st;
-    }
-    return LSGD_OK;
+    a.copy_blocks = blocks;
+    // one workgroup per logical block: grid-stride forms (2048-8192 workgroups) measured 10-25% slower
+    const int64_t grid = std::min<int64_t>(blocks, stride_grid_cap());
+    hipLaunchKernelGGL((copy_out_rmajor_kernel<VEC, U, RK>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0,
+                       stream, a);
+    return check_launch("lsgd_step (copy-out)");
 }
 
 // The copy-out pass of a flat step: p (already updated on `stream`) to the

@@ -74,6 +74,11 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
 // The same for lsgd_sgd_step.
 bool separate_copy_out_update(int32_t n_replicas, size_t rsz);
 
+// Largest grid of a grid-stride kernel whose XCD assignment must not change
+// between strides: kMaxGridBlocks, or the blocks_per_cu cap of
+// lsgd_set_launch_shape rounded down to a multiple of 8.
+int64_t stride_grid_cap();
+
 // Workgroups per window of the replica-major copy-out pass whose workgroups
 // each read `block_p_bytes` of p: a multiple of 8, so that each XCD reads the
 // same part of the window for every replica.

@@ -478,7 +478,7 @@ struct StepArgs {
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
     int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
     int32_t win_blocks;    // replica-major copy-out: workgroups per window and replica group (a multiple of 8)
-    int64_t block0;        // replica-major copy-out: workgroup number of this launch's first workgroup
+    int64_t copy_blocks;   // replica-major copy-out: logical workgroups (the grid strides over them)
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
     const void* grads[kMaxWorkers];
     void* replicas[kMaxReplicas];
@@ -945,14 +945,13 @@ __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
 // load keep the pass at the write bandwidth (one unit and one replica per lane
 // left the bfloat16 pass at about half of it). Binary32 replicas take
 // 4-element units, bfloat16 replicas 8-element units, so every store is 16
-// bytes. The host splits grids above kMaxGridBlocks into several launches.
+// bytes. Grids above kMaxGridBlocks stride over the logical workgroups.
 template <int VEC, int U, int RK>
-__global__ __launch_bounds__(kBlock) void copy_out_rmajor_kernel(StepArgs a) {
+__device__ __forceinline__ void copy_out_rmajor_block(const StepArgs& a, int64_t b) {
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     const int n_rg = (a.n_replicas + RK - 1) / RK;
     const int64_t per_win = static_cast<int64_t>(a.win_blocks) * n_rg;
-    const int64_t b = a.block0 + blockIdx.x;
     const int64_t w = b / per_win;
     const int64_t rb = b - w * per_win;
     const int q = static_cast<int>(rb / a.win_blocks);
@@ -977,6 +976,13 @@ __global__ __launch_bounds__(kBlock) void copy_out_rmajor_kernel(StepArgs a) {
             else if (u == full && rem != 0) store_replica<VEC, true>(dst, a.rdt, u * VEC, rem, x[t]);
         }
     }
+}
+
+// The grid (a multiple of 8 workgroups, or all of them) strides over the
+// logical workgroups, so each keeps its XCD.
+template <int VEC, int U, int RK>
+__global__ __launch_bounds__(kBlock) void copy_out_rmajor_kernel(StepArgs a) {
+    for (int64_t b = blockIdx.x; b < a.copy_blocks; b += gridDim.x) copy_out_rmajor_block<VEC, U, RK>(a, b);
 }
 
 }  // namespace lsgd

@@ -134,15 +134,10 @@ lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t
                                           (static_cast<int64_t>(plan->n_buckets) + 7) / 8 * 8);
     const int64_t blocks = (plan->n_buckets + win - 1) / win * ((plan->n_replicas + RK - 1) / RK) * win;
     a.win_blocks = static_cast<int32_t>(win);
-    for (int64_t b0 = 0; b0 < blocks; b0 += kMaxGridBlocks) {   // b0 stays a multiple of 8
-        a.block0 = b0;
-        const int64_t nb = std::min<int64_t>(kMaxGridBlocks, blocks - b0);
-        hipLaunchKernelGGL((copy_out_plan_rmajor<VEC, U, RK>), dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, s,
-                           a);
-        const lsgd_status st = check_launch("lsgd_step_plan (copy-out)");
-        if (st != LSGD_OK) return st;
-    }
-    return LSGD_OK;
+    a.copy_blocks = blocks;
+    const int64_t grid = std::min<int64_t>(blocks, stride_grid_cap());   // the kernel strides over the rest
+    hipLaunchKernelGGL((copy_out_plan_rmajor<VEC, U, RK>), dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, s, a);
+    return check_launch("lsgd_step_plan (copy-out)");
 }
 
 // LARS pass-1 kernels: compile-time (W, G) as for the step, else segmented.

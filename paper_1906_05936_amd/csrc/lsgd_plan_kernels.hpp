@@ -35,7 +35,7 @@ struct PlanArgs {
     int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
     int32_t win_blocks;    // replica-major copy-out: buckets per window (a multiple of 8)
-    int64_t block0;        // replica-major copy-out: workgroup number of this launch's first workgroup
+    int64_t copy_blocks;   // replica-major copy-out: logical workgroups (the grid strides over them)
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
 };
 
@@ -127,10 +127,9 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
 // replicas), b = (w*ceil(R/RK) + q)*win_blocks + s; a lane loads U units of
 // p, then stores them to each replica of the group.
 template <int VEC, int U, int RK>
-__global__ __launch_bounds__(kBlock) void copy_out_plan_rmajor(PlanArgs a) {
+__device__ __forceinline__ void copy_out_plan_block(const PlanArgs& a, int64_t b) {
     const int n_rg = (a.n_replicas + RK - 1) / RK;
     const int64_t per_win = static_cast<int64_t>(a.win_blocks) * n_rg;
-    const int64_t b = a.block0 + blockIdx.x;
     const int64_t w = b / per_win;
     const int64_t rb = b - w * per_win;
     const int q = static_cast<int>(rb / a.win_blocks);
@@ -172,6 +171,11 @@ __global__ __launch_bounds__(kBlock) void copy_out_plan_rmajor(PlanArgs a) {
             for (int k = 0; k < nr; ++k) store_replica<VEC, true>(dst[k], a.rdt, start + full * VEC, rem, x);
         }
     }
+}
+
+template <int VEC, int U, int RK>
+__global__ __launch_bounds__(kBlock) void copy_out_plan_rmajor(PlanArgs a) {
+    for (int64_t b = blockIdx.x; b < a.copy_blocks; b += gridDim.x) copy_out_plan_block<VEC, U, RK>(a, b);
 }
 
 }  // namespace lsgd

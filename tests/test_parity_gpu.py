@@ -418,20 +418,23 @@ def test_results_independent_of_launch_shape():
             outs = []
             for sh in shapes:
                 lsgd.set_launch_shape(*sh)
-                p, m = p0.clone(), torch.zeros(n, device=DEV)
-                reps = [torch.empty(n, device=DEV) for _ in range(2)]
-                for _ in range(2):
-                    lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
-                gm = [torch.empty(n, device=DEV) for _ in range(G)]
-                lsgd.group_mean(grads, gow, G, gm)
-                gbar = torch.empty(n, device=DEV)
-                lsgd.global_mean(gm, gbar)
-                outs.append((p, m, reps[1], gbar))
-            for sh, o in zip(shapes[1:], outs[1:]):
-                for a, b in zip(outs[0], o):
-                    assert torch.equal(a, b), sh
+                for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE):   # the copy-out grid strides too
+                    lsgd.set_copy_out_mode(mode)
+                    p, m = p0.clone(), torch.zeros(n, device=DEV)
+                    reps = [torch.empty(n, device=DEV) for _ in range(3)]
+                    for _ in range(2):
+                        lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
+                    gm = [torch.empty(n, device=DEV) for _ in range(G)]
+                    lsgd.group_mean(grads, gow, G, gm)
+                    gbar = torch.empty(n, device=DEV)
+                    lsgd.global_mean(gm, gbar)
+                    outs.append((sh, mode, (p, m, reps[0], reps[2], gbar)))
+            for sh, mode, o in outs[1:]:
+                for a, b in zip(outs[0][2], o):
+                    assert torch.equal(a, b), (sh, mode)
     finally:
         lsgd.set_launch_shape(*default)
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
 
 
 @pytest.mark.parametrize("nbytes", [16, 48, 4096 + 16, 1 << 20, (1 << 27) + 16 * 333])
@@ -677,8 +680,13 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
     oracle.lsgd_step(ph, mh, gh, gow, G, 0.1, 0.9, 1e-4, rr, oracle.BF16 if rdt == "bf16" else oracle.F32)
     rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
     sizes = [n // 3, 1, n - n // 3 - 1]
+    default_shape = lsgd.get_launch_shape()
     try:
-        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO):
+        # the last pass: the copy-out pass on a grid of one workgroup per CU, striding
+        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO, "strided"):
+            if mode == "strided":
+                lsgd.set_launch_shape(default_shape[0], 1, default_shape[2])
+                mode = lsgd.COPY_OUT_SEPARATE
             lsgd.set_copy_out_mode(mode)
             p, m = to_dev(p0), torch.zeros(n, device=DEV)
             reps = [torch.full((n,), 7, device=DEV, dtype=rtd) for _ in range(R)]
@@ -703,6 +711,7 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
             plan.close()
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+        lsgd.set_launch_shape(*default_shape)
 
 
 def test_graph_with_separate_copy_out_matches_eager():
