@@ -172,9 +172,10 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
 // 24 MB the window no longer stays in L2 and the pass slows by a third.
 constexpr int64_t kCopyWindowBytes = 8 << 20;
 
-int64_t copy_window_blocks(int64_t block_p_bytes) {
-    const int64_t blocks = kCopyWindowBytes / block_p_bytes;
-    return std::max<int64_t>(8, blocks / 8 * 8);
+int64_t copy_window_blocks(int64_t block_p_bytes, int64_t blocks) {
+    const int64_t target = std::max<int64_t>(8, kCopyWindowBytes / block_p_bytes / 8 * 8);
+    const int64_t windows = std::max<int64_t>(1, (blocks + target - 1) / target);
+    return ((blocks + windows - 1) / windows + 7) / 8 * 8;   // equal windows, the last one barely padded
 }
 
 // The same choice for lsgd_sgd_step (reads 12 bytes per element, writes 8 plus

@@ -109,7 +109,7 @@ lsgd_status launch_copy_out_rmajor(StepArgs& a, hipStream_t stream) {
     const int64_t units = (a.n + VEC - 1) / VEC;
     const int64_t span = static_cast<int64_t>(kBlock) * U;   // units per workgroup
     const int64_t need = (units + span - 1) / span;
-    const int64_t win = std::min<int64_t>(copy_window_blocks(4 * VEC * span), (need + 7) / 8 * 8);
+    const int64_t win = copy_window_blocks(4 * VEC * span, need);
     const int64_t blocks = (need + win - 1) / win * ((a.n_replicas + RK - 1) / RK) * win;
     a.win_blocks = static_cast<int32_t>(win);
     a.copy_blocks = blocks;

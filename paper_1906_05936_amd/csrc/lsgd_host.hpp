@@ -79,10 +79,11 @@ bool separate_copy_out_update(int32_t n_replicas, size_t rsz);
 // lsgd_set_launch_shape rounded down to a multiple of 8.
 int64_t stride_grid_cap();
 
-// Workgroups per window of the replica-major copy-out pass whose workgroups
-// each read `block_p_bytes` of p: a multiple of 8, so that each XCD reads the
-// same part of the window for every replica.
-int64_t copy_window_blocks(int64_t block_p_bytes);
+// Workgroups per window of the replica-major copy-out pass over `blocks`
+// workgroups that each read `block_p_bytes` of p: about 8 MB of p per window,
+// windows of equal size, a multiple of 8 workgroups (so that each XCD reads
+// the same part of the window for every replica).
+int64_t copy_window_blocks(int64_t block_p_bytes, int64_t blocks);
 
 // Grid of exactly `blocks` logical workgroups, each covering `block_bytes` of
 // every buffer, padded for the XCD chunking (kernels skip logical blocks

@@ -130,8 +130,7 @@ template <int VEC, int RK>
 lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t s) {
     constexpr int U = 2048 / (VEC * kBlock);
     static_assert(U >= 1, "at least one unit per lane");
-    const int64_t win = std::min<int64_t>(copy_window_blocks(4 * plan->piece),
-                                          (static_cast<int64_t>(plan->n_buckets) + 7) / 8 * 8);
+    const int64_t win = copy_window_blocks(4 * plan->piece, plan->n_buckets);
     const int64_t blocks = (plan->n_buckets + win - 1) / win * ((plan->n_replicas + RK - 1) / RK) * win;
     a.win_blocks = static_cast<int32_t>(win);
     a.copy_blocks = blocks;
