@@ -80,7 +80,7 @@ class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
     def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3,
-                 lars_exclude=None, tensor_layout="separate"):
+                 lars_exclude=None, tensor_layout="separate", copy_out="auto"):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
@@ -145,6 +145,20 @@ class Setup:
 
                 def step():
                     check(fn(h, *hyper, s))
+                if R and separate_copy_out(wl, R, copy_out):
+                    # the same two kernels launched one at a time: the step over
+                    # a plan of the same tensors without replicas, then the
+                    # plan's copy-out pass
+                    self.plan0 = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, [])
+                    h0 = self.plan0._handle
+
+                    def step_part():
+                        check(fn(h0, *hyper, s))
+
+                    def copy_part():
+                        check(lib.lsgd_plan_copy_out(h, s))
+                    self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes()),
+                                  ("copy_out_plan_rmajor", copy_part, self._copy_bytes())]
         else:
             self.plan = None
             self.params = [flat_p]
@@ -172,27 +186,57 @@ class Setup:
 
             def step():
                 check(fn(*args))
+            if R and separate_copy_out(wl, R, copy_out):
+                # the same two kernels launched one at a time: the step without
+                # replicas on the same buffers, then the copy-out pass
+                args0 = args[:11] + (None, 0) + args[13:]
+                copy_args = (self.params[0].data_ptr(), wl.n, common[11], R, common[13],
+                             ctypes.c_void_p(stream.cuda_stream))
+
+                def step_part():
+                    check(fn(*args0))
+
+                def copy_part():
+                    check(lib.lsgd_copy_out(*copy_args))
+                self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes()),
+                              ("copy_out_rmajor_kernel", copy_part, self._copy_bytes())]
         del scratch
         self.step = step
         self.stream = stream
 
+    def _step_bytes(self):
+        """Algorithmic bytes of the step kernel when it writes no replica."""
+        wl = self.wl
+        return wl.algorithmic_bytes(0) + (wl.n * wl.n_workers * 4 if self.broadcast_grad else 0)
+
+    def _copy_bytes(self):
+        """Algorithmic bytes of the copy-out pass: p read, R replicas written."""
+        wl = self.wl
+        return wl.n * (4 + self.R * (2 if wl.replica_dtype == "bf16" else 4))
+
+    parts = None     # [(kernel, callable, algorithmic bytes)] when the step is two kernels
+    plan0 = None
+
     def close(self):
         if self.plan is not None:
             self.plan.close()
+        if self.plan0 is not None:
+            self.plan0.close()
 
 
-def time_steps(setup, steps, warmup):
-    """Average ms per step over `steps` back-to-back launches, HIP events on the
-    launch stream, synchronized on both sides."""
+def time_steps(setup, steps, warmup, fn=None):
+    """Average ms per step (or per call of `fn`) over `steps` back-to-back
+    launches, HIP events on the launch stream, synchronized on both sides."""
     import torch
+    fn = fn or setup.step
     for _ in range(warmup):
-        setup.step()
+        fn()
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(setup.stream)
     for _ in range(steps):
-        setup.step()
+        fn()
     t1.record(setup.stream)
     t1.synchronize()
     torch.cuda.synchronize()
@@ -508,23 +552,29 @@ def derive_traffic(args):
     write_rows = _read_counters(args.write_csv)
     if args.lars:
         return _derive_traffic_lars(args, wl, R, fetch_rows, write_rows)
-    kname = kernel_match(wl)
-    f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", kname)
-    w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", kname)
-    if any("copy_out" in r.get("Kernel_Name", "") for r in fetch_rows):   # the step's copy-out pass
-        f_c2, _ = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", "copy_out")
-        w_c2, _ = _per_dispatch_kib(write_rows, "WRITE_SIZE", "copy_out")
-        f_k, w_k, kname = f_k + f_c2, w_k + w_c2, kname + " + copy_out"
     f_c, _ = _calib_kib(fetch_rows, "FETCH_SIZE")
     w_c, _ = _calib_kib(write_rows, "WRITE_SIZE")
     known = CALIB_ELEMS * 4 / 1024.0
     f_scale, w_scale = known / f_c, known / w_c
-    fetch_b = f_k * f_scale * 1024
-    write_b = w_k * w_scale * 1024
+    kname = kernel_match(wl)
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    split = any("copy_out" in r.get("Kernel_Name", "") for r in fetch_rows)   # the step's copy-out pass
+    per_alg = {kname: wl.algorithmic_bytes(0 if split else R)}
+    if split:
+        per_alg["copy_out"] = wl.n * (4 + R * rb)
+    per = {}
+    for k, a in per_alg.items():
+        f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", k)
+        w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", k)
+        rbytes, wbytes = f_k * f_scale * 1024, w_k * w_scale * 1024
+        per[k] = {"fetch_kib_per_dispatch": f_k, "write_kib_per_dispatch": w_k, "dispatches": [nf, nw],
+                  "read_bytes": rbytes, "write_bytes": wbytes, "traffic_bytes": rbytes + wbytes,
+                  "algorithmic_bytes": a, "traffic_over_algorithmic": (rbytes + wbytes) / a}
+    fetch_b = sum(v["read_bytes"] for v in per.values())
+    write_b = sum(v["write_bytes"] for v in per.values())
     alg = wl.algorithmic_bytes(R)
-    out = {"workload": wl.name, "replicas": R, "kernel": kname, "source_digest": libbuild.source_digest(),
-           "fetch_kib_per_dispatch": f_k, "write_kib_per_dispatch": w_k, "dispatches": [nf, nw],
-           "copy_fetch_kib": f_c, "copy_write_kib": w_c, "copy_known_kib": known,
+    out = {"workload": wl.name, "replicas": R, "kernel": " + ".join(per), "source_digest": libbuild.source_digest(),
+           "kernels": per, "copy_fetch_kib": f_c, "copy_write_kib": w_c, "copy_known_kib": known,
            "fetch_scale": f_scale, "write_scale": w_scale,
            "traffic_bytes": fetch_b + write_b, "read_bytes": fetch_b, "write_bytes": write_b,
            "algorithmic_bytes": alg, "traffic_over_algorithmic": (fetch_b + write_b) / alg}
@@ -589,7 +639,9 @@ def _derive_traffic_lars(args, wl, R, fetch_rows, write_rows):
     print(json.dumps(out))
 
 
-def stored_traffic(wl, R, lars=False):
+def stored_traffic(wl, R, lars=False, kernel=None):
+    """HBM bytes per step (or per launch of `kernel`) from the committed counter
+    summary, or None when it is missing or older than the current kernels."""
     from paper_1906_05936_amd import build as libbuild
     path = os.path.join(PROFILES, "traffic_%s%s_R%d.json" % (wl.name, "_lars" if lars else "", R))
     if not os.path.exists(path):
@@ -598,7 +650,12 @@ def stored_traffic(wl, R, lars=False):
         t = json.load(f)
     if t.get("source_digest") != libbuild.source_digest():
         return None          # the kernels changed since the counters were taken
-    return t["traffic_bytes"]
+    if kernel is None:
+        return t["traffic_bytes"]
+    for k, v in t.get("kernels", {}).items():
+        if k == kernel or (k == "copy_out" and "copy_out" in kernel):
+            return v["traffic_bytes"]
+    return None
 
 
 # ---------------------------------------------------------------- main
@@ -671,8 +728,15 @@ def main(argv=None):
             raise SystemExit("--lars-exclude-vectors knows the ResNet-50 tensor list only")
         lars_excl = workloads.resnet50_vector_params()
     setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
-                  args.tensor_layout)
+                  args.tensor_layout, args.copy_out)
     ms = time_steps(setup, args.steps, args.warmup)
+    kernels = []
+    if setup.parts:   # two kernels per step: each timed on its own, same buffers, same K
+        for name, fn, nbytes in setup.parts:
+            kms = time_steps(setup, args.steps, args.warmup, fn)
+            kg = nbytes / (kms * 1e-3) / 1e9
+            kernels.append({"kernel": name, "ms": round(kms, 6), "algorithmic_bytes": nbytes,
+                            "GBps": round(kg, 2), "frac": round(kg / PEAK_HBM_GBPS, 4)})
     alg = wl.algorithmic_bytes(R) + extra_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
     traffic = stored_traffic(wl, R, args.lars)
@@ -700,11 +764,18 @@ def main(argv=None):
                      "traffic": traffic, "algorithmic_bytes": alg,
                      "kernel": kernel_match(wl, setup.reduction, args.lars)
                                + (" + lars_trust_kernel + lars_update_kernel" if args.lars else "")
-                               + (" + copy_out" if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
-                                                    else separate_copy_out(wl, R, args.copy_out)) else "")
-                               + (" (whole step)" if args.lars or separate_copy_out(wl, R, args.copy_out) else "")},
+                               + (" + copy_out" if args.lars and lars_separate_copy_out(wl, R, args.copy_out) else "")
+                               + (" (whole step)" if args.lars else "")},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
+    if kernels:
+        # the dominant kernel (most time per step) against the roofline, timed on its own
+        dom = max(kernels, key=lambda k: k["ms"])
+        result["roofline"] = {"bound": "hbm", "achieved": dom["GBps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                              "frac": dom["frac"], "traffic": stored_traffic(wl, R, False, dom["kernel"]),
+                              "algorithmic_bytes": dom["algorithmic_bytes"], "kernel": dom["kernel"]}
+        result["kernels"] = kernels
+        result["kernels_sum_ms"] = round(sum(k["ms"] for k in kernels), 6)
     if R != 0 and not args.no_r0:
         setup.close()
         del setup

@@ -103,7 +103,7 @@ LSGD_API const char* lsgd_last_error(void);
  * are bit-identical for every shape, because each element is computed by one
  * lane from its own inputs in a fixed order). Plans launch one workgroup per
  * bucket: xcd_chunk applies at each lsgd_step_plan, units_per_lane at
- * lsgd_plan_create, blocks_per_cu not at all.
+ * lsgd_plan_create, blocks_per_cu only to their copy-out pass.
  *   xcd_chunk       0 = workgroups in hardware order; C > 0 = each of the eight
  *                   XCDs runs C consecutive logical workgroups per turn (the grid
  *                   is padded to a multiple of 8*C; not applied to grids smaller
@@ -178,6 +178,23 @@ LSGD_API lsgd_status lsgd_global_mean(const float* const* group_means, int32_t n
 LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* grad_mean,
                                    int64_t n, float lr, float momentum_coef,
                                    float weight_decay, void* const* replicas,
+                                   int32_t n_replicas, lsgd_dtype rdt, void* stream);
+
+/*
+ * The copy-out alone (Alg. 3 Broadcast of the updated parameters to the
+ * workers; e.g. after restoring params):
+ *   replicas[r][i] = params[i] (binary32) or params[i] rounded to bfloat16,
+ *   nearest-even (rdt LSGD_BF16), for r < n_replicas.
+ * params: n binary32 (read). replicas: host array of n_replicas device
+ * pointers (may be NULL when n_replicas == 0), each n elements of dtype rdt,
+ * written. 0 <= n_replicas <= LSGD_MAX_REPLICAS. Always the copy-out pass of
+ * lsgd_set_copy_out_mode's separate form (replica-major over windows of
+ * params), whatever the mode. n == 0 or n_replicas == 0 is a no-op. Errors:
+ * LSGD_ERR_NULL, LSGD_ERR_SIZE, LSGD_ERR_DTYPE, LSGD_ERR_ALIGN (a buffer not
+ * 16-byte aligned), LSGD_ERR_ALIAS (a replica overlapping params or another
+ * replica), LSGD_ERR_HIP.
+ */
+LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* replicas,
                                    int32_t n_replicas, lsgd_dtype rdt, void* stream);
 
 /*
@@ -317,6 +334,13 @@ LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momen
 LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float momentum_coef,
                                        float weight_decay, const lsgd_step_options* options,
                                        void* stream);
+
+/* The copy-out alone over a plan (Alg. 3 Broadcast; lsgd_copy_out for every
+ * tensor): each replica tensor = its params tensor (binary32, or bfloat16
+ * nearest-even), in one launch of the plan's copy-out pass. No-op for a plan
+ * without replicas. Errors: LSGD_ERR_NULL (plan NULL), LSGD_ERR_HIP (wrong
+ * device, launch failure). */
+LSGD_API lsgd_status lsgd_plan_copy_out(const lsgd_plan* plan, void* stream);
 
 /* ---- LARS on a plan: one trust ratio per tensor -------------------------
  *

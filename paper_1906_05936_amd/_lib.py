@@ -32,7 +32,8 @@ EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_step", "lsgd_step_ex", "lsgd_lr_at", "lsgd_lr_schedule_step", "lsgd_plan_create",
            "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
            "lsgd_lars_workspace_size", "lsgd_lars_step_plan", "lsgd_set_copy_out_mode",
-           "lsgd_get_copy_out_mode", "lsgd_plan_set_lars_exclude")
+           "lsgd_get_copy_out_mode", "lsgd_plan_set_lars_exclude", "lsgd_copy_out",
+           "lsgd_plan_copy_out")
 
 
 class StepOptions(ctypes.Structure):
@@ -71,6 +72,8 @@ def _load():
     lib.lsgd_group_mean.argtypes = [P, c_int, i32, P, i32, i64, P, P]
     lib.lsgd_global_mean.argtypes = [P, i32, i64, P, P]
     lib.lsgd_sgd_step.argtypes = [P, P, P, i64, f32, f32, f32, P, i32, c_int, P]
+    lib.lsgd_copy_out.argtypes = [P, i64, P, i32, c_int, P]
+    lib.lsgd_plan_copy_out.argtypes = [P, P]
     lib.lsgd_step.argtypes = [P, P, P, c_int, i32, P, i32, i64, f32, f32, f32, P, i32, c_int, P]
     lib.lsgd_plan_create.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, c_int, i32, P, i32, P, i32,
                                      c_int]
@@ -87,7 +90,8 @@ def _load():
     lib.lsgd_plan_set_lars_exclude.argtypes = [P, P]
     lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
     lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P, P]
-    for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
+    for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_copy_out", "lsgd_plan_copy_out",
+                 "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
                  "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_step_plan_ex",
                  "lsgd_lr_schedule_step"):
@@ -310,6 +314,20 @@ def sgd_step(params, momentum, grad_mean, lr, momentum_coef, weight_decay, repli
     check(st)
 
 
+def copy_out(params, replicas, stream=None):
+    """lsgd_copy_out: every replica = params (binary32, or bfloat16 nearest-even)."""
+    n = params.numel()
+    dev = params.device
+    _dev_tensor(params, "params", torch.float32)
+    for r in replicas:
+        _dev_tensor(r, "replica", None, n, dev)
+    rdt = _common_dtype(replicas, "replicas")
+    with torch.cuda.device(dev):
+        st = lib.lsgd_copy_out(params.data_ptr(), n, ptr_array([r.data_ptr() for r in replicas]), len(replicas),
+                               rdt, _stream(stream, dev))
+    check(st)
+
+
 class Plan:
     """lsgd_plan_*: the fused step over a list of parameter tensors, one launch.
 
@@ -363,6 +381,14 @@ class Plan:
                 opts = _options(reduction, broadcast_grad, lr_device, self.device)
                 st = lib.lsgd_step_plan_ex(self._handle, lr, momentum_coef, weight_decay,
                                            ctypes.byref(opts), _stream(stream, self.device))
+        check(st)
+
+    def copy_out(self, stream=None):
+        """lsgd_plan_copy_out: every replica tensor = its params tensor."""
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        with torch.cuda.device(self.device):
+            st = lib.lsgd_plan_copy_out(self._handle, _stream(stream, self.device))
         check(st)
 
     def set_lars_exclude(self, exclude=None):

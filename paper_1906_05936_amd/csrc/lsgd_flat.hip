@@ -376,6 +376,27 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     return launch_copy_out(a, stream);
 }
 
+LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* replicas, int32_t n_replicas,
+                                   lsgd_dtype rdt, void* stream) {
+    if (n < 0) return fail(LSGD_ERR_SIZE, "n=%lld < 0", static_cast<long long>(n));
+    const bool live = n > 0 && n_replicas > 0;
+    std::vector<Range> ranges;
+    lsgd_status st = check_replicas(replicas, n_replicas, rdt, n, live, ranges);
+    if (st != LSGD_OK || !live) return st;
+    if (!params) return fail(LSGD_ERR_NULL, "params is NULL");
+    if (!aligned16(params)) return fail(LSGD_ERR_ALIGN, "params is not 16-byte aligned");
+    ranges.push_back(range_of(params, n, 4, false, "params"));
+    if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+    StepArgs a;
+    memset(&a, 0, sizeof a);
+    a.p = const_cast<float*>(params);   // read only by the copy-out kernel
+    a.n = n;
+    a.n_replicas = n_replicas;
+    a.rdt = static_cast<int32_t>(rdt);
+    for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
+    return launch_copy_out(a, stream);
+}
+
 namespace {
 bool schedule_valid(const lsgd_lr_schedule* c) {
     return c && c->base_batch > 0 && c->warmup_iters >= 0 && c->decay_iters >= 0;

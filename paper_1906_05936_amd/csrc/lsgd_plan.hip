@@ -405,6 +405,18 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
                                   : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
 }
 
+LSGD_API lsgd_status lsgd_plan_copy_out(const lsgd_plan* plan, void* stream) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    if (plan->n_buckets == 0 || plan->n_replicas == 0) return LSGD_OK;
+    lsgd_status st = check_device(plan);
+    if (st != LSGD_OK) return st;
+    LaunchShape ls;
+    PlanArgs a = plan_args(plan, Hyper{0.f, 0.f, 0.f}, nullptr, ls);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, a, s)
+                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
+}
+
 LSGD_API lsgd_status lsgd_step_plan(const lsgd_plan* plan, float lr, float momentum_coef,
                                     float weight_decay, void* stream) {
     return lsgd_step_plan_ex(plan, lr, momentum_coef, weight_decay, nullptr, stream);

@@ -41,7 +41,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = set(declared_functions())
-    assert {"lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_step",
+    assert {"lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_copy_out", "lsgd_plan_copy_out", "lsgd_step",
             "lsgd_plan_create", "lsgd_step_plan", "lsgd_plan_destroy",
             "lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
@@ -165,6 +165,25 @@ def test_sgd_step_validation():
     assert f(n=0, p=0, m=0, g=0) == OK
 
 
+def test_copy_out_validation():
+    f = lambda p=A, n=100, reps=None, R=0, rdt=0: lib.lsgd_copy_out(
+        p, n, pa(reps) if reps is not None else None, R, rdt, None)
+    rep = [A + 100 * MB]
+    assert f(n=-1) == SIZE
+    assert f(reps=rep * 129, R=129) == SIZE
+    assert f(reps=rep, R=1, rdt=5) == DTYPE
+    assert f(R=1) == NULL
+    assert f(reps=[0], R=1) == NULL
+    assert f(p=0, reps=rep, R=1) == NULL
+    assert f(p=A + 4, reps=rep, R=1) == ALIGN
+    assert f(reps=[A + 100 * MB + 8], R=1) == ALIGN
+    assert f(reps=[A + 256], R=1) == ALIAS                      # replica inside params
+    assert f(reps=rep * 2, R=2) == ALIAS                         # two replicas on one buffer
+    assert f(reps=[A + 100 * MB, A + 100 * MB + 192], R=2, rdt=1) == ALIAS
+    assert f(n=0, p=0, reps=rep, R=1) == OK
+    assert f(p=0, R=0) == OK
+
+
 def plan_create(numel=(100, 64), G=2, gow=(0, 0, 1, 1), R=0, gdt=0, rdt=0, params=None,
                 mom=None, grads=None, replicas=None):
     T = len(numel)
@@ -195,6 +214,7 @@ def test_plan_validation_errors():
     assert lib.lsgd_plan_create(None, 1, i64a([1]), pa([A]), pa([A]), pa([A]), 0, 1, i32a([0]), 1,
                                 None, 0, 0) == NULL
     assert lib.lsgd_step_plan(None, 0.1, 0.9, 1e-4, None) == NULL
+    assert lib.lsgd_plan_copy_out(None, None) == NULL
     lib.lsgd_plan_destroy(None)   # NULL-safe
     del h
 

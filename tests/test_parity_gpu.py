@@ -708,10 +708,54 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
                 assert_close(to_host(pt[t]), ph[offs[t]:offs[t + 1]], "plan params %d mode %d" % (t, mode))
                 for r in range(R):
                     assert np.array_equal(to_host(rt[r][t]), rr[r][offs[t]:offs[t + 1]]), (mode, t, r)
+            # the plan's copy-out on its own (lsgd_plan_copy_out) rewrites the same replicas
+            for rl in rt:
+                for x in rl:
+                    x.fill_(7)
+            plan.copy_out()
+            torch.cuda.synchronize()
+            for t in range(3):
+                for r in range(R):
+                    assert np.array_equal(to_host(rt[r][t]), rr[r][offs[t]:offs[t + 1]]), ("copy_out", mode, t, r)
             plan.close()
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
         lsgd.set_launch_shape(*default_shape)
+
+
+@pytest.mark.parametrize("n,R,rdt,strided", [(1, 1, "f32", False), (7, 3, "bf16", False), (4097, 16, "f32", False),
+                                              (4097, 5, "bf16", False), (4_500_007, 3, "f32", False),
+                                              (4_500_011, 4, "bf16", True), (2_000_001, 9, "f32", True)])
+def test_copy_out_entry_matches_oracle(n, R, rdt, strided):
+    """lsgd_copy_out on its own: binary32 replicas equal params bit for bit,
+    bfloat16 replicas equal the oracle's nearest-even rounding (values include
+    NaN, infinities, signed zeros, subnormals and ties); params untouched.
+    Ragged sizes, several 8 MB windows, replica counts the replicas-per-workgroup
+    grouping does not divide, and a strided grid (one workgroup per CU)."""
+    log("copy_out n=%d R=%d %s strided=%s" % (n, R, rdt, strided))
+    rng = np.random.default_rng(n + R)
+    ph = (rng.standard_normal(n) * 3).astype(np.float32)
+    special = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-40, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8,
+                        3.3895314e38, -1.0 - 2 ** -8], np.float32)
+    k = min(n, special.size)
+    ph[rng.choice(n, k, replace=False)] = special[:k]
+    p = to_dev(ph)
+    rtd = torch.bfloat16 if rdt == "bf16" else torch.float32
+    reps = [torch.full((n,), 3, device=DEV, dtype=rtd) for _ in range(R)]
+    default = lsgd.get_launch_shape()
+    try:
+        if strided:
+            lsgd.set_launch_shape(default[0], 1, default[2])
+        lsgd.copy_out(p, reps)
+        torch.cuda.synchronize()
+    finally:
+        lsgd.set_launch_shape(*default)
+    want = oracle.f32_to_bf16(ph) if rdt == "bf16" else ph
+    assert np.array_equal(to_host(p).view(np.uint32), ph.view(np.uint32))
+    for r in range(R):
+        got = to_host(reps[r])
+        assert np.array_equal(got.view(np.uint16 if rdt == "bf16" else np.uint32),
+                              want.view(np.uint16 if rdt == "bf16" else np.uint32)), r
 
 
 def test_graph_with_separate_copy_out_matches_eager():
