@@ -243,6 +243,27 @@ def time_steps(setup, steps, warmup, fn=None):
     return t0.elapsed_time(t1) / steps
 
 
+def time_parts(setup, steps, warmup):
+    """Average ms of each kernel of a step launched one kernel at a time
+    (setup.parts, in step order), with a HIP event recorded on the launch stream
+    before and after every kernel: each kernel runs where it runs in the step,
+    after its predecessor, on the same buffers."""
+    import torch
+    fns = [fn for _, fn, _ in setup.parts]
+    for _ in range(warmup):
+        for fn in fns:
+            fn()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record(setup.stream)
+        for j, fn in enumerate(fns):
+            fn()
+            ev[i][j + 1].record(setup.stream)
+    torch.cuda.synchronize()
+    return [sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps for j in range(len(fns))]
+
+
 def copy_ceiling(dev, calibrate):
     """GB/s of lsgd_stream_copy over 2 GiB (2 GiB read + 2 GiB written): a
     measured ceiling for a plain two-stream read+write pattern, to read the
@@ -731,9 +752,8 @@ def main(argv=None):
                   args.tensor_layout, args.copy_out)
     ms = time_steps(setup, args.steps, args.warmup)
     kernels = []
-    if setup.parts:   # two kernels per step: each timed on its own, same buffers, same K
-        for name, fn, nbytes in setup.parts:
-            kms = time_steps(setup, args.steps, args.warmup, fn)
+    if setup.parts:   # two kernels per step: the step again, an event between its kernels
+        for (name, _, nbytes), kms in zip(setup.parts, time_parts(setup, args.steps, args.warmup)):
             kg = nbytes / (kms * 1e-3) / 1e9
             kernels.append({"kernel": name, "ms": round(kms, 6), "algorithmic_bytes": nbytes,
                             "GBps": round(kg, 2), "frac": round(kg / PEAK_HBM_GBPS, 4)})
@@ -769,7 +789,7 @@ def main(argv=None):
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if kernels:
-        # the dominant kernel (most time per step) against the roofline, timed on its own
+        # the dominant kernel (most time per step) against the roofline
         dom = max(kernels, key=lambda k: k["ms"])
         result["roofline"] = {"bound": "hbm", "achieved": dom["GBps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                               "frac": dom["frac"], "traffic": stored_traffic(wl, R, False, dom["kernel"]),
