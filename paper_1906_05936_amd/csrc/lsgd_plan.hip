@@ -25,6 +25,7 @@ struct lsgd_plan {
     int64_t piece;  // elements per piece and per bucket
     lsgd::PlanChunk* d_chunks;
     int32_t* d_bucket_begin;
+    lsgd::CopyDesc* d_copy_desc;
     void** d_ptrs;
     // LARS: per-tensor scratch offsets and chunk ranges, and every buffer's
     // byte range (for the workspace aliasing check)
@@ -103,6 +104,7 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     memset(&a, 0, sizeof a);
     a.chunks = plan->d_chunks;
     a.bucket_begin = plan->d_bucket_begin;
+    a.copy_desc = plan->d_copy_desc;
     a.ptrs = plan->d_ptrs;
     a.stride = plan->stride;
     a.n_workers = plan->n_workers;
@@ -190,6 +192,7 @@ void free_plan(lsgd_plan* p) {
     if (!p) return;
     if (p->d_chunks) (void)hipFree(p->d_chunks);
     if (p->d_bucket_begin) (void)hipFree(p->d_bucket_begin);
+    if (p->d_copy_desc) (void)hipFree(p->d_copy_desc);
     if (p->d_ptrs) (void)hipFree(p->d_ptrs);
     if (p->d_gbar_off) (void)hipFree(p->d_gbar_off);
     if (p->d_tensor_chunks) (void)hipFree(p->d_tensor_chunks);
@@ -329,6 +332,15 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     if (e == hipSuccess)
         e = hipMemcpy(p->d_bucket_begin, bucket_begin.data(), bucket_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(p->d_ptrs, table.data(), table_bytes, hipMemcpyHostToDevice);
+    std::vector<CopyDesc> desc(static_cast<size_t>(std::max(p->n_buckets, 1)));
+    for (int32_t b = 0; b < p->n_buckets; ++b) {
+        const PlanChunk& ch = chunks[static_cast<size_t>(bucket_begin[b])];
+        desc[b] = CopyDesc{static_cast<const float*>(table[static_cast<size_t>(ch.tensor) * stride]), ch.tensor,
+                           bucket_begin[b + 1] - bucket_begin[b], ch.start, ch.len};
+    }
+    if (e == hipSuccess) e = hipMalloc(&p->d_copy_desc, desc.size() * sizeof(CopyDesc));
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_copy_desc, desc.data(), desc.size() * sizeof(CopyDesc), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMalloc(&p->d_gbar_off, gbar_off.size() * sizeof(int64_t));
     if (e == hipSuccess) e = hipMalloc(&p->d_lars_exclude, static_cast<size_t>(n_tensors));
     if (e == hipSuccess) {

@@ -20,11 +20,23 @@ struct PlanChunk {
     int64_t len;
 };
 
+// Per bucket, for the copy-out pass: its first piece (tensor, element range,
+// the tensor's params) and the bucket's piece count, so that a workgroup
+// finds its params address in one table read instead of three dependent ones.
+struct CopyDesc {
+    const float* p;
+    int32_t tensor;
+    int32_t n_chunks;
+    int64_t start;
+    int64_t len;
+};
+
 // Per tensor the device pointer table holds `stride` entries:
 // [p, m, grads in member order (N), replicas (R)].
 struct PlanArgs {
     const PlanChunk* chunks;
     const int32_t* bucket_begin;  // [n_buckets + 1]: workgroup b runs chunks [begin[b], begin[b+1])
+    const CopyDesc* copy_desc;    // [n_buckets]
     void* const* ptrs;
     int32_t stride, n_workers, n_groups, W;
     int32_t n_replicas, rdt;
@@ -126,6 +138,36 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
 // b copies bucket w*win_blocks + s to replica group q (RK consecutive
 // replicas), b = (w*ceil(R/RK) + q)*win_blocks + s; a lane loads U units of
 // p, then stores them to each replica of the group.
+// One piece [start, start+len) of a tensor to the nr replicas in dst.
+template <int VEC, int U, int RK>
+__device__ __forceinline__ void copy_out_piece(const float* p, void* const (&dst)[RK], int nr, int rdt,
+                                               int64_t start, int64_t len) {
+    const int64_t full = len / VEC;
+    for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
+        float x[U][VEC];
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+            const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
+            if (u < full) load_f32_cached<VEC, false>(p, start + u * VEC, VEC, x[i]);
+        }
+#pragma unroll
+        for (int k = 0; k < RK; ++k) {
+            if (k >= nr) break;
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
+                if (u < full) store_replica<VEC, false>(dst[k], rdt, start + u * VEC, VEC, x[i]);
+            }
+        }
+    }
+    const int rem = static_cast<int>(len - full * VEC);
+    if (rem != 0 && threadIdx.x == 0) {
+        float x[VEC];
+        load_f32_cached<VEC, true>(p, start + full * VEC, rem, x);
+        for (int k = 0; k < nr; ++k) store_replica<VEC, true>(dst[k], rdt, start + full * VEC, rem, x);
+    }
+}
+
 template <int VEC, int U, int RK>
 __device__ __forceinline__ void copy_out_plan_block(const PlanArgs& a, int64_t b) {
     const int n_rg = (a.n_replicas + RK - 1) / RK;
@@ -137,39 +179,24 @@ __device__ __forceinline__ void copy_out_plan_block(const PlanArgs& a, int64_t b
     if (bucket >= a.n_buckets) return;   // padding of the last window
     const int r0 = q * RK;
     const int nr = min(RK, a.n_replicas - r0);
-    const int32_t c_end = read_table(&a.bucket_begin[bucket + 1]);
-    for (int32_t c = read_table(&a.bucket_begin[bucket]); c < c_end; ++c) {
-        const PlanChunk* cp = &a.chunks[c];
-        const int64_t start = read_table(&cp->start), len = read_table(&cp->len);
-        void* const* t = a.ptrs + static_cast<int64_t>(read_table(&cp->tensor)) * a.stride;
-        const float* p = static_cast<const float*>(read_table(&t[0]));
+    const CopyDesc* d = &a.copy_desc[bucket];
+    if (read_table(&d->n_chunks) == 1) {   // one piece: its params address comes with it
+        void* const* t = a.ptrs + static_cast<int64_t>(read_table(&d->tensor)) * a.stride;
         void* dst[RK];
 #pragma unroll
         for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[2 + a.n_workers + r0 + k]) : nullptr;
-        const int64_t full = len / VEC;
-        for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
-            float x[U][VEC];
+        copy_out_piece<VEC, U, RK>(read_table(&d->p), dst, nr, a.rdt, read_table(&d->start), read_table(&d->len));
+        return;
+    }
+    const int32_t c_end = read_table(&a.bucket_begin[bucket + 1]);
+    for (int32_t c = read_table(&a.bucket_begin[bucket]); c < c_end; ++c) {
+        const PlanChunk* cp = &a.chunks[c];
+        void* const* t = a.ptrs + static_cast<int64_t>(read_table(&cp->tensor)) * a.stride;
+        void* dst[RK];
 #pragma unroll
-            for (int i = 0; i < U; ++i) {
-                const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
-                if (u < full) load_f32_cached<VEC, false>(p, start + u * VEC, VEC, x[i]);
-            }
-#pragma unroll
-            for (int k = 0; k < RK; ++k) {
-                if (k >= nr) break;
-#pragma unroll
-                for (int i = 0; i < U; ++i) {
-                    const int64_t u = t0 + static_cast<int64_t>(i) * kBlock;
-                    if (u < full) store_replica<VEC, false>(dst[k], a.rdt, start + u * VEC, VEC, x[i]);
-                }
-            }
-        }
-        const int rem = static_cast<int>(len - full * VEC);
-        if (rem != 0 && threadIdx.x == 0) {
-            float x[VEC];
-            load_f32_cached<VEC, true>(p, start + full * VEC, rem, x);
-            for (int k = 0; k < nr; ++k) store_replica<VEC, true>(dst[k], a.rdt, start + full * VEC, rem, x);
-        }
+        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[2 + a.n_workers + r0 + k]) : nullptr;
+        copy_out_piece<VEC, U, RK>(static_cast<const float*>(read_table(&t[0])), dst, nr, a.rdt,
+                                   read_table(&cp->start), read_table(&cp->len));
     }
 }
 
