@@ -391,7 +391,7 @@ def test_workload_full_size_sampled(name):
         torch.cuda.synchronize()
         assert_close(gather(params), p_ref, "%s params step %d" % (name, step))
         assert_close(gather(mom), m_ref, "%s momentum step %d" % (name, step))
-        for r in (0, R // 2, R - 1):
+        for r in range(R):   # every replica: the copy-out pass writes each from its own workgroups
             assert np.array_equal(gather(reps[r]), rr[r]), "%s replica %d step %d" % (name, r, step)
         if step % 10 == 0 or step == wl.steps - 1:
             log("  %s step %d ok (%d sampled elements)" % (name, step, idx.size))
