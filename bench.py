@@ -421,6 +421,74 @@ def cpu_baseline(setup, seconds):
                                                                           steps, el)}
 
 
+def host_threads():
+    """Host threads for the all-cores oracle run: the CPUs this process may use,
+    at most OMP_NUM_THREADS when that is set."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    return max(1, min(n, int(omp)) if omp.isdigit() and int(omp) > 0 else n)
+
+
+def cpu_baseline_all_cores(setup, seconds, max_bytes=2 << 30):
+    """The same oracle step on every host thread at once, each thread on its own
+    contiguous block of elements (ctypes releases the interpreter lock during
+    the C call), as many rounds as fit in `seconds`. The blocks together cover
+    the first elements of the inputs, up to `max_bytes` of host copies, so that
+    they do not fit in the host caches."""
+    import threading
+    import numpy as np
+    import torch
+    import oracle
+
+    wl, R = setup.wl, setup.R
+    T = host_threads()
+    host_bytes = wl.n_workers * wl.grad_bytes + 8 + R * (2 if wl.replica_dtype == "bf16" else 4)
+    S = int(min(wl.n, max(1 << 20, min(T << 20, max_bytes // host_bytes))))
+    S -= S % T
+    B = S // T
+    src = lambda t: t[0][:S].detach().cpu()
+    def host(t):
+        x = src(t)
+        return x.view(torch.int16).numpy().view(np.uint16).copy() if x.dtype == torch.bfloat16 else x.numpy().copy()
+    if setup.plan is not None:      # the leading elements of the flat concatenation
+        cat = lambda ts: [torch.cat([x.reshape(-1) for x in ts])]
+        p, m = host(cat(setup.params)), host(cat(setup.mom))
+        grads = [host(cat(g)) for g in setup.grads]
+    else:
+        p, m = host(setup.params), host(setup.mom)
+        grads = [host(g) for g in setup.grads]
+    rdt = oracle.BF16 if wl.replica_dtype == "bf16" else oracle.F32
+    reps = [np.zeros(S, np.uint16 if rdt == oracle.BF16 else np.float32) for _ in range(R)]
+    literal = setup.reduction == "literal" or setup.broadcast_grad
+
+    def block(k):
+        sl = slice(k * B, (k + 1) * B)
+        if literal:
+            oracle.lsgd_step_literal(p[sl], m[sl], [g[sl] for g in grads], setup.gow, wl.groups, wl.lr, wl.mu,
+                                     wl.wd, [r[sl] for r in reps], rdt, broadcast_grad=setup.broadcast_grad)
+        else:
+            oracle.lsgd_step(p[sl], m[sl], [g[sl] for g in grads], setup.gow, wl.groups, wl.lr, wl.mu, wl.wd,
+                             [r[sl] for r in reps], rdt)
+    rounds = 0
+    t0 = time.perf_counter()
+    while True:
+        th = [threading.Thread(target=block, args=(k,)) for k in range(T)]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join()
+        rounds += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    elem_per_s = S * rounds / el
+    per_elem = (wl.algorithmic_bytes(R) / wl.n + (4 * wl.n_workers if setup.broadcast_grad else 0))
+    return {"value": round(elem_per_s * per_elem / 1e9, 4), "unit": "GB/s", "cores": T, "kind": "oracle",
+            "steps_per_s": round(elem_per_s / wl.n, 6),
+            "sample": "first %d of %d elements in %d blocks of %d, one per host thread, all %d worker gradients "
+                      "and %d replicas, %d rounds in %.1f s" % (S, wl.n, T, B, wl.n_workers, R, rounds, el)}
+
+
 def cpu_baseline_unfused(setup, seconds):
     """The oracle's three unfused steps (group means, global mean, update and
     copy-out) on the first 2^20 elements, one host thread, scaled by the
@@ -811,6 +879,8 @@ def main(argv=None):
             setup.R = R
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(setup, args.cpu_seconds)
+        if not args.lars:
+            result["cpu_baseline_all_cores"] = cpu_baseline_all_cores(setup, args.cpu_seconds)
     setup.close()
     print(json.dumps(result), flush=True)
 

@@ -91,3 +91,35 @@ def test_derive_traffic_per_kernel_with_a_copy_out_pass(tmp_path, monkeypatch):
     assert bench.stored_traffic(wl, R, False, "copy_out_rmajor_kernel") == k["copy_out"]["traffic_bytes"]
     assert bench.stored_traffic(wl, R, False, "step_flat_ct") == k["step_flat_ct"]["traffic_bytes"]
     assert bench.stored_traffic(wl, R) == out["traffic_bytes"]
+
+
+def test_all_cores_cpu_baseline_runs_the_oracle_on_blocks(monkeypatch):
+    """The all-cores baseline on host tensors of the tiny workload: one block per
+    host thread, the result fields, and (separately) that stepping the oracle
+    block by block gives the bits of one call over the whole range."""
+    import types
+    import numpy as np
+    import torch
+    import oracle
+    wl = workloads.WORKLOADS["tiny"]
+    monkeypatch.setenv("OMP_NUM_THREADS", "3")
+    gen = torch.Generator().manual_seed(5)
+    st = types.SimpleNamespace(
+        wl=wl, R=2, plan=None, reduction="mean_of_means", broadcast_grad=False, gow=wl.group_of_worker(),
+        params=[torch.randn(wl.n, generator=gen)], mom=[torch.zeros(wl.n)],
+        grads=[[torch.randn(wl.n, generator=gen) * 1e-2] for _ in range(wl.n_workers)])
+    out = bench.cpu_baseline_all_cores(st, 0.05)
+    assert out["cores"] == min(3, bench.host_threads()) and out["value"] > 0 and out["kind"] == "oracle"
+    # element blocks are independent: blockwise steps equal one whole step, bit for bit
+    rng = np.random.default_rng(3)
+    n, T = 10_007, 4
+    p0 = rng.standard_normal(n).astype(np.float32)
+    gs = [rng.standard_normal(n).astype(np.float32) * 1e-2 for _ in range(4)]
+    pa, ma, ra = p0.copy(), np.zeros(n, np.float32), [np.zeros(n, np.float32)]
+    oracle.lsgd_step(pa, ma, gs, [0, 0, 1, 1], 2, 0.1, 0.9, 1e-4, ra)
+    pb, mb, rb = p0.copy(), np.zeros(n, np.float32), [np.zeros(n, np.float32)]
+    B = -(-n // T)
+    for k in range(T):
+        sl = slice(k * B, min(n, (k + 1) * B))
+        oracle.lsgd_step(pb[sl], mb[sl], [g[sl] for g in gs], [0, 0, 1, 1], 2, 0.1, 0.9, 1e-4, [rb[0][sl]])
+    assert pa.tobytes() == pb.tobytes() and ma.tobytes() == mb.tobytes() and ra[0].tobytes() == rb[0].tobytes()
