@@ -24,14 +24,13 @@ struct FlatPick {
 // Both give the same bits.
 template <typename GT, int W>
 FlatKernel pick_flat_g(int G) {
-    constexpr int U = TileUnits<GT>::U;
     switch (G) {
-        case 1: return step_flat_ct<GT, W, 1, U>;
-        case 2: return step_flat_ct<GT, W, 2, U>;
-        case 4: return step_flat_ct<GT, W, 4, U>;
-        case 8: return step_flat_ct<GT, W, 8, U>;
+        case 1: return step_flat_ct<GT, W, 1, tile_units<GT>(W)>;
+        case 2: return step_flat_ct<GT, W, 2, tile_units<GT>(W * 2)>;
+        case 4: return step_flat_ct<GT, W, 4, tile_units<GT>(W * 4)>;
+        case 8: return step_flat_ct<GT, W, 8, tile_units<GT>(W * 8)>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16, U>;
+            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16, tile_units<GT>(W * 16)>;
             else return nullptr;
     }
     return nullptr;
@@ -47,7 +46,7 @@ FlatPick pick_flat(int W, int G) {
         case 8: k = pick_flat_g<GT, 8>(G); break;
         case 16: k = pick_flat_g<GT, 16>(G); break;
     }
-    if (k) return FlatPick{k, TileUnits<GT>::U};
+    if (k) return FlatPick{k, tile_units<GT>(W * G)};
     return FlatPick{nullptr, 1};
 }
 
@@ -68,7 +67,7 @@ struct MeanPick {
 // Group means: compile-time W for powers of two up to 16, else runtime W.
 template <typename GT>
 MeanPick pick_group_mean(int W) {
-    constexpr int U = TileUnits<GT>::U;
+    constexpr int U = sizeof(GT) == 4 ? 2 : 1;   // W gradients per tile: the unrolled form up to 16
     switch (W) {
         case 1: return MeanPick{group_mean_kernel_ct<GT, 1, U>, U};
         case 2: return MeanPick{group_mean_kernel_ct<GT, 2, U>, U};

@@ -502,12 +502,6 @@ struct MeanArgs {
 
 // ------------------------------------------------------------- per-unit bodies
 
-// Units per lane tile in the compile-time fused kernels (measured: two fp32
-// units per lane, visited stream-major, beat one; bf16 tiles stay at one unit
-// to bound registers).
-template <typename GT> struct TileUnits;
-template <> struct TileUnits<float> { static constexpr int U = 2; };
-template <> struct TileUnits<uint16_t> { static constexpr int U = 1; };
 
 // Units per lane tile in the flat runtime-layout (segmented) kernel
 // (measured: two binary32 units per lane, stream-major, +2-5% over one on
@@ -524,6 +518,18 @@ template <> struct SegTileUnits<uint16_t> { static constexpr int U = 1; };
 // occupancy) for the 64- and 128-worker groupings.
 constexpr int kUnrollFloats = 128;
 constexpr int kStreamFloats = 64;
+
+// Units per lane tile in the compile-time fused kernels for N = W*G
+// gradients. Binary32: two units (visited stream-major; measured +6-8% over
+// one) while the whole tree fits the unrolled form (N <= 16), four once the
+// groups stream through the accumulator (N >= 32: +3-8% over two at 8x4,
+// 4x8, 8x8, 16x4, 2x16 and 16x8, in same-process A/Bs; at N <= 16 three or
+// four units lose 1-3%, since they leave the unrolled form). bfloat16 tiles
+// stay at one unit (two lost 17% at 8x8).
+template <typename GT>
+constexpr int tile_units(int n_workers) {
+    return sizeof(GT) == 4 ? (n_workers * 2 * Unit<GT>::VEC <= kUnrollFloats ? 2 : 4) : 1;
+}
 
 // Pairwise sum of K leaves (compile-time K, a power of two) of T floats each:
 // unrolled while K * LW floats (LW = floats a leaf loads) stay within

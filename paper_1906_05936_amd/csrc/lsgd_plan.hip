@@ -65,12 +65,12 @@ static_assert(piece_elems<float>(1) % 8 == 0 && piece_elems<uint16_t>(1) % 8 == 
 template <typename GT, int W>
 PlanKernel pick_plan_g(int G) {
     switch (G) {
-        case 1: return step_plan_kernel<GT, W, 1, TileUnits<GT>::U>;
-        case 2: return step_plan_kernel<GT, W, 2, TileUnits<GT>::U>;
-        case 4: return step_plan_kernel<GT, W, 4, TileUnits<GT>::U>;
-        case 8: return step_plan_kernel<GT, W, 8, TileUnits<GT>::U>;
+        case 1: return step_plan_kernel<GT, W, 1, tile_units<GT>(W)>;
+        case 2: return step_plan_kernel<GT, W, 2, tile_units<GT>(W * 2)>;
+        case 4: return step_plan_kernel<GT, W, 4, tile_units<GT>(W * 4)>;
+        case 8: return step_plan_kernel<GT, W, 8, tile_units<GT>(W * 8)>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16, TileUnits<GT>::U>;
+            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16, tile_units<GT>(W * 16)>;
             else return nullptr;
     }
     return nullptr;
@@ -86,7 +86,7 @@ PlanPick pick_plan(int W, int G) {
         case 8: k = pick_plan_g<GT, 8>(G); break;
         case 16: k = pick_plan_g<GT, 16>(G); break;
     }
-    if (k) return PlanPick{k, TileUnits<GT>::U};
+    if (k) return PlanPick{k, tile_units<GT>(W * G)};
     return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>,
                     SegTileUnits<GT>::U};
 }
@@ -144,14 +144,13 @@ lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t
 // LARS pass-1 kernels: compile-time (W, G) as for the step, else segmented.
 template <typename GT, int W>
 LarsKernel pick_lars_g(int G) {
-    constexpr int U = TileUnits<GT>::U;
     switch (G) {
-        case 1: return lars_norms_kernel<GT, W, 1, U>;
-        case 2: return lars_norms_kernel<GT, W, 2, U>;
-        case 4: return lars_norms_kernel<GT, W, 4, U>;
-        case 8: return lars_norms_kernel<GT, W, 8, U>;
+        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W)>;
+        case 2: return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2)>;
+        case 4: return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4)>;
+        case 8: return lars_norms_kernel<GT, W, 8, tile_units<GT>(W * 8)>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, U>;
+            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, tile_units<GT>(W * 16)>;
             else return nullptr;
     }
     return nullptr;

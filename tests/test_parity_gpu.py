@@ -907,7 +907,8 @@ def test_vector_longer_than_2_to_31_elements():
 TAIL_SIZES = list(range(1, 68)) + [2 ** k + d for k in (7, 10, 11, 12, 13, 17) for d in (-1, 1)]
 
 
-@pytest.mark.parametrize("gdt,G,W,R,rdt", [("f32", 2, 2, 1, "f32"), ("bf16", 4, 4, 2, "bf16"), ("f32", 3, 5, 1, "f32")])
+@pytest.mark.parametrize("gdt,G,W,R,rdt", [("f32", 2, 2, 1, "f32"), ("bf16", 4, 4, 2, "bf16"), ("f32", 3, 5, 1, "f32"),
+                                           ("f32", 8, 4, 2, "f32")])
 def test_every_tail_size_flat(gdt, G, W, R, rdt):
     """n = 1..67 and 2^k +- 1: every ragged end of the 4- and 8-element units,
     flat step bit-exact against the oracle."""
@@ -930,13 +931,12 @@ def test_every_tail_size_flat(gdt, G, W, R, rdt):
             assert np.array_equal(to_host(reps[r]), rr[r]), (n, r)
 
 
-@pytest.mark.parametrize("gdt", ["f32", "bf16"])
-def test_every_tail_size_as_plan_tensors(gdt):
+@pytest.mark.parametrize("gdt,G,W", [("f32", 2, 4), ("bf16", 2, 4), ("f32", 8, 4)])
+def test_every_tail_size_as_plan_tensors(gdt, G, W):
     """The same sizes as the tensors of one plan (many small tensors share a
     bucket): plain step, then a LARS step, each tensor bit-exact against the
-    oracle."""
+    oracle (8x4 binary32: four-unit tiles and 4096-element pieces)."""
     rng = np.random.default_rng(68)
-    G, W = 2, 4
     N = G * W
     gow = groups_for(G, W, "shuffled", seed=4)
     sizes = TAIL_SIZES
