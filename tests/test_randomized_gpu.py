@@ -20,7 +20,7 @@ else:  # collected but skipped on machines without a GPU
     lsgd = None
 
 DEV = torch.device("cuda:0")
-N_CASES = 48
+N_CASES = 96
 
 
 def log(msg):
