@@ -61,6 +61,10 @@ def parse_args(argv=None):
     ap.add_argument("--tensor-layout", choices=("separate", "arena"), default="separate",
                     help="multi-tensor workloads: every tensor its own allocation, or each worker's (and "
                          "replica's, p's, m's) tensors as views into one allocation")
+    ap.add_argument("--lr-schedule", action="store_true",
+                    help="each step reads its rate from device memory, after the device schedule step")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time its replays")
     ap.add_argument("--copy-out", choices=("auto", "fused", "separate"), default="auto",
                     help="replicas written inside the step kernel or by a copy-out pass of their own")
     ap.add_argument("--broadcast-grad", action="store_true",
@@ -80,7 +84,7 @@ class Setup:
     """Device buffers of one workload and a zero-overhead step callable."""
 
     def __init__(self, wl, R, dev, reduction=None, broadcast_grad=False, lars=False, trust_coef=1e-3,
-                 lars_exclude=None, tensor_layout="separate", copy_out="auto"):
+                 lars_exclude=None, tensor_layout="separate", copy_out="auto", lr_schedule=False):
         import torch
         import paper_1906_05936_amd as lsgd
         import workloads
@@ -98,6 +102,19 @@ class Setup:
             raise SystemExit("--lars needs a workload with per-tensor sizes (a plan)")
         self.lars, self.trust_coef, self.lars_exclude = lars, trust_coef, lars_exclude
         rtd = torch.bfloat16 if wl.replica_dtype == "bf16" else torch.float32
+        # --lr-schedule: the rate comes from device memory, written by the
+        # device schedule step that precedes every step (Sec. 5.3's schedule)
+        lr_ptr = None
+        if lr_schedule:
+            self._sched = lsgd.lr_schedule(wl.lr, 256.0, 256.0, warmup_iters=50, decay_iters=1000)
+            self._iteration = torch.zeros(1, dtype=torch.int64, device=dev)
+            self._lr = torch.zeros(1, dtype=torch.float32, device=dev)
+            lr_ptr = ctypes.c_void_p(self._lr.data_ptr())
+            sched_args = (ctypes.byref(self._sched), ctypes.c_void_p(self._iteration.data_ptr()), lr_ptr,
+                          ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
+
+            def sched():
+                check(lib.lsgd_lr_schedule_step(*sched_args))
         stream = torch.cuda.current_stream(dev)
         flat_p = workloads.init_params(wl, dev)
         scratch = torch.empty(wl.n, device=dev) if wl.grad_dtype == "bf16" else None
@@ -136,10 +153,16 @@ class Setup:
                 self.workspace = torch.empty(self.plan.lars_workspace_size(), dtype=torch.uint8, device=dev)
                 fn = lib.lsgd_lars_step_plan
                 extra = (ctypes.c_float(trust_coef), ctypes.c_void_p(self.workspace.data_ptr()),
-                         ctypes.c_size_t(self.workspace.numel()), None, None)
+                         ctypes.c_size_t(self.workspace.numel()), None, lr_ptr)
 
                 def step():
                     check(fn(h, *hyper, *extra, s))
+            elif lr_schedule:
+                self._opts = StepOptions(0, 0, lr_ptr)
+                opts = ctypes.byref(self._opts)
+
+                def step():
+                    check(lib.lsgd_step_plan_ex(h, *hyper, opts, s))
             else:
                 fn = lib.lsgd_step_plan
 
@@ -175,18 +198,18 @@ class Setup:
                       ctypes.c_float(wl.lr), ctypes.c_float(wl.mu), ctypes.c_float(wl.wd),
                       ptr_array([r[0].data_ptr() for r in self.reps]), R,
                       1 if rtd == torch.bfloat16 else 0)
-            if reduction == "mean_of_means" and not broadcast_grad:
+            if reduction == "mean_of_means" and not broadcast_grad and not lr_schedule:
                 fn = lib.lsgd_step
                 args = common + (ctypes.c_void_p(stream.cuda_stream),)
             else:
                 self._opts = StepOptions(1 if reduction == "literal" else 0, 1 if broadcast_grad else 0,
-                                         None)
+                                         lr_ptr)
                 fn = lib.lsgd_step_ex
                 args = common + (ctypes.byref(self._opts), ctypes.c_void_p(stream.cuda_stream))
 
             def step():
                 check(fn(*args))
-            if R and separate_copy_out(wl, R, copy_out):
+            if R and separate_copy_out(wl, R, copy_out) and not lr_schedule:
                 # the same two kernels launched one at a time: the step without
                 # replicas on the same buffers, then the copy-out pass
                 args0 = args[:11] + (None, 0) + args[13:]
@@ -201,6 +224,12 @@ class Setup:
                 self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes()),
                               ("copy_out_rmajor_kernel", copy_part, self._copy_bytes())]
         del scratch
+        if lr_schedule:
+            inner = step
+
+            def step():
+                sched()
+                inner()
         self.step = step
         self.stream = stream
 
@@ -241,6 +270,33 @@ def time_steps(setup, steps, warmup, fn=None):
     t1.synchronize()
     torch.cuda.synchronize()
     return t0.elapsed_time(t1) / steps
+
+
+def whole_step_label(wl, R, setup, args):
+    """The kernels of one step, for a roofline line taken over the whole step."""
+    names = [kernel_match(wl, setup.reduction, args.lars)]
+    if args.lars:
+        names += ["lars_trust_kernel", "lars_update_kernel"]
+    if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars else separate_copy_out(wl, R, args.copy_out)):
+        names.append("copy_out")
+    if args.lr_schedule:
+        names.insert(0, "schedule_step_kernel")
+    return " + ".join(names) + (" (whole step)" if len(names) > 1 else "")
+
+
+def captured(setup):
+    """One step captured in a HIP graph on the setup's stream (not executed by
+    the capture); returns the replay callable. The library records kernel
+    launches only (no memsets), so every replay repeats the eager step."""
+    import torch
+    setup.step()                      # an eager step first: nothing lazy happens inside the capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=setup.stream):
+        setup.step()
+    torch.cuda.synchronize()
+    setup._graph = graph
+    return graph.replay
 
 
 def time_parts(setup, steps, warmup):
@@ -816,11 +872,15 @@ def main(argv=None):
         if wl.tensor_sizes != tuple(workloads.resnet50_param_sizes()):
             raise SystemExit("--lars-exclude-vectors knows the ResNet-50 tensor list only")
         lars_excl = workloads.resnet50_vector_params()
+    if args.graph:   # steps launch on a side stream that can be captured
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        torch.cuda.set_stream(side)
     setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
-                  args.tensor_layout, args.copy_out)
-    ms = time_steps(setup, args.steps, args.warmup)
+                  args.tensor_layout, args.copy_out, args.lr_schedule)
+    ms = time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None)
     kernels = []
-    if setup.parts:   # two kernels per step: the step again, an event between its kernels
+    if setup.parts and not args.graph:   # two kernels per step: the step again, an event between its kernels
         for (name, _, nbytes), kms in zip(setup.parts, time_parts(setup, args.steps, args.warmup)):
             kg = nbytes / (kms * 1e-3) / 1e9
             kernels.append({"kernel": name, "ms": round(kms, 6), "algorithmic_bytes": nbytes,
@@ -845,15 +905,14 @@ def main(argv=None):
                        "lars_excluded_tensors": sum(lars_excl) if lars_excl else 0} if args.lars else {}),
                    "copy_out": ("separate pass" if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
                                                      else separate_copy_out(wl, R, args.copy_out))
-                                else "in the step kernel")},
+                                else "in the step kernel"),
+                   **({"lr": "device schedule step before every step"} if args.lr_schedule else {}),
+                   **({"launch": "HIP graph replay"} if args.graph else {})},
         "steps_per_s": round(1e3 / ms, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": alg,
-                     "kernel": kernel_match(wl, setup.reduction, args.lars)
-                               + (" + lars_trust_kernel + lars_update_kernel" if args.lars else "")
-                               + (" + copy_out" if args.lars and lars_separate_copy_out(wl, R, args.copy_out) else "")
-                               + (" (whole step)" if args.lars else "")},
+                     "kernel": whole_step_label(wl, R, setup, args)},
         "copy_ceiling_GBps": round(ceiling, 1),
     }
     if kernels:
@@ -869,8 +928,8 @@ def main(argv=None):
         del setup
         torch.cuda.empty_cache()
         setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
-                      args.tensor_layout)
-        ms0 = time_steps(setup, args.steps, args.warmup)
+                      args.tensor_layout, args.copy_out, args.lr_schedule)
+        ms0 = time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None)
         alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
                         "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),
