@@ -813,6 +813,8 @@ def main(argv=None):
               "GPU's HBM (one GPU's share of the aggregation); runs on %d GPUs are not part of "
               "this build." % max(args.gpus, world), file=sys.stderr)
         sys.exit(2)
+    if args.path == "unfused" and (args.graph or args.lr_schedule or args.lars):
+        raise SystemExit("--graph, --lr-schedule and --lars apply to the fused path")
     if args.derive_traffic:
         derive_traffic(args)
         return

@@ -29,6 +29,13 @@ def _write_rows(path, counter, rows):
                         "Counter_Value": value})
 
 
+def test_unfused_path_rejects_fused_only_options():
+    for opt in ("--graph", "--lr-schedule", "--lars"):
+        r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--path", "unfused", opt],
+                           capture_output=True, text=True, timeout=120)
+        assert r.returncode != 0 and "fused path" in r.stderr, (opt, r.stderr)
+
+
 def test_derive_traffic_scales_by_the_calibration_copy(tmp_path, monkeypatch):
     """Synthetic counter rows: the 1 GiB copy reads FETCH_SIZE = half its bytes
     and WRITE_SIZE = all of them, so the step's rows are scaled by 2 and 1;
