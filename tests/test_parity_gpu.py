@@ -964,4 +964,11 @@ def test_every_tail_size_as_plan_tensors(gdt, G, W):
         assert np.float32(tg[t]) == np.float32(tr), (s, tg[t], tr)
         assert_close(to_host(params[t]), ph[t], "LARS params size %d" % s)
         assert_close(to_host(mom[t]), mh[t], "LARS momentum size %d" % s)
+    # the plan's copy-out pass on its own over every tail size (shared buckets too)
+    for x in reps[0]:
+        x.fill_(3)
+    plan.copy_out()
+    torch.cuda.synchronize()
+    for t, s in enumerate(sizes):
+        assert torch.equal(reps[0][t], params[t]), ("copy_out", s)
     plan.close()
