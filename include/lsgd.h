@@ -294,7 +294,8 @@ LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int
  * (e.g. the 161 tensors of ResNet-50, the model of Sec. 5.3) in ONE kernel
  * launch. The plan copies a chunk table and a pointer table to device memory
  * once; lsgd_step_plan then launches one kernel. Tensors are cut into pieces
- * of 2048 elements (times the launch shape's units_per_lane at creation);
+ * of 2048 elements (4096 for binary32 gradients with more than 16 workers in
+ * power-of-two groups; times the launch shape's units_per_lane at creation);
  * small tensors are bucketed so that one workgroup covers several of them.
  *   numel     [n_tensors] host int64, elements of each tensor (>= 0).
  *   params, momentum [n_tensors] device pointers (binary32).
