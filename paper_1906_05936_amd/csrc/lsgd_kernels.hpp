@@ -586,15 +586,33 @@ __device__ __forceinline__ void load_state(const Src& s, const int64_t (&e0)[U],
     for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
 }
 
-// Parameters, momentum and replicas stored.
+// Parameters and momentum of the compile-time fused kernels go through the
+// caches (write-back) for up to 16 gradient buffers and nontemporally above.
+// Measured in the same process with the Infinity Cache flushed before every
+// step (so that no step reads what the previous one left there): 2x2 +12%,
+// 4x4 +1-2.5%, 8x2 +1%; 4x8 -0.6%, 8x8 -2%, 16x8 -3%, 8x8 bfloat16 -5%.
+// The choice is made at compile time where it can be: a runtime branch
+// between the two store forms cost the 64- and 128-buffer kernels 2-3%.
+__host__ __device__ constexpr bool cached_state_for(int n_workers) { return n_workers <= 16; }
+
+// Parameters, momentum and replicas stored. Parameters and momentum go
+// through the caches (write-back) when s.cached_state() is set, else with
+// nontemporal stores.
 template <int VEC, int U, bool TAIL, typename Src>
 __device__ __forceinline__ void store_state(const Src& s, const int64_t (&e0)[U], int cnt,
                                             const float (&p)[U * VEC], const float (&m)[U * VEC]) {
     constexpr int T = U * VEC;
+    if (s.cached_state()) {
 #pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+        for (int q = 0; q < U; ++q) store_f32_cached<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
 #pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+        for (int q = 0; q < U; ++q) store_f32_cached<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    }
     const int R = s.n_replicas();
     const int rdt = s.rdt();
     for (int r = 0; r < R; ++r) {
@@ -726,7 +744,10 @@ __device__ __forceinline__ void fused_unit_seg(const Src& s, int N, int G, const
 }
 
 // Pointer source for the planless fused step: everything from StepArgs.
-struct FlatSrc {
+// CACHED: store parameters and momentum through the caches (1) or
+// nontemporally (0).
+template <int CACHED>
+struct FlatSrcT {
     const StepArgs& a;
     Hyper h;
     __device__ const void* grad(int k) const { return a.grads[k]; }
@@ -738,6 +759,7 @@ struct FlatSrc {
     __device__ Hyper hyper() const { return h; }
     __device__ int bcast_grad() const { return a.bcast_grad; }
     __device__ int n_workers() const { return a.n_workers; }
+    __device__ int cached_state() const { return CACHED; }
 };
 
 // ------------------------------------------------------------- flat kernels
@@ -749,7 +771,7 @@ struct FlatSrc {
 template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
+    const FlatSrcT<cached_state_for(W * G) ? 1 : 0> s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     for_tiles<U, VEC>(
@@ -767,7 +789,7 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
 template <typename GT, int LV, int U>
 __global__ __launch_bounds__(kBlock) void step_flat_seg(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrc s{a, resolve_hyper(a.h, a.lr_ptr)};
+    const FlatSrcT<0> s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     const bool literal = a.literal != 0;

@@ -108,6 +108,7 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     a.ptrs = plan->d_ptrs;
     a.stride = plan->stride;
     a.n_workers = plan->n_workers;
+    a.cached_state = cached_state_for(plan->n_workers) ? 1 : 0;   // read by the LARS update
     a.n_groups = plan->n_groups;
     a.W = plan->W;
     a.n_replicas = plan->n_replicas;

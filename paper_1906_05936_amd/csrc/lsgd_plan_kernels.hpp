@@ -48,10 +48,13 @@ struct PlanArgs {
     int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
     int32_t win_blocks;    // replica-major copy-out: buckets per window (a multiple of 8)
     int64_t copy_blocks;   // replica-major copy-out: logical workgroups (the grid strides over them)
+    int32_t cached_state;  // LARS update: store parameters and momentum through the caches
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
 };
 
-struct PlanSrc {
+// CACHED as for FlatSrcT (-1: PlanArgs::cached_state decides).
+template <int CACHED>
+struct PlanSrcT {
     void* const* t;  // this tensor's row of the pointer table
     const PlanArgs& a;
     Hyper h;
@@ -64,12 +67,14 @@ struct PlanSrc {
     __device__ Hyper hyper() const { return h; }
     __device__ int bcast_grad() const { return a.bcast_grad; }
     __device__ int n_workers() const { return a.n_workers; }
+    __device__ int cached_state() const { return CACHED < 0 ? a.cached_state : CACHED; }
 };
+using PlanSrc = PlanSrcT<-1>;
 
 // One workgroup per bucket (in XCD-chunked order); a bucket is a run of chunks
 // (one large piece, or several small tensors). Chunk and pointer-table reads
 // are uniform per workgroup. chunk(s, ch, c) processes chunk c.
-template <typename ChunkFn>
+template <int CACHED = -1, typename ChunkFn>
 __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn& chunk) {
     const uint32_t b = logical_block(blockIdx.x, a.xcd_chunk);
     if (b >= static_cast<uint32_t>(a.n_buckets)) return;   // padding of the chunked grid
@@ -78,7 +83,7 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
     for (int32_t c = read_table(&a.bucket_begin[b]); c < c_end; ++c) {
         const PlanChunk* cp = &a.chunks[c];
         const PlanChunk ch{read_table(&cp->tensor), 0, read_table(&cp->start), read_table(&cp->len)};
-        const PlanSrc s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
+        const PlanSrcT<CACHED> s{a.ptrs + static_cast<int64_t>(ch.tensor) * a.stride, a, h};
         chunk(s, ch, c);
     }
 }
@@ -88,7 +93,7 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
 template <typename GT, int W, int G, int U>
 __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+    for_plan_chunks<cached_state_for(W * G) ? 1 : 0>(a, [&](const auto& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
             if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
@@ -114,7 +119,7 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     constexpr int U = SegTileUnits<GT>::U;
     const bool literal = a.literal != 0;
     auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
-    for_plan_chunks(a, [&](const PlanSrc& s, const PlanChunk& ch, int32_t) {
+    for_plan_chunks<0>(a, [&](const PlanSrcT<0>& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
             if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
