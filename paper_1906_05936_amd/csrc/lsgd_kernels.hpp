@@ -576,21 +576,33 @@ __device__ __forceinline__ void broadcast_mean(const Src& s, const int64_t (&e0)
     }
 }
 
+// Parameters and momentum loaded, through the caches where they will be
+// stored through them (s.cached_state(); see store_state), else
+// nontemporally.
 template <int VEC, int U, bool TAIL, typename Src>
 __device__ __forceinline__ void load_state(const Src& s, const int64_t (&e0)[U], int cnt,
                                            float (&p)[U * VEC], float (&m)[U * VEC]) {
     constexpr int T = U * VEC;
+    if (s.cached_state()) {
 #pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+        for (int q = 0; q < U; ++q) load_f32_cached<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
 #pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+        for (int q = 0; q < U; ++q) load_f32_cached<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.p(), e0[q], cnt, slice<VEC, T>(p, q));
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_f32<VEC, TAIL>(s.m(), e0[q], cnt, slice<VEC, T>(m, q));
+    }
 }
 
 // Parameters and momentum of the compile-time fused kernels go through the
 // caches (write-back) for up to 16 gradient buffers and nontemporally above.
 // Measured in the same process with the Infinity Cache flushed before every
-// step (so that no step reads what the previous one left there): 2x2 +12%,
-// 4x4 +1-2.5%, 8x2 +1%; 4x8 -0.6%, 8x8 -2%, 16x8 -3%, 8x8 bfloat16 -5%.
+// step (so that no step reads what the previous one left there): cached
+// stores 2x2 +12%, 4x4 +1-5%, 8x2 +1%; 4x8 -0.6%, 8x8 -2%, 16x8 -3%, 8x8
+// bfloat16 -5%; cached loads of the same lines on top of them another
+// +3.5-6% (2x2, 4x4, 8x2).
 // The choice is made at compile time where it can be: a runtime branch
 // between the two store forms cost the 64- and 128-buffer kernels 2-3%.
 __host__ __device__ constexpr bool cached_state_for(int n_workers) { return n_workers <= 16; }
