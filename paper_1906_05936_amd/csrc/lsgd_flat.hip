@@ -22,29 +22,39 @@ struct FlatPick {
 // Compile-time (W, G) kernels for power-of-two counts up to 16 each (and
 // N <= 128); every other grouping takes the segmented runtime-layout kernel.
 // Both give the same bits.
+// The compile-time kernel for (W, G), with parameters and momentum through
+// the caches when `cached` (instantiated only where cached_state_for holds).
+template <typename GT, int W, int G>
+FlatKernel flat_ct(bool cached) {
+    constexpr int U = tile_units<GT>(W * G);
+    if constexpr (cached_state_for(W * G))
+        if (cached) return step_flat_ct<GT, W, G, U, 1>;
+    return step_flat_ct<GT, W, G, U, 0>;
+}
+
 template <typename GT, int W>
-FlatKernel pick_flat_g(int G) {
+FlatKernel pick_flat_g(int G, bool cached) {
     switch (G) {
-        case 1: return step_flat_ct<GT, W, 1, tile_units<GT>(W)>;
-        case 2: return step_flat_ct<GT, W, 2, tile_units<GT>(W * 2)>;
-        case 4: return step_flat_ct<GT, W, 4, tile_units<GT>(W * 4)>;
-        case 8: return step_flat_ct<GT, W, 8, tile_units<GT>(W * 8)>;
+        case 1: return flat_ct<GT, W, 1>(cached);
+        case 2: return flat_ct<GT, W, 2>(cached);
+        case 4: return flat_ct<GT, W, 4>(cached);
+        case 8: return flat_ct<GT, W, 8>(cached);
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_flat_ct<GT, W, 16, tile_units<GT>(W * 16)>;
+            if constexpr (W * 16 <= kMaxWorkers) return flat_ct<GT, W, 16>(cached);
             else return nullptr;
     }
     return nullptr;
 }
 
 template <typename GT>
-FlatPick pick_flat(int W, int G) {
+FlatPick pick_flat(int W, int G, bool cached) {
     FlatKernel k = nullptr;
     switch (W) {
-        case 1: k = pick_flat_g<GT, 1>(G); break;
-        case 2: k = pick_flat_g<GT, 2>(G); break;
-        case 4: k = pick_flat_g<GT, 4>(G); break;
-        case 8: k = pick_flat_g<GT, 8>(G); break;
-        case 16: k = pick_flat_g<GT, 16>(G); break;
+        case 1: k = pick_flat_g<GT, 1>(G, cached); break;
+        case 2: k = pick_flat_g<GT, 2>(G, cached); break;
+        case 4: k = pick_flat_g<GT, 4>(G, cached); break;
+        case 8: k = pick_flat_g<GT, 8>(G, cached); break;
+        case 16: k = pick_flat_g<GT, 16>(G, cached); break;
     }
     if (k) return FlatPick{k, tile_units<GT>(W * G)};
     return FlatPick{nullptr, 1};
@@ -237,7 +247,9 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
     FlatPick k{nullptr, 1};
-    if (!literal) k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups) : pick_flat<float>(a.W, n_groups);
+    const bool cached = use_cached_state(n_workers, n);
+    if (!literal)
+        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups, cached) : pick_flat<float>(a.W, n_groups, cached);
     if (!k.kernel) {
         // runtime layout: group j is members [start[j], start[j+1]) of the member order
         int32_t max_count = n_groups;
@@ -368,8 +380,8 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     a.upl = ls.upl;
     const bool split = separate_copy_out_update(n_replicas, dtype_size(rdt));
     if (split) a.n_replicas = 0;
-    hipLaunchKernelGGL(sgd_kernel<kSgdTile>, dim3(ls.blocks), dim3(kBlock), 0,
-                       static_cast<hipStream_t>(stream), a);
+    const FlatKernel sk = use_cached_state(1, n) ? sgd_kernel<kSgdTile, 1> : sgd_kernel<kSgdTile, 0>;
+    hipLaunchKernelGGL(sk, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     if ((st = check_launch("lsgd_sgd_step")) != LSGD_OK || !split) return st;
     a.n_replicas = n_replicas;
     return launch_copy_out(a, stream);

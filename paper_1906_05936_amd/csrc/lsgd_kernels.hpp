@@ -596,16 +596,25 @@ __device__ __forceinline__ void load_state(const Src& s, const int64_t (&e0)[U],
     }
 }
 
-// Parameters and momentum of the compile-time fused kernels go through the
-// caches (write-back) for up to 16 gradient buffers and nontemporally above.
-// Measured in the same process with the Infinity Cache flushed before every
-// step (so that no step reads what the previous one left there): cached
-// stores 2x2 +12%, 4x4 +1-5%, 8x2 +1%; 4x8 -0.6%, 8x8 -2%, 16x8 -3%, 8x8
-// bfloat16 -5%; cached loads of the same lines on top of them another
-// +3.5-6% (2x2, 4x4, 8x2).
-// The choice is made at compile time where it can be: a runtime branch
-// between the two store forms cost the 64- and 128-buffer kernels 2-3%.
+// Parameters and momentum of the compile-time fused kernels and of the
+// update kernel go through the caches (write-back) when there are at most 16
+// gradient buffers and parameters plus momentum fit the Infinity Cache
+// (kCachedStateBytes), nontemporally otherwise. Measured in the same process
+// with the Infinity Cache flushed before every step (so that no step reads
+// what the previous one left there), cached loads and stores against
+// nontemporal ones: 4x4 +4% at n = 1.2e7, +7% at 2.6e7, +5% at 3e7, +3% at
+// 3.5e7, +0.6% at 4e7, -1% at 5e7, -4% at 1e8 and 2e8; 2x2 +12-14% up to
+// 3.5e7, even at 2e8; the update alone +8% at 2.6e7, -4% at 3.5e8. With 32
+// and more buffers cached stores lost 1-5% at every size. The kernels are
+// instantiated both ways where the first condition holds and the host picks
+// one at launch (a runtime branch between the forms inside one kernel cost
+// the 64- and 128-buffer kernels 2-3%).
+constexpr int64_t kCachedStateBytes = int64_t{288} << 20;
 __host__ __device__ constexpr bool cached_state_for(int n_workers) { return n_workers <= 16; }
+// The whole rule, for n elements of parameters (and of momentum).
+__host__ __device__ constexpr bool use_cached_state(int n_workers, int64_t n) {
+    return cached_state_for(n_workers) && n <= kCachedStateBytes / 8;
+}
 
 // Parameters, momentum and replicas stored. Parameters and momentum go
 // through the caches (write-back) when s.cached_state() is set, else with
@@ -780,10 +789,10 @@ struct FlatSrcT {
 // (n % VEC elements) is handled by thread 0 of block 0 after its loop.
 // The unit index space is [0, full] with unit `full` the ragged tail
 // (n % VEC elements, present only when that is nonzero).
-template <typename GT, int W, int G, int U>
+template <typename GT, int W, int G, int U, int CACHED>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrcT<cached_state_for(W * G) ? 1 : 0> s{a, resolve_hyper(a.h, a.lr_ptr)};
+    const FlatSrcT<CACHED> s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     for_tiles<U, VEC>(
@@ -933,22 +942,36 @@ __global__ __launch_bounds__(kBlock) void global_mean_kernel(MeanArgs a) {
 
 // lsgd_sgd_step: update and copy-out from a precomputed mean gradient, one
 // tile of U 4-element units, stream-major.
-template <int U, bool TAIL>
+template <int U, bool TAIL, int CACHED>
 __device__ __forceinline__ void sgd_tile(const StepArgs& a, const Hyper& h, const int64_t (&e0)[U],
                                          int cnt) {
     constexpr int T = U * 4;
     float g[T], p[T], m[T];
 #pragma unroll
     for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.gbar, e0[q], cnt, slice<4, T>(g, q));
+    if constexpr (CACHED != 0) {
 #pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+        for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
 #pragma unroll
-    for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+        for (int q = 0; q < U; ++q) load_f32_cached<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+        for (int q = 0; q < U; ++q) load_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    }
     sgd_update<T>(h, g, p, m);
+    if constexpr (CACHED != 0) {
 #pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+        for (int q = 0; q < U; ++q) store_f32_cached<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
 #pragma unroll
-    for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+        for (int q = 0; q < U; ++q) store_f32_cached<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.p, e0[q], cnt, slice<4, T>(p, q));
+#pragma unroll
+        for (int q = 0; q < U; ++q) store_f32<4, TAIL>(a.m, e0[q], cnt, slice<4, T>(m, q));
+    }
     for (int r = 0; r < a.n_replicas; ++r) {
         void* rp = a.replicas[r];
 #pragma unroll
@@ -956,18 +979,18 @@ __device__ __forceinline__ void sgd_tile(const StepArgs& a, const Hyper& h, cons
     }
 }
 
-template <int U>
+template <int U, int CACHED>
 __global__ __launch_bounds__(kBlock) void sgd_kernel(StepArgs a) {
     const Hyper h = resolve_hyper(a.h, a.lr_ptr);
     const int64_t full = a.n / 4;
     const int rem = static_cast<int>(a.n - full * 4);
     for_tiles<U, 4>(
         full, full + (rem != 0), a.xcd_chunk, a.upl,
-        [&](const int64_t (&e0)[U]) { sgd_tile<U, false>(a, h, e0, 4); },
+        [&](const int64_t (&e0)[U]) { sgd_tile<U, false, CACHED>(a, h, e0, 4); },
         [&](int64_t u) {
             const int64_t e[1] = {u * 4};
-            if (u < full) sgd_tile<1, false>(a, h, e, 4);
-            else sgd_tile<1, true>(a, h, e, rem);
+            if (u < full) sgd_tile<1, false, CACHED>(a, h, e, 4);
+            else sgd_tile<1, true, CACHED>(a, h, e, rem);
         });
 }
 

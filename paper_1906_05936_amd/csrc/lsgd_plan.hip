@@ -23,6 +23,7 @@ struct lsgd_plan {
     lsgd_dtype gdt, rdt;
     int32_t n_buckets, n_chunks, stride;
     int64_t piece;  // elements per piece and per bucket
+    int64_t total_elems;  // elements of all tensors
     lsgd::PlanChunk* d_chunks;
     int32_t* d_bucket_begin;
     lsgd::CopyDesc* d_copy_desc;
@@ -62,29 +63,39 @@ constexpr int64_t piece_elems(int tile) { return static_cast<int64_t>(kBlock) * 
 static_assert(piece_elems<float>(1) % 8 == 0 && piece_elems<uint16_t>(1) % 8 == 0,
               "pieces must start on unit boundaries");
 
+template <typename GT, int W, int G>
+PlanKernel plan_ct(bool cached) {
+    constexpr int U = tile_units<GT>(W * G);
+    if constexpr (cached_state_for(W * G))
+        if (cached) return step_plan_kernel<GT, W, G, U, 1>;
+    return step_plan_kernel<GT, W, G, U, 0>;
+}
+
 template <typename GT, int W>
-PlanKernel pick_plan_g(int G) {
+PlanKernel pick_plan_g(int G, bool cached) {
     switch (G) {
-        case 1: return step_plan_kernel<GT, W, 1, tile_units<GT>(W)>;
-        case 2: return step_plan_kernel<GT, W, 2, tile_units<GT>(W * 2)>;
-        case 4: return step_plan_kernel<GT, W, 4, tile_units<GT>(W * 4)>;
-        case 8: return step_plan_kernel<GT, W, 8, tile_units<GT>(W * 8)>;
+        case 1: return plan_ct<GT, W, 1>(cached);
+        case 2: return plan_ct<GT, W, 2>(cached);
+        case 4: return plan_ct<GT, W, 4>(cached);
+        case 8: return plan_ct<GT, W, 8>(cached);
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return step_plan_kernel<GT, W, 16, tile_units<GT>(W * 16)>;
+            if constexpr (W * 16 <= kMaxWorkers) return plan_ct<GT, W, 16>(cached);
             else return nullptr;
     }
     return nullptr;
 }
 
+// The plan kernel for (W, G): compile-time for powers of two up to 16, with
+// parameters and momentum through the caches when `cached`; else segmented.
 template <typename GT>
-PlanPick pick_plan(int W, int G) {
+PlanPick pick_plan(int W, int G, bool cached = false) {
     PlanKernel k = nullptr;
     switch (W) {
-        case 1: k = pick_plan_g<GT, 1>(G); break;
-        case 2: k = pick_plan_g<GT, 2>(G); break;
-        case 4: k = pick_plan_g<GT, 4>(G); break;
-        case 8: k = pick_plan_g<GT, 8>(G); break;
-        case 16: k = pick_plan_g<GT, 16>(G); break;
+        case 1: k = pick_plan_g<GT, 1>(G, cached); break;
+        case 2: k = pick_plan_g<GT, 2>(G, cached); break;
+        case 4: k = pick_plan_g<GT, 4>(G, cached); break;
+        case 8: k = pick_plan_g<GT, 8>(G, cached); break;
+        case 16: k = pick_plan_g<GT, 16>(G, cached); break;
     }
     if (k) return PlanPick{k, tile_units<GT>(W * G)};
     return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>,
@@ -108,7 +119,7 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     a.ptrs = plan->d_ptrs;
     a.stride = plan->stride;
     a.n_workers = plan->n_workers;
-    a.cached_state = cached_state_for(plan->n_workers) ? 1 : 0;   // read by the LARS update
+    a.cached_state = use_cached_state(plan->n_workers, plan->total_elems) ? 1 : 0;   // read by the LARS update
     a.n_groups = plan->n_groups;
     a.W = plan->W;
     a.n_replicas = plan->n_replicas;
@@ -318,6 +329,7 @@ LSGD_API lsgd_status lsgd_plan_create(lsgd_plan** out, int32_t n_tensors, const 
     p->n_buckets = static_cast<int32_t>(bucket_begin.size()) - 1;
     p->stride = stride;
     p->piece = kPiece;
+    for (int32_t t = 0; t < n_tensors; ++t) p->total_elems += numel[t];
     p->gbar_floats = gbar_floats;
     p->ranges = new std::vector<Range>(ranges);
     hipError_t e = hipSuccess;
@@ -403,8 +415,9 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
         k = seg_levels(max_count) == 5 ? (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 5> : step_plan_seg<float, 5>)
                                        : (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 8> : step_plan_seg<float, 8>);
     } else {
-        k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups).kernel
-                                   : pick_plan<float>(plan->W, plan->n_groups).kernel;
+        const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
+        k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached).kernel
+                                   : pick_plan<float>(plan->W, plan->n_groups, cached).kernel;
     }
     const bool split = separate_copy_out(plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4, plan->n_replicas,
                                          plan->rdt == LSGD_BF16 ? 2 : 4);

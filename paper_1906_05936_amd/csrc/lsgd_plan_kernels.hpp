@@ -90,10 +90,10 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
 
 // Compile-time (W, G): tiles of U units kBlock apart, then the units of a
 // partial last tile, then the ragged end (thread 0).
-template <typename GT, int W, int G, int U>
+template <typename GT, int W, int G, int U, int CACHED>
 __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    for_plan_chunks<cached_state_for(W * G) ? 1 : 0>(a, [&](const auto& s, const PlanChunk& ch, int32_t) {
+    for_plan_chunks<CACHED>(a, [&](const auto& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
             if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {

@@ -896,6 +896,14 @@ def test_vector_longer_than_2_to_31_elements():
             assert_close(to_host(p.index_select(0, ti)), ph, "params mode %d" % mode)
             assert_close(to_host(m.index_select(0, ti)), mh, "momentum mode %d" % mode)
             assert np.array_equal(to_host(rep.index_select(0, ti)), rr[0]), mode
+        # the update alone on the same vector (its nontemporal form: p and m exceed the caches)
+        lsgd.sgd_step(p, m, grads[0], 0.1, 0.9, 1e-4, [rep])
+        rr = [np.zeros(idx.size, np.float32)]
+        oracle.sgd_step(ph, mh, gh[0], 0.1, 0.9, 1e-4, rr)
+        torch.cuda.synchronize()
+        assert_close(to_host(p.index_select(0, ti)), ph, "params after sgd_step")
+        assert_close(to_host(m.index_select(0, ti)), mh, "momentum after sgd_step")
+        assert np.array_equal(to_host(rep.index_select(0, ti)), rr[0])
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
     del p, m, grads, rep
