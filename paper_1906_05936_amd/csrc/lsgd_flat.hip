@@ -62,9 +62,10 @@ FlatPick pick_flat(int W, int G, bool cached) {
 
 // Runtime group layouts: accumulator levels for the largest count.
 template <typename GT>
-FlatPick pick_flat_seg(int max_count) {
+FlatPick pick_flat_seg(int max_count, bool cached) {
     constexpr int U = SegTileUnits<GT>::U;
-    return FlatPick{seg_levels(max_count) == 5 ? step_flat_seg<GT, 5, U> : step_flat_seg<GT, 8, U>, U};
+    if (seg_levels(max_count) != 5) return FlatPick{step_flat_seg<GT, 8, U, 0>, U};
+    return FlatPick{cached ? step_flat_seg<GT, 5, U, 1> : step_flat_seg<GT, 5, U, 0>, U};
 }
 
 using MeanKernel = void (*)(MeanArgs);
@@ -259,7 +260,7 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
             if (j > 0) max_count = std::max(max_count, b - static_cast<int32_t>(a.group_start[j - 1]));
         }
         a.literal = literal ? 1 : 0;
-        k = gdt == LSGD_BF16 ? pick_flat_seg<uint16_t>(max_count) : pick_flat_seg<float>(max_count);
+        k = gdt == LSGD_BF16 ? pick_flat_seg<uint16_t>(max_count, cached) : pick_flat_seg<float>(max_count, cached);
     }
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;

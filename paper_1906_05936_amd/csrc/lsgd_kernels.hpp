@@ -807,10 +807,10 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
 // Runtime group layouts (non-power-of-two or large counts, and the
 // paper-literal reduction): group j is members [group_start[j],
 // group_start[j+1]) of the member-ordered pointer table.
-template <typename GT, int LV, int U>
+template <typename GT, int LV, int U, int CACHED>
 __global__ __launch_bounds__(kBlock) void step_flat_seg(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
-    const FlatSrcT<0> s{a, resolve_hyper(a.h, a.lr_ptr)};
+    const FlatSrcT<CACHED> s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
     const int rem = static_cast<int>(a.n - full * VEC);
     const bool literal = a.literal != 0;

@@ -63,6 +63,14 @@ constexpr int64_t piece_elems(int tile) { return static_cast<int64_t>(kBlock) * 
 static_assert(piece_elems<float>(1) % 8 == 0 && piece_elems<uint16_t>(1) % 8 == 0,
               "pieces must start on unit boundaries");
 
+// The segmented plan kernel for groups and group counts up to max_count
+// (the cached form exists for counts up to 31, the only ones it can have).
+template <typename GT>
+PlanKernel plan_seg(int max_count, bool cached) {
+    if (seg_levels(max_count) != 5) return step_plan_seg<GT, 8, 0>;
+    return cached ? step_plan_seg<GT, 5, 1> : step_plan_seg<GT, 5, 0>;
+}
+
 template <typename GT, int W, int G>
 PlanKernel plan_ct(bool cached) {
     constexpr int U = tile_units<GT>(W * G);
@@ -98,8 +106,7 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
         case 16: k = pick_plan_g<GT, 16>(G, cached); break;
     }
     if (k) return PlanPick{k, tile_units<GT>(W * G)};
-    return PlanPick{seg_levels(W > G ? W : G) == 5 ? step_plan_seg<GT, 5> : step_plan_seg<GT, 8>,
-                    SegTileUnits<GT>::U};
+    return PlanPick{plan_seg<GT>(W > G ? W : G, cached), SegTileUnits<GT>::U};
 }
 
 lsgd_status check_device(const lsgd_plan* plan) {
@@ -412,8 +419,8 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     PlanKernel k;
     if (literal || plan->W == 0) {
         const int32_t max_count = std::max(plan->max_group, plan->n_groups);
-        k = seg_levels(max_count) == 5 ? (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 5> : step_plan_seg<float, 5>)
-                                       : (plan->gdt == LSGD_BF16 ? step_plan_seg<uint16_t, 8> : step_plan_seg<float, 8>);
+        const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
+        k = plan->gdt == LSGD_BF16 ? plan_seg<uint16_t>(max_count, cached) : plan_seg<float>(max_count, cached);
     } else {
         const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
         k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached).kernel

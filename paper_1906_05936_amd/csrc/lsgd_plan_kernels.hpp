@@ -113,13 +113,13 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
 
 // Runtime group layouts (non-power-of-two or large counts, and the
 // paper-literal reduction over any partition): one unit per lane.
-template <typename GT, int LV>
+template <typename GT, int LV, int CACHED>
 __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int U = SegTileUnits<GT>::U;
     const bool literal = a.literal != 0;
     auto gs = [&](int j) { return static_cast<int>(a.group_start[j]); };
-    for_plan_chunks<0>(a, [&](const PlanSrcT<0>& s, const PlanChunk& ch, int32_t) {
+    for_plan_chunks<CACHED>(a, [&](const PlanSrcT<CACHED>& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
         for (int64_t t0 = threadIdx.x; t0 < full; t0 += static_cast<int64_t>(kBlock) * U) {
             if (t0 + static_cast<int64_t>(U - 1) * kBlock < full) {
