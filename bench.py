@@ -672,7 +672,8 @@ def separate_copy_out(wl, R, mode="auto"):
     if mode == "separate":
         return True
     rb = 2 if wl.replica_dtype == "bf16" else 4
-    return R * rb >= 32 or wl.n_workers * wl.grad_bytes >= 256
+    cached = wl.n_workers <= 16 and 8 * wl.n <= (288 << 20)   # parameters and momentum through the caches
+    return R * rb >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
 
 
 def kernel_match(wl, reduction=None, lars=False):
@@ -735,7 +736,12 @@ def lars_separate_copy_out(wl, R, mode="auto"):
     for labels and per-kernel accounting."""
     if R == 0 or mode == "fused":
         return False
-    return mode == "separate" or (wl.replica_dtype == "f32" and R >= 4)
+    if mode == "separate":
+        return True
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    if wl.n_workers <= 16 and 8 * wl.n <= (288 << 20):   # parameters and momentum through the caches
+        return R * rb >= 16
+    return rb == 4 and R >= 4
 
 
 def lars_kernel_bytes(wl, R, mode="auto"):

@@ -152,19 +152,25 @@ LaunchShape pad_for_xcd_chunk(int64_t blocks, int64_t block_bytes) {
 int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_order_relaxed); }
 
 // Automatic rule, from same-process measurements of the fused pass against
-// step-then-copy-out (the replica-major pass) at N = 16, 64, 128 gradients
-// and R = 1..128 replicas, flat steps and plans, binary32 and bfloat16. The
-// separate pass won once the replicas take 32 bytes per element or more
-// (R = 16 with 16 gradients: +7-9%; R = 64: +18-20%; 64 bfloat16 gradients:
-// even) or the gradients 256 bytes (128 binary32 gradients, R = 2: +6%,
-// R = 128: +20%), and was within 3% either way below that.
-bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz) {
+// step-then-copy-out (the replica-major pass) at N = 4..128 gradients and
+// R = 1..128 replicas, flat steps and plans, binary32 and bfloat16. With
+// nontemporal parameter and momentum accesses the separate pass won once the
+// replicas take 32 bytes per element or more (R = 16 with 16 gradients:
+// +7-9%; R = 64: +18-20%) or the gradients 256 bytes (128 binary32
+// gradients, R = 2: +6%, R = 128: +20%), and was within 3% either way below
+// that. When parameters and momentum go through the caches
+// (use_cached_state) the fused pass gains more, and the crossing moves to 64
+// bytes: at 32 the fused pass won by 2-4% (4x4 R = 8, 2x2 R = 8, 4x4
+// bfloat16 R = 16), at 64 the separate one by 3-12% (4x4 R = 16, 2x2 R = 16,
+// the ResNet-50 plan), at 256 by 28%.
+bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n) {
     if (n_replicas <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
     const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
-    return static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz) >= 32 || grad_bytes >= 256;
+    const int64_t replica_bytes = static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz);
+    return replica_bytes >= (use_cached_state(n_workers, n) ? 64 : 32) || grad_bytes >= 256;
 }
 
 // 8 MB of p per window: 1 MB in each of the eight XCD L2 caches (4 MB each),
@@ -179,14 +185,19 @@ int64_t copy_window_blocks(int64_t block_p_bytes, int64_t blocks) {
 }
 
 // The same choice for lsgd_sgd_step (reads 12 bytes per element, writes 8 plus
-// the replicas). Measured: with binary32 replicas the separate pass won from
-// R = 4 (+2%; R = 8: +4%, R = 16: +15%, R = 64: +10%) and lost below (R = 1:
-// -11%); with bfloat16 replicas the fused pass won or tied at every R up to 64.
-bool separate_copy_out_update(int32_t n_replicas, size_t rsz) {
+// the replicas) and the LARS update. Measured with nontemporal parameter and
+// momentum accesses: with binary32 replicas the separate pass won from R = 4
+// (+2%; R = 8: +4%, R = 16: +15%, R = 64: +10%) and lost below (R = 1: -11%);
+// with bfloat16 replicas the fused pass won or tied at every R up to 64. With
+// them through the caches (`cached`): the separate pass won from 16 replica
+// bytes per element (binary32 R = 4: +3%, R = 16: +4%; bfloat16 R = 8: +4%,
+// R = 16: +14%, R = 64: +11%) and lost below (bfloat16 R = 4: -9%).
+bool separate_copy_out_update(int32_t n_replicas, size_t rsz, bool cached) {
     if (n_replicas <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
+    if (cached) return static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz) >= 16;
     return rsz == 4 && n_replicas >= 4;
 }
 

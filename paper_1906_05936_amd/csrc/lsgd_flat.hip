@@ -265,7 +265,7 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    const bool split = separate_copy_out(n_workers, dtype_size(gdt), n_replicas, dtype_size(rdt));
+    const bool split = separate_copy_out(n_workers, dtype_size(gdt), n_replicas, dtype_size(rdt), n);
     if (split) a.n_replicas = 0;
     hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     if ((st = check_launch(literal ? "lsgd_step_ex" : "lsgd_step")) != LSGD_OK || !split) return st;
@@ -379,7 +379,7 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     const LaunchShape ls = launch_shape((n + 3) / 4, kSgdTile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    const bool split = separate_copy_out_update(n_replicas, dtype_size(rdt));
+    const bool split = separate_copy_out_update(n_replicas, dtype_size(rdt), use_cached_state(1, n));
     if (split) a.n_replicas = 0;
     const FlatKernel sk = use_cached_state(1, n) ? sgd_kernel<kSgdTile, 1> : sgd_kernel<kSgdTile, 0>;
     hipLaunchKernelGGL(sk, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);

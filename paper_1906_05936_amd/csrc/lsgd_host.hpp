@@ -68,11 +68,13 @@ LaunchShape launch_shape(int64_t units, int tile = 1);
 // The launch shape's passes per workgroup (units_per_lane).
 int32_t launch_passes_per_block();
 
-// Whether a step with N gradients of gsz bytes and R replicas of rsz bytes
-// writes its replicas in a copy-out pass of its own (lsgd_set_copy_out_mode).
-bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz);
-// The same for lsgd_sgd_step.
-bool separate_copy_out_update(int32_t n_replicas, size_t rsz);
+// Whether a step with N gradients of gsz bytes, R replicas of rsz bytes and n
+// elements writes its replicas in a copy-out pass of its own
+// (lsgd_set_copy_out_mode).
+bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n);
+// The same for lsgd_sgd_step and the LARS update; `cached`: their parameter
+// and momentum accesses go through the caches.
+bool separate_copy_out_update(int32_t n_replicas, size_t rsz, bool cached);
 
 // Largest grid of a grid-stride kernel whose XCD assignment must not change
 // between strides: kMaxGridBlocks, or the blocks_per_cu cap of

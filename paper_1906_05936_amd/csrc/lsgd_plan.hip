@@ -427,7 +427,7 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
                                    : pick_plan<float>(plan->W, plan->n_groups, cached).kernel;
     }
     const bool split = separate_copy_out(plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4, plan->n_replicas,
-                                         plan->rdt == LSGD_BF16 ? 2 : 4);
+                                         plan->rdt == LSGD_BF16 ? 2 : 4, plan->total_elems);
     if (split) a.n_replicas = 0;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, s, a);
@@ -517,7 +517,8 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
     if ((st = check_launch("lsgd_lars_step_plan (trust)")) != LSGD_OK) return st;
     if (plan->n_buckets == 0) return LSGD_OK;
     // the update reads and writes as lsgd_sgd_step does: the same copy-out rule
-    const bool split = separate_copy_out_update(plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4);
+    const bool split = separate_copy_out_update(plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,
+                                                use_cached_state(plan->n_workers, plan->total_elems));
     if (split) la.pa.n_replicas = 0;
     hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
     if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK || !split) return st;
