@@ -910,6 +910,53 @@ def test_vector_longer_than_2_to_31_elements():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("G,W,gdt,R,rdt,plan", [(4, 4, "f32", 16, "f32", False), (3, 5, "f32", 5, "bf16", False),
+                                                (2, 2, "bf16", 2, "bf16", False), (4, 4, "f32", 16, "f32", True)])
+def test_nontemporal_forms_above_the_cache_limit(G, W, gdt, R, rdt, plan):
+    """Vectors whose parameters and momentum exceed the cached form's limit
+    (8n > 288 MB) take the nontemporal kernels even with 16 or fewer workers:
+    two steps on sampled elements against the oracle, flat (compile-time and
+    segmented) and through a three-tensor plan."""
+    n = 40_000_003
+    log("n = %d above the cache limit: G=%d W=%d %s R=%d %s plan=%s" % (n, G, W, gdt, R, rdt, plan))
+    N = G * W
+    gow = groups_for(G, W, "shuffled", seed=9)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(40)
+    gt = torch.bfloat16 if gdt == "bf16" else torch.float32
+    rt = torch.bfloat16 if rdt == "bf16" else torch.float32
+    p = torch.randn(n, generator=gen, device=DEV).mul_(0.05)
+    m = torch.zeros(n, device=DEV)
+    grads = [torch.randn(n, generator=gen, device=DEV).mul_(0.01).to(gt) for _ in range(N)]
+    reps = [torch.empty(n, device=DEV, dtype=rt) for _ in range(R)]
+    idx = workloads.sample_indices(n, 4096, seed=41)
+    sizes = [13_333_336, 8, n - 13_333_344]   # views at 16-byte-aligned offsets
+    idx = np.unique(np.concatenate([idx, np.cumsum([0] + sizes)[1:-1], np.cumsum(sizes)[:-1] - 1]))
+    ti = torch.from_numpy(idx).to(DEV)
+    ph, mh = to_host(p.index_select(0, ti)), np.zeros(idx.size, np.float32)
+    gh = [to_host(g.index_select(0, ti)) for g in grads]
+    pl = None
+    if plan:
+        v = lambda t: workloads.view_tensors(t, sizes)
+        pl = lsgd.Plan(v(p), v(m), [v(g) for g in grads], gow, G, [v(r) for r in reps])
+    for step in range(2):
+        if pl is not None:
+            pl.step(0.1, 0.9, 1e-4)
+        else:
+            lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps)
+        rr = [np.zeros(idx.size, np.uint16 if rdt == "bf16" else np.float32) for _ in range(R)]
+        oracle.lsgd_step(ph, mh, gh, gow, G, 0.1, 0.9, 1e-4, rr, oracle.BF16 if rdt == "bf16" else oracle.F32)
+        torch.cuda.synchronize()
+        assert_close(to_host(p.index_select(0, ti)), ph, "params step %d" % step)
+        assert_close(to_host(m.index_select(0, ti)), mh, "momentum step %d" % step)
+        for r in range(R):
+            assert np.array_equal(to_host(reps[r].index_select(0, ti)), rr[r]), (step, r)
+    if pl is not None:
+        pl.close()
+    del p, m, grads, reps
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------- tail sizes
 
 TAIL_SIZES = list(range(1, 68)) + [2 ** k + d for k in (7, 10, 11, 12, 13, 17) for d in (-1, 1)]
