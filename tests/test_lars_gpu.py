@@ -212,6 +212,50 @@ def test_lars_full_size_resnet50_tensors():
     plan.close()
 
 
+def test_lars_above_the_cache_limit():
+    """Two tensors of 2e7 elements (parameters and momentum beyond the cached
+    form's 288 MB limit: the update's nontemporal form), 2 x 2 workers, four
+    binary32 replicas (a copy-out pass), two steps, every element compared."""
+    sizes = [20_000_000, 20_000_004]
+    G, W, R = 2, 2, 4
+    N = G * W
+    gow = workloads.contiguous_groups(G, W)
+    rng = np.random.default_rng(12)
+    ph = [(rng.standard_normal(s) * 0.05).astype(np.float32) for s in sizes]
+    mh = [np.zeros(s, np.float32) for s in sizes]
+    params = [to_dev(x) for x in ph]
+    mom = [torch.zeros(s, device=DEV) for s in sizes]
+    grads = [[torch.empty(s, device=DEV) for s in sizes] for _ in range(N)]
+    reps = [[torch.empty(s, device=DEV) for s in sizes] for _ in range(R)]
+    plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+    trust = torch.empty(len(sizes), device=DEV)
+    for step in range(2):
+        gh = [[(rng.standard_normal(s) * 1e-2).astype(np.float32) for s in sizes] for _ in range(N)]
+        for w in range(N):
+            for t in range(len(sizes)):
+                grads[w][t].copy_(to_dev(gh[w][t]))
+        plan.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, trust_out=trust)
+        torch.cuda.synchronize()
+        tg = to_host(trust)
+        for t, s in enumerate(sizes):
+            rr = [np.zeros(s, np.float32) for _ in range(R)]
+            tr = oracle.lars_step(ph[t], mh[t], [gh[w][t] for w in range(N)], gow, G, 0.1, 0.9, 1e-4,
+                                  TRUST_COEF, rr)
+            assert ulps(tg[t], tr) <= 1, (t, step, tg[t], tr)
+            pg, mg = to_host(params[t]), to_host(mom[t])
+            if np.float32(tg[t]) == np.float32(tr):
+                assert np.array_equal(pg, ph[t]) and np.array_equal(mg, mh[t]), (t, step)
+                for r in range(R):
+                    assert np.array_equal(to_host(reps[r][t]), rr[r]), (t, r, step)
+            else:
+                close(pg, ph[t], "params[%d]" % t)
+                close(mg, mh[t], "momentum[%d]" % t)
+                ph[t][:] = pg
+                mh[t][:] = mg
+        log("  step %d ok" % step)
+    plan.close()
+
+
 def test_lars_argument_errors():
     """Workspace too small, misaligned, or overlapping a plan buffer: the call
     raises and launches nothing."""
