@@ -816,8 +816,8 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world > 1:
         print("bench.py measures one GPU: every worker gradient of the workload sits in that "
-              "GPU's HBM (one GPU's share of the aggregation); runs on %d GPUs are not part of "
-              "this build." % max(args.gpus, world), file=sys.stderr)
+              "GPU's HBM (one GPU's share of the aggregation); the library has no collectives "
+              "between GPUs, so %d GPUs cannot be measured." % max(args.gpus, world), file=sys.stderr)
         sys.exit(2)
     if args.path == "unfused" and (args.graph or args.lr_schedule or args.lars):
         raise SystemExit("--graph, --lr-schedule and --lars apply to the fused path")
