@@ -526,7 +526,9 @@ constexpr int kStreamFloats = 128;
 // groups stream through the accumulator (N >= 32: +3-8% over two at 8x4,
 // 4x8, 8x8, 16x4, 2x16 and 16x8, in same-process A/Bs; at N <= 16 three or
 // four units lose 1-3%, since they leave the unrolled form). bfloat16 tiles
-// stay at one unit (two lost 17% at 8x8).
+// stay at one unit: two units measured -1% at 4x4, +0.6% / -0.2% on the
+// 3.5e8-element 8x8 workload (step kernel alone / whole step), +1.6% at 8x8
+// and +4% at 16x8 on 2.6e7 elements.
 template <typename GT>
 constexpr int tile_units(int n_workers) {
     return sizeof(GT) == 4 ? (n_workers * 2 * Unit<GT>::VEC <= kUnrollFloats ? 2 : 4) : 1;
