@@ -48,6 +48,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget")
     ap.add_argument("--no-r0", action="store_true", help="skip the secondary R=0 measurement")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache measurement (a cache flush before every step)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also launch a plain 1 GiB copy kernel (counter calibration)")
     ap.add_argument("--reduction", choices=("mean_of_means", "literal"), default=None,
@@ -209,7 +211,7 @@ class Setup:
 
             def step():
                 check(fn(*args))
-            if R and separate_copy_out(wl, R, copy_out) and not lr_schedule:
+            if R and separate_copy_out(wl, R, copy_out) and not lr_schedule and not broadcast_grad:
                 # the same two kernels launched one at a time: the step without
                 # replicas on the same buffers, then the copy-out pass
                 args0 = args[:11] + (None, 0) + args[13:]
@@ -253,23 +255,78 @@ class Setup:
             self.plan0.close()
 
 
-def time_steps(setup, steps, warmup, fn=None):
-    """Average ms per step (or per call of `fn`) over `steps` back-to-back
-    launches, HIP events on the launch stream, synchronized on both sides."""
+REPEATS = 5        # timed repeats of the K-step loop; the line reports their median
+
+
+def time_steps(setup, steps, warmup, fn=None, repeats=REPEATS):
+    """Milliseconds per step (or per call of `fn`) of each of `repeats` timed
+    loops of `steps` back-to-back launches, after `warmup` untimed ones: HIP
+    events on the launch stream, the device synchronized before and after
+    every loop."""
     import torch
     fn = fn or setup.step
     for _ in range(warmup):
         fn()
-    torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(setup.stream)
-    for _ in range(steps):
+    out = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(setup.stream)
+        for _ in range(steps):
+            fn()
+        t1.record(setup.stream)
+        t1.synchronize()
+        torch.cuda.synchronize()
+        out.append(t0.elapsed_time(t1) / steps)
+    return out
+
+
+def median(xs):
+    s = sorted(xs)
+    k = len(s) // 2
+    return s[k] if len(s) % 2 else 0.5 * (s[k - 1] + s[k])
+
+
+class CacheFlush:
+    """A plain copy of FLUSH_BYTES (lsgd_stream_copy) that evicts the 256 MB
+    Infinity Cache and the L2 caches: every buffer of the step that follows is
+    read from HBM."""
+    FLUSH_BYTES = 512 << 20
+
+    def __init__(self, dev, stream):
+        import torch
+        n = self.FLUSH_BYTES // 4
+        self.src = torch.ones(n, device=dev)
+        self.dst = torch.empty_like(self.src)
+        self.stream = stream
+
+    def __call__(self):
+        import paper_1906_05936_amd as lsgd
+        lsgd.stream_copy(self.dst, self.src, stream=self.stream)
+
+
+def time_steps_cold(setup, steps, warmup, flush, fn=None, repeats=REPEATS):
+    """Like time_steps, but every step runs after a cache flush on the same
+    stream and only the step is timed (HIP events recorded after the flush and
+    after the step): per repeat, the mean over `steps` such steps."""
+    import torch
+    fn = fn or setup.step
+    for _ in range(warmup):
+        flush()
         fn()
-    t1.record(setup.stream)
-    t1.synchronize()
-    torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps
+    out = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for a, b in ev:
+            flush()
+            a.record(setup.stream)
+            fn()
+            b.record(setup.stream)
+        torch.cuda.synchronize()
+        out.append(sum(a.elapsed_time(b) for a, b in ev) / steps)
+    return out
 
 
 def whole_step_label(wl, R, setup, args):
@@ -277,8 +334,12 @@ def whole_step_label(wl, R, setup, args):
     names = [kernel_match(wl, setup.reduction, args.lars)]
     if args.lars:
         names += ["lars_trust_kernel", "lars_update_kernel"]
-    if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars else separate_copy_out(wl, R, args.copy_out)):
-        names.append("copy_out")
+    if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
+            else separate_copy_out(wl, R, args.copy_out, args.broadcast_grad)):
+        if R:
+            names.append("copy_out")
+        if args.broadcast_grad and wl.n_workers > 1:
+            names.append("copy_out (broadcast)")
     if args.lr_schedule:
         names.insert(0, "schedule_step_kernel")
     return " + ".join(names) + (" (whole step)" if len(names) > 1 else "")
@@ -299,25 +360,30 @@ def captured(setup):
     return graph.replay
 
 
-def time_parts(setup, steps, warmup):
-    """Average ms of each kernel of a step launched one kernel at a time
-    (setup.parts, in step order), with a HIP event recorded on the launch stream
-    before and after every kernel: each kernel runs where it runs in the step,
-    after its predecessor, on the same buffers."""
+def time_parts(setup, steps, warmup, repeats=REPEATS):
+    """Milliseconds of each kernel of a step launched one kernel at a time
+    (setup.parts, in step order), with a HIP event recorded on the launch
+    stream before and after every kernel: each kernel runs where it runs in the
+    step, after its predecessor, on the same buffers. Per kernel, the median
+    over `repeats` loops of the mean over `steps` steps."""
     import torch
     fns = [fn for _, fn, _ in setup.parts]
     for _ in range(warmup):
         for fn in fns:
             fn()
-    torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
-    for i in range(steps):
-        ev[i][0].record(setup.stream)
-        for j, fn in enumerate(fns):
-            fn()
-            ev[i][j + 1].record(setup.stream)
-    torch.cuda.synchronize()
-    return [sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps for j in range(len(fns))]
+    per_rep = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
+        for i in range(steps):
+            ev[i][0].record(setup.stream)
+            for j, fn in enumerate(fns):
+                fn()
+                ev[i][j + 1].record(setup.stream)
+        torch.cuda.synchronize()
+        per_rep.append([sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
+                        for j in range(len(fns))])
+    return [median([r[j] for r in per_rep]) for j in range(len(fns))]
 
 
 def copy_ceiling(dev, calibrate):
@@ -408,19 +474,10 @@ class UnfusedSetup:
                 n * (4 + 16 + self.R * rb)]                        # update: read gbar, p, m; write p, m, R
 
     def time_calls(self, steps, warmup):
-        """Average ms per call of each of the three kernels (events between them)."""
-        import torch
-        for _ in range(warmup):
-            self.step()
-        torch.cuda.synchronize()
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
-        for k in range(steps):
-            for c in range(3):
-                ev[k][c].record(self.stream)
-                self.calls[c]()
-            ev[k][3].record(self.stream)
-        torch.cuda.synchronize()
-        return [sum(ev[k][c].elapsed_time(ev[k][c + 1]) for k in range(steps)) / steps for c in range(3)]
+        """Milliseconds per call of each of the three kernels (events between
+        them; median of the repeats)."""
+        self.parts = [(None, c, None) for c in self.calls]
+        return time_parts(self, steps, warmup)
 
 
 # ---------------------------------------------------------------- CPU baseline
@@ -664,20 +721,22 @@ def _calib_kib(rows, counter):
     return sum(vals.values()) / len(vals), len(vals)
 
 
-def separate_copy_out(wl, R, mode="auto"):
+def separate_copy_out(wl, R, mode="auto", bcast=False):
     """The library's rule for the copy-out pass (lsgd_set_copy_out_mode), for
-    labels only."""
-    if R == 0 or mode == "fused":
+    labels only: copies of R replicas, and with the gradient broadcast of the
+    mean gradient to the other N - 1 members."""
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    copy_bytes = R * rb + (4 * (wl.n_workers - 1) if bcast else 0)
+    if copy_bytes == 0 or mode == "fused":
         return False
     if mode == "separate":
         return True
-    rb = 2 if wl.replica_dtype == "bf16" else 4
     cached = wl.n_workers <= 16 and 8 * wl.n <= (288 << 20)   # parameters and momentum through the caches
-    return R * rb >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
+    return copy_bytes >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
 
 
 def kernel_match(wl, reduction=None, lars=False):
-    ct = (not wl.group_sizes and reduction != "literal" and wl.groups in (1, 2, 4, 8, 16)
+    ct = (not wl.group_sizes and wl.groups in (1, 2, 4, 8, 16)
           and wl.workers_per_group in (1, 2, 4, 8, 16) and wl.n_workers <= 128)
     if lars:
         return "lars_norms_kernel" if ct else "lars_norms_seg"
@@ -839,7 +898,8 @@ def main(argv=None):
                             "separate": lsgd.COPY_OUT_SEPARATE}[args.copy_out])
     if args.path == "unfused":
         setup = UnfusedSetup(wl, R, dev)
-        ms = time_steps(setup, args.steps, args.warmup)
+        reps_ms = time_steps(setup, args.steps, args.warmup)
+        ms = median(reps_ms)
         per_call = setup.time_calls(args.steps, args.warmup)
         nbytes = setup.bytes_per_call()
         alg = sum(nbytes)
@@ -850,6 +910,7 @@ def main(argv=None):
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
             "data": "synthetic",
+            "repeats_ms_per_step": [round(x, 6) for x in reps_ms],
             "config": {"workload": wl.name, "path": "unfused", "n": wl.n, "groups": wl.groups,
                        "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                        "replicas": R},
@@ -871,9 +932,8 @@ def main(argv=None):
         print(json.dumps(result), flush=True)
         return
     def extra_bytes():
-        # gradient broadcast writes every worker buffer; LARS re-reads p and
-        # writes and re-reads the mean gradient
-        return (wl.n * wl.n_workers * 4 if args.broadcast_grad else 0) + (12 * wl.n if args.lars else 0)
+        # the gradient broadcast writes the mean gradient into every worker buffer
+        return wl.n * wl.n_workers * 4 if args.broadcast_grad else 0
 
     lars_excl = None
     if args.lars_exclude_vectors:
@@ -886,7 +946,9 @@ def main(argv=None):
         torch.cuda.set_stream(side)
     setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
                   args.tensor_layout, args.copy_out, args.lr_schedule)
-    ms = time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None)
+    replay = captured(setup) if args.graph else None
+    reps_ms = time_steps(setup, args.steps, args.warmup, replay)
+    ms = median(reps_ms)
     kernels = []
     if setup.parts and not args.graph:   # two kernels per step: the step again, an event between its kernels
         for (name, _, nbytes), kms in zip(setup.parts, time_parts(setup, args.steps, args.warmup)):
@@ -902,6 +964,7 @@ def main(argv=None):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
+        "repeats_ms_per_step": [round(x, 6) for x in reps_ms],
         "config": {"workload": wl.name, "n": wl.n, "groups": wl.groups,
                    "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                    "replicas": R, "replica_dtype": wl.replica_dtype,
@@ -912,7 +975,8 @@ def main(argv=None):
                    **({"lars": True, "trust_coef": args.trust_coef,
                        "lars_excluded_tensors": sum(lars_excl) if lars_excl else 0} if args.lars else {}),
                    "copy_out": ("separate pass" if (lars_separate_copy_out(wl, R, args.copy_out) if args.lars
-                                                     else separate_copy_out(wl, R, args.copy_out))
+                                                     else separate_copy_out(wl, R, args.copy_out,
+                                                                            args.broadcast_grad))
                                 else "in the step kernel"),
                    **({"lr": "device schedule step before every step"} if args.lr_schedule else {}),
                    **({"launch": "HIP graph replay"} if args.graph else {})},
@@ -931,13 +995,29 @@ def main(argv=None):
                               "algorithmic_bytes": dom["algorithmic_bytes"], "kernel": dom["kernel"]}
         result["kernels"] = kernels
         result["kernels_sum_ms"] = round(sum(k["ms"] for k in kernels), 6)
+    if args.lars:
+        # what the LARS kernels move besides the method's bytes: the mean
+        # gradient written to the scratch and read back, and p read again
+        impl = alg + 12 * wl.n
+        result["lars_implementation_bytes"] = impl
+        result["lars_implementation_GBps"] = round(impl / (ms * 1e-3) / 1e9, 2)
+    if not args.no_cold:
+        flush = CacheFlush(dev, setup.stream)
+        cold = time_steps_cold(setup, args.steps, args.warmup, flush, replay)
+        cms = median(cold)
+        result["cold_cache"] = {"ms_per_step": round(cms, 6), "GBps": round(alg / (cms * 1e-3) / 1e9, 2),
+                                "frac": round(alg / (cms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                                "repeats_ms_per_step": [round(x, 6) for x in cold],
+                                "flush": "%d MiB copy (lsgd_stream_copy) before every step, events around the "
+                                         "step only" % (CacheFlush.FLUSH_BYTES >> 20)}
+        del flush
     if R != 0 and not args.no_r0:
         setup.close()
         del setup
         torch.cuda.empty_cache()
         setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
                       args.tensor_layout, args.copy_out, args.lr_schedule)
-        ms0 = time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None)
+        ms0 = median(time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None))
         alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
                         "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),

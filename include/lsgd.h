@@ -100,10 +100,16 @@ LSGD_API const char* lsgd_last_error(void);
 
 /*
  * Launch shape of the planless kernels, process-wide (a tuning knob; results
- * are bit-identical for every shape, because each element is computed by one
- * lane from its own inputs in a fixed order). Plans launch one workgroup per
- * bucket: xcd_chunk applies at each lsgd_step_plan, units_per_lane at
- * lsgd_plan_create, blocks_per_cu only to their copy-out pass.
+ * of the steps are bit-identical for every shape, because each element is
+ * computed by one lane from its own inputs in a fixed order). Plans launch one
+ * workgroup per bucket: xcd_chunk applies at each lsgd_step_plan, units_per_lane
+ * at lsgd_plan_create, blocks_per_cu only to their copy-out pass. The one
+ * result that can depend on a shape is a LARS trust ratio
+ * (lsgd_lars_step_plan): its norms are summed piece by piece, and a plan's
+ * piece size is fixed by units_per_lane when the plan is created, so plans
+ * created with different units_per_lane may give ratios (and hence LARS
+ * steps) that differ in the last bit; for one plan, LARS results do not
+ * depend on the shape.
  *   xcd_chunk       0 = workgroups in hardware order; C > 0 = each of the eight
  *                   XCDs runs C consecutive logical workgroups per turn (the grid
  *                   is padded to a multiple of 8*C; not applied to grids smaller
@@ -201,11 +207,16 @@ LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* 
                                    int32_t n_replicas, lsgd_dtype rdt, void* stream);
 
 /*
- * One fused Layered SGD step: group means, global mean, update and copy-out in
- * one pass over memory. Reads every gradient, parameter and momentum element
- * once; writes parameters, momentum and the replicas once. Arguments as for the
- * three calls above. The results are bit-identical to lsgd_group_mean, then
- * lsgd_global_mean, then lsgd_sgd_step.
+ * One fused Layered SGD step: group means, global mean, update and copy-out.
+ * The step kernel reads every gradient, parameter and momentum element once
+ * and writes parameters and momentum once; the group means and the mean
+ * gradient stay in registers. The replicas are written either by that kernel
+ * or, where lsgd_set_copy_out_mode's rule takes the separate form (the
+ * default at 64 or more replica bytes per element with up to 16 workers), by
+ * a copy-out pass launched right after it, which reads the new parameters
+ * once more. Arguments as for the three calls above. The results are
+ * bit-identical to lsgd_group_mean, then lsgd_global_mean, then
+ * lsgd_sgd_step, in either form.
  */
 LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
                                lsgd_dtype gdt, int32_t n_workers,

@@ -163,14 +163,17 @@ int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_ord
 // bytes: at 32 the fused pass won by 2-4% (4x4 R = 8, 2x2 R = 8, 4x4
 // bfloat16 R = 16), at 64 the separate one by 3-12% (4x4 R = 16, 2x2 R = 16,
 // the ResNet-50 plan), at 256 by 28%.
-bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n) {
-    if (n_replicas <= 0) return false;
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n) {
+    if (copy_bytes <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
     const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
-    const int64_t replica_bytes = static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz);
-    return replica_bytes >= (use_cached_state(n_workers, n) ? 64 : 32) || grad_bytes >= 256;
+    return copy_bytes >= (use_cached_state(n_workers, n) ? 64 : 32) || grad_bytes >= 256;
+}
+
+bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n) {
+    return separate_copy_out_bytes(n_workers, gsz, static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz), n);
 }
 
 // 8 MB of p per window: 1 MB in each of the eight XCD L2 caches (4 MB each),

@@ -233,44 +233,69 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     }
     if ((st = check_overlap(ranges)) != LSGD_OK) return st;
 
+    // equal group sizes: the literal reduction then runs in the compile-time
+    // kernels too (W = 0 marks unequal groups)
+    int32_t W = n_workers / n_groups;
+    if (literal)
+        for (int32_t j = 0; j < n_groups; ++j)
+            if (gstart[j + 1] - gstart[j] != gstart[1] - gstart[0]) W = 0;
     a.p = params;
     a.m = momentum;
     a.n = n;
     a.h = Hyper{lr, momentum_coef, weight_decay};
     a.n_workers = n_workers;
     a.n_groups = n_groups;
-    a.W = n_workers / n_groups;
+    a.W = W;
     a.n_replicas = n_replicas;
     a.rdt = static_cast<int32_t>(rdt);
     a.lr_ptr = o.lr_device;
-    a.bcast_grad = bcast ? 1 : 0;
+    a.literal = literal ? 1 : 0;
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
     FlatPick k{nullptr, 1};
     const bool cached = use_cached_state(n_workers, n);
-    if (!literal)
-        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(a.W, n_groups, cached) : pick_flat<float>(a.W, n_groups, cached);
+    if (W > 0)
+        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(W, n_groups, cached) : pick_flat<float>(W, n_groups, cached);
     if (!k.kernel) {
         // runtime layout: group j is members [start[j], start[j+1]) of the member order
         int32_t max_count = n_groups;
         for (int32_t j = 0; j <= n_groups; ++j) {
-            const int32_t b = literal ? gstart[j] : j * a.W;
+            const int32_t b = literal ? gstart[j] : j * W;
             a.group_start[j] = static_cast<uint8_t>(b);
             if (j > 0) max_count = std::max(max_count, b - static_cast<int32_t>(a.group_start[j - 1]));
         }
-        a.literal = literal ? 1 : 0;
         k = gdt == LSGD_BF16 ? pick_flat_seg<uint16_t>(max_count, cached) : pick_flat_seg<float>(max_count, cached);
     }
     const LaunchShape ls = launch_shape((n + vec - 1) / vec, k.tile);
     a.xcd_chunk = ls.xcd_chunk;
     a.upl = ls.upl;
-    const bool split = separate_copy_out(n_workers, dtype_size(gdt), n_replicas, dtype_size(rdt), n);
+    // Copies per element besides parameters and momentum: the replicas, and
+    // with the broadcast the mean gradient to the other N - 1 members. Split
+    // off, the step kernel writes the mean gradient to the first member only
+    // and copy passes of their own write the rest.
+    const int32_t bcast_copies = bcast ? n_workers - 1 : 0;
+    const bool split = separate_copy_out_bytes(
+        n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n);
+    a.bcast_grad = bcast ? (split ? 1 : n_workers) : 0;
     if (split) a.n_replicas = 0;
     hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), a);
     if ((st = check_launch(literal ? "lsgd_step_ex" : "lsgd_step")) != LSGD_OK || !split) return st;
-    a.n_replicas = n_replicas;
-    return launch_copy_out(a, stream);
+    if (n_replicas > 0) {
+        a.n_replicas = n_replicas;
+        if ((st = launch_copy_out(a, stream)) != LSGD_OK) return st;
+    }
+    if (bcast_copies > 0) {
+        StepArgs b;
+        memset(&b, 0, sizeof b);
+        b.p = static_cast<float*>(const_cast<void*>(a.grads[0]));   // read only by the copy pass
+        b.n = n;
+        b.n_replicas = bcast_copies;
+        b.rdt = static_cast<int32_t>(LSGD_F32);
+        for (int32_t k2 = 0; k2 < bcast_copies; ++k2) b.replicas[k2] = const_cast<void*>(a.grads[k2 + 1]);
+        return launch_copy_out(b, stream);
+    }
+    return LSGD_OK;
 }
 
 LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,

@@ -72,6 +72,9 @@ int32_t launch_passes_per_block();
 // elements writes its replicas in a copy-out pass of its own
 // (lsgd_set_copy_out_mode).
 bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n);
+// The same rule for `copy_bytes` bytes per element of copies (replicas, and
+// the gradient broadcast's copies of the mean gradient to the other members).
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n);
 // The same for lsgd_sgd_step and the LARS update; `cached`: their parameter
 // and momentum accesses go through the caches.
 bool separate_copy_out_update(int32_t n_replicas, size_t rsz, bool cached);

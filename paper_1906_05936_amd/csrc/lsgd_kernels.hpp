@@ -475,8 +475,8 @@ struct StepArgs {
     int32_t n_replicas, rdt;
     uint32_t xcd_chunk, upl;
     const float* lr_ptr;   // non-null: the learning rate is read here when the kernel runs
-    int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
-    int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
+    int32_t bcast_grad;    // write the mean gradient into the first bcast_grad (binary32) member buffers
+    int32_t literal;       // paper-literal reduction (else mean of means)
     int32_t win_blocks;    // replica-major copy-out: workgroups per window and replica group (a multiple of 8)
     int64_t copy_blocks;   // replica-major copy-out: logical workgroups (the grid strides over them)
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
@@ -559,16 +559,18 @@ __device__ __forceinline__ void pw_leaves(const Leaf& leaf, float (&out)[T]) {
     }
 }
 
-// Optional broadcast of the mean gradient into every worker's (binary32)
-// gradient buffer.
+// Optional broadcast of the mean gradient into the (binary32) gradient
+// buffers of the first s.bcast_grad() members: all N when the step kernel
+// writes the whole broadcast, only the first member when a copy pass of its
+// own then copies that buffer to the others.
 template <typename GT, int U, bool TAIL, typename Src>
 __device__ __forceinline__ void broadcast_mean(const Src& s, const int64_t (&e0)[U], int cnt,
                                                float (&gbar)[U * Unit<GT>::VEC]) {
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
     if constexpr (sizeof(GT) == 4) {
-        if (s.bcast_grad()) {
-            const int nw = s.n_workers();
+        const int nw = s.bcast_grad();
+        if (nw > 0) {
             for (int k = 0; k < nw; ++k) {
                 float* g = static_cast<float*>(const_cast<void*>(s.grad(k)));
 #pragma unroll
@@ -673,12 +675,20 @@ __device__ __forceinline__ void finish_tile(const Src& s, const int64_t (&e0)[U]
 // front. Large: groups are streamed GU at a time and folded into a pairwise
 // accumulator over groups, which yields the same PW order. TAIL (the ragged
 // end of a tensor, cnt < VEC elements) only with U = 1.
+// Mean of means: each group's sum / W, then the sum over groups / G. With
+// s.literal() (uniform) the paper-literal form: each group's sum / N = W*G,
+// summed over the groups with no further division. Every divisor is a power
+// of two, so each division is a multiplication by the exact reciprocal (the
+// same rounding of the same exact quotient).
 template <typename GT, int W, int G, int U, bool TAIL, typename Src>
 __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U], int cnt,
                                              float (&gbar)[U * Unit<GT>::VEC]) {
     static_assert(!TAIL || U == 1, "ragged units are processed one at a time");
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
+    const bool lit = s.literal() != 0;
+    const float group_scale = lit ? 1.0f / static_cast<float>(W * G) : 1.0f / static_cast<float>(W);
+    const float total_scale = lit ? 1.0f : 1.0f / static_cast<float>(G);
     auto group_leaf = [&](int j, float (&gm)[T]) {
         auto member_leaf = [&](int k, float (&x)[T]) {
             const void* g = s.grad(j * W + k);
@@ -688,12 +698,12 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
         float sum[T];
         pw_tree<0, W, T>(member_leaf, sum);
 #pragma unroll
-        for (int v = 0; v < T; ++v) gm[v] = sum[v] / static_cast<float>(W);
+        for (int v = 0; v < T; ++v) gm[v] = sum[v] * group_scale;
     };
     float tot[T];
     pw_leaves<G, T, W * T>(group_leaf, tot);
 #pragma unroll
-    for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
+    for (int v = 0; v < T; ++v) gbar[v] = tot[v] * total_scale;
 }
 
 template <typename GT, int W, int G, int U, bool TAIL, typename Src>
@@ -782,15 +792,16 @@ struct FlatSrcT {
     __device__ Hyper hyper() const { return h; }
     __device__ int bcast_grad() const { return a.bcast_grad; }
     __device__ int n_workers() const { return a.n_workers; }
+    __device__ int literal() const { return a.literal; }
     __device__ int cached_state() const { return CACHED; }
 };
 
 // ------------------------------------------------------------- flat kernels
 
-// Grid-stride loop over the full units of a flat vector; the ragged tail
-// (n % VEC elements) is handled by thread 0 of block 0 after its loop.
-// The unit index space is [0, full] with unit `full` the ragged tail
-// (n % VEC elements, present only when that is nonzero).
+// Lane tiles over the units of a flat vector (for_tiles). The unit index space
+// is [0, full] with unit `full` the ragged tail (n % VEC elements, present
+// only when that is nonzero): the lane whose partial tile holds it runs it
+// through the TAIL form of the unit body.
 template <typename GT, int W, int G, int U, int CACHED>
 __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
     constexpr int VEC = Unit<GT>::VEC;

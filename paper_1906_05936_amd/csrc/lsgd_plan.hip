@@ -134,6 +134,8 @@ PlanArgs plan_args(const lsgd_plan* plan, Hyper h, const float* lr_device, Launc
     a.h = h;
     a.lr_ptr = lr_device;
     a.n_buckets = plan->n_buckets;
+    a.copy_src = 0;                              // the copy-out: p to the replicas
+    a.copy_dst = 2 + plan->n_workers;
     for (int32_t j = 0; j <= plan->n_groups; ++j) a.group_start[j] = static_cast<uint8_t>(plan->group_start[j]);
     const int64_t block_bytes = (plan->gdt == LSGD_BF16 ? 2 : 4) * plan->piece;
     ls = pad_for_xcd_chunk(plan->n_buckets, block_bytes);
@@ -152,7 +154,7 @@ lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t
     constexpr int U = 2048 / (VEC * kBlock);
     static_assert(U >= 1, "at least one unit per lane");
     const int64_t win = copy_window_blocks(4 * plan->piece, plan->n_buckets);
-    const int64_t blocks = (plan->n_buckets + win - 1) / win * ((plan->n_replicas + RK - 1) / RK) * win;
+    const int64_t blocks = (plan->n_buckets + win - 1) / win * ((a.n_replicas + RK - 1) / RK) * win;
     a.win_blocks = static_cast<int32_t>(win);
     a.copy_blocks = blocks;
     const int64_t grid = std::min<int64_t>(blocks, stride_grid_cap());   // the kernel strides over the rest
@@ -415,26 +417,45 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     LaunchShape ls;
     PlanArgs a = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
     a.literal = literal ? 1 : 0;
-    a.bcast_grad = bcast ? 1 : 0;
-    PlanKernel k;
-    if (literal || plan->W == 0) {
-        const int32_t max_count = std::max(plan->max_group, plan->n_groups);
-        const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
-        k = plan->gdt == LSGD_BF16 ? plan_seg<uint16_t>(max_count, cached) : plan_seg<float>(max_count, cached);
+    const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
+    // equal groups (W > 0): the compile-time kernels for powers of two, for
+    // either reduction; the segmented kernel otherwise
+    PlanKernel k = nullptr;
+    if (plan->W > 0) {
+        const PlanPick pk = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached)
+                                                   : pick_plan<float>(plan->W, plan->n_groups, cached);
+        k = pk.kernel;
     } else {
-        const bool cached = use_cached_state(plan->n_workers, plan->total_elems);
-        k = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached).kernel
-                                   : pick_plan<float>(plan->W, plan->n_groups, cached).kernel;
+        const int32_t max_count = std::max(plan->max_group, plan->n_groups);
+        k = plan->gdt == LSGD_BF16 ? plan_seg<uint16_t>(max_count, cached) : plan_seg<float>(max_count, cached);
     }
-    const bool split = separate_copy_out(plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4, plan->n_replicas,
-                                         plan->rdt == LSGD_BF16 ? 2 : 4, plan->total_elems);
+    // as for flat steps: the replicas and the broadcast's copies of the mean
+    // gradient to the other N - 1 members go to copy passes of their own
+    // where the rule takes the separate form
+    const int32_t bcast_copies = bcast ? plan->n_workers - 1 : 0;
+    const bool split = separate_copy_out_bytes(
+        plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4,
+        static_cast<int64_t>(plan->n_replicas) * (plan->rdt == LSGD_BF16 ? 2 : 4) + 4 * bcast_copies,
+        plan->total_elems);
+    a.bcast_grad = bcast ? (split ? 1 : plan->n_workers) : 0;
     if (split) a.n_replicas = 0;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, s, a);
     if ((st = check_launch("lsgd_step_plan")) != LSGD_OK || !split) return st;
-    a.n_replicas = plan->n_replicas;
-    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, a, s)
-                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
+    if (plan->n_replicas > 0) {
+        a.n_replicas = plan->n_replicas;
+        st = plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, a, s)
+                                    : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
+        if (st != LSGD_OK) return st;
+    }
+    if (bcast_copies > 0) {   // the first member's gradient (slot 2) to the others (slots 3 ..)
+        a.copy_src = 2;
+        a.copy_dst = 3;
+        a.n_replicas = bcast_copies;
+        a.rdt = static_cast<int32_t>(LSGD_F32);
+        return launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
+    }
+    return LSGD_OK;
 }
 
 LSGD_API lsgd_status lsgd_plan_copy_out(const lsgd_plan* plan, void* stream) {

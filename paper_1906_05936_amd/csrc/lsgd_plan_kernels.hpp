@@ -44,11 +44,13 @@ struct PlanArgs {
     uint32_t xcd_chunk;
     const float* lr_ptr;
     Hyper h;
-    int32_t literal;       // runtime-layout kernel: paper-literal reduction (else mean of means)
-    int32_t bcast_grad;    // write the mean gradient into every (binary32) gradient buffer
+    int32_t literal;       // paper-literal reduction (else mean of means)
+    int32_t bcast_grad;    // write the mean gradient into the first bcast_grad (binary32) member buffers
     int32_t win_blocks;    // replica-major copy-out: buckets per window (a multiple of 8)
     int64_t copy_blocks;   // replica-major copy-out: logical workgroups (the grid strides over them)
     int32_t cached_state;  // LARS update: store parameters and momentum through the caches
+    int32_t copy_src;      // copy-out pass: table slot of its source (0: p; 2: the first member's gradient)
+    int32_t copy_dst;      // copy-out pass: table slot of its first destination (n_replicas of them)
     uint8_t group_start[kMaxWorkers + 4];  // runtime-layout kernel: group j is members [start[j], start[j+1])
 };
 
@@ -67,6 +69,7 @@ struct PlanSrcT {
     __device__ Hyper hyper() const { return h; }
     __device__ int bcast_grad() const { return a.bcast_grad; }
     __device__ int n_workers() const { return a.n_workers; }
+    __device__ int literal() const { return a.literal; }
     __device__ int cached_state() const { return CACHED < 0 ? a.cached_state : CACHED; }
 };
 using PlanSrc = PlanSrcT<-1>;
@@ -142,7 +145,10 @@ __global__ __launch_bounds__(kBlock) void step_plan_seg(PlanArgs a) {
 // copy_out_rmajor_kernel with buckets in place of fixed-size blocks): workgroup
 // b copies bucket w*win_blocks + s to replica group q (RK consecutive
 // replicas), b = (w*ceil(R/RK) + q)*win_blocks + s; a lane loads U units of
-// p, then stores them to each replica of the group.
+// the source, then stores them to each destination of the group. The source
+// is table slot copy_src of each tensor (p for the copy-out of the replicas;
+// the first member's gradient for the copy pass of the gradient broadcast),
+// the R destinations slots copy_dst .. copy_dst + R - 1.
 // One piece [start, start+len) of a tensor to the nr replicas in dst.
 template <int VEC, int U, int RK>
 __device__ __forceinline__ void copy_out_piece(const float* p, void* const (&dst)[RK], int nr, int rdt,
@@ -189,8 +195,8 @@ __device__ __forceinline__ void copy_out_plan_block(const PlanArgs& a, int64_t b
         void* const* t = a.ptrs + static_cast<int64_t>(read_table(&d->tensor)) * a.stride;
         void* dst[RK];
 #pragma unroll
-        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[2 + a.n_workers + r0 + k]) : nullptr;
-        const float* p = read_table(&d->p);
+        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[a.copy_dst + r0 + k]) : nullptr;
+        const float* p = a.copy_src == 0 ? read_table(&d->p) : static_cast<const float*>(read_table(&t[a.copy_src]));
         const int64_t start = read_table(&d->start), len = read_table(&d->len);
         const int64_t full = len / VEC;
         const int rem = static_cast<int>(len - full * VEC);
@@ -225,8 +231,8 @@ __device__ __forceinline__ void copy_out_plan_block(const PlanArgs& a, int64_t b
         void* const* t = a.ptrs + static_cast<int64_t>(read_table(&cp->tensor)) * a.stride;
         void* dst[RK];
 #pragma unroll
-        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[2 + a.n_workers + r0 + k]) : nullptr;
-        copy_out_piece<VEC, U, RK>(static_cast<const float*>(read_table(&t[0])), dst, nr, a.rdt,
+        for (int k = 0; k < RK; ++k) dst[k] = k < nr ? read_table(&t[a.copy_dst + r0 + k]) : nullptr;
+        copy_out_piece<VEC, U, RK>(static_cast<const float*>(read_table(&t[a.copy_src])), dst, nr, a.rdt,
                                    read_table(&cp->start), read_table(&cp->len));
     }
 }

@@ -32,12 +32,23 @@ def check_common(b):
     rl = b["roofline"]
     assert rl["bound"] == "hbm" and rl["peak"] == 8000.0 and rl["unit"] == "GB/s"
     assert abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-3
+    reps = b["repeats_ms_per_step"]     # five timed loops of K steps; the line reports their median
+    assert len(reps) == 5 and abs(b["ms_per_step"] - sorted(reps)[2]) < 1e-6
 
 
 def test_bench_default_line():
     b = run_bench("--no-r0")
     check_common(b)
     assert b["config"]["workload"] == "tiny" and b["config"]["copy_out"] == "in the step kernel"
+    cold = b["cold_cache"]       # a cache flush before every timed step
+    assert cold["ms_per_step"] > 0 and len(cold["repeats_ms_per_step"]) == 5
+
+
+def test_bench_broadcast_and_literal_variants():
+    b = run_bench("--no-r0", "--no-cold", "--broadcast-grad", "--reduction", "literal")
+    check_common(b)
+    assert b["config"]["reduction"] == "literal" and b["config"]["broadcast_grad"]
+    assert b["roofline"]["kernel"].startswith("step_flat_ct")
 
 
 def test_bench_split_step_reports_the_dominant_kernel():

@@ -4,9 +4,12 @@ against the CPU oracle (oracle_lars_step, one tensor at a time).
 Bar: each tensor's trust ratio within one binary32 ulp of the oracle's (both
 evaluate the norms in binary64 and round once; the GPU sums in a blocked
 order, the oracle sequentially, so a ratio may differ in its last bit in rare
-cases). Where the trust ratios agree bit for bit, parameters, momentum and
-replicas are bit-exact; otherwise the contract tolerance
-|gpu - ref| <= 1e-6*|ref| + 1e-6*rms(ref) applies.
+cases) and within one ulp of the exact ratio (exact sums of squares, 60-digit
+square roots and division). Where the trust ratios agree bit for bit,
+parameters, momentum and replicas are bit-exact; otherwise the contract
+tolerance |gpu - ref| <= 1e-6*|ref| + 1e-6*rms(ref) applies, and that
+tensor's GPU state is then reset to the oracle's, so that every step starts
+both sides from the oracle's trajectory.
 """
 import sys
 
@@ -14,6 +17,7 @@ import numpy as np
 import pytest
 import torch
 
+import fullsize
 import oracle
 import workloads
 
@@ -64,6 +68,24 @@ def ulps(a, b):
     return abs(int(np.float32(a).view(np.int32)) - int(np.float32(b).view(np.int32)))
 
 
+def oracle_gbar(grads_h, gow, G):
+    """The oracle's binary32 mean gradient of one tensor (mean of means)."""
+    return oracle.global_mean(oracle.group_means(grads_h, gow, G))
+
+
+def check_exact_trust(t_gpu, p_before, gbar, wd, eta, what):
+    """The GPU trust ratio within one binary32 ulp of the exact ratio."""
+    exact = fullsize.trust_60_digits(p_before, gbar, wd, eta)
+    assert fullsize.within_one_ulp(t_gpu, exact), "%s: trust %r, exact %s" % (what, t_gpu, exact)
+
+
+def reset_to_oracle(params_t, mom_t, ph_t, mh_t):
+    """After a one-ulp trust difference: the GPU tensor continues from the
+    oracle's state (the oracle's trajectory is never taken from the GPU)."""
+    params_t.copy_(to_dev(ph_t))
+    mom_t.copy_(to_dev(mh_t))
+
+
 # Mixed sizes: ragged ends, single elements, several pieces, an empty tensor;
 # tensor ZERO_P starts at p = 0 and tensor ZERO_G gets zero gradients (trust 1).
 SIZES = [1, 3, 64, 1000, 8191, 8193, 0, 20_000, 5, 4096, 9408, 16_385, 70_001]
@@ -102,8 +124,11 @@ class Case:
         exact = 0
         for t, s in enumerate(SIZES):
             rr = [np.zeros(s, np.uint16 if self.rdt == "bf16" else np.float32) for _ in range(self.R)]
-            tr = oracle.lars_step(self.ph[t], self.mh[t], [self.gh[w][t] for w in range(self.N)],
-                                  self.gow, self.G, lr, mu, wd, eta, rr,
+            g_t = [self.gh[w][t] for w in range(self.N)]
+            if s:
+                check_exact_trust(tg[t], self.ph[t], oracle_gbar(g_t, self.gow, self.G), wd, eta,
+                                  "tensor %d step %d" % (t, step))
+            tr = oracle.lars_step(self.ph[t], self.mh[t], g_t, self.gow, self.G, lr, mu, wd, eta, rr,
                                   oracle.BF16 if self.rdt == "bf16" else oracle.F32)
             assert ulps(tg[t], tr) <= 1, "tensor %d step %d: trust %r vs %r" % (t, step, tg[t], tr)
             if t == ZERO_G or s == 0 or (t == ZERO_P and step == 0):   # p = 0 only before the first update
@@ -118,9 +143,7 @@ class Case:
             else:
                 close(pg, self.ph[t], "params[%d] step %d" % (t, step))
                 close(mg, self.mh[t], "momentum[%d] step %d" % (t, step))
-                # keep following the GPU's state so later steps compare like with like
-                self.ph[t][:] = pg
-                self.mh[t][:] = mg
+                reset_to_oracle(self.params[t], self.mom[t], self.ph[t], self.mh[t])
         log("  step %d: %d of %d trust ratios bit-equal" % (step, exact, len(SIZES)))
 
 
@@ -151,6 +174,41 @@ def test_lars_copy_out_modes(mode, R, rdt):
         c.plan.close()
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+
+
+def test_lars_results_independent_of_launch_shape_for_one_plan():
+    """One plan (its pieces, hence the order of its norm sums, fixed at
+    creation): the LARS step gives the same trust ratios, parameters, momentum
+    and replicas whatever the XCD renumbering and the copy-out grid cap at
+    step time."""
+    c = Case(4, 4, "f32", 5, "f32", seed=57)
+    c.new_grads()
+    p0 = [x.clone() for x in c.params]
+    m0 = [x.clone() for x in c.mom]
+    default = lsgd.get_launch_shape()
+    outs = []
+    try:
+        for sh in [(-1, 0, 1), (0, 0, 1), (4, 0, 1), (2, 3, 1)]:
+            lsgd.set_launch_shape(*sh)
+            for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE):
+                lsgd.set_copy_out_mode(mode)
+                for t in range(len(SIZES)):
+                    c.params[t].copy_(p0[t])
+                    c.mom[t].copy_(m0[t])
+                trust = torch.empty(len(SIZES), device=DEV)
+                c.plan.lars_step(0.1, 0.9, 1e-4, TRUST_COEF, trust_out=trust)
+                torch.cuda.synchronize()
+                outs.append(((sh, mode), trust.clone(), [x.clone() for x in c.params],
+                             [x.clone() for x in c.mom], [x.clone() for x in c.reps[c.R - 1]]))
+    finally:
+        lsgd.set_launch_shape(*default)
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+    for key, trust, ps, ms, rs in outs[1:]:
+        assert torch.equal(trust, outs[0][1]), key
+        for t in range(len(SIZES)):
+            assert torch.equal(ps[t], outs[0][2][t]) and torch.equal(ms[t], outs[0][3][t]), (key, t)
+            assert torch.equal(rs[t], outs[0][4][t]), (key, t)
+    c.plan.close()
 
 
 def test_lars_special_coefficients():
@@ -195,8 +253,10 @@ def test_lars_full_size_resnet50_tensors():
         exact = 0
         for t, s in enumerate(sizes):
             rr = [np.zeros(s, np.float32) for _ in range(R)]
-            tr = oracle.lars_step(ph[t], mh[t], [g[offs[t]:offs[t + 1]] for g in gh], gow, G,
-                                  wl.lr, wl.mu, wl.wd, TRUST_COEF, rr)
+            g_t = [g[offs[t]:offs[t + 1]] for g in gh]
+            check_exact_trust(tg[t], ph[t], oracle_gbar(g_t, gow, G), wl.wd, TRUST_COEF,
+                              "tensor %d step %d" % (t, step))
+            tr = oracle.lars_step(ph[t], mh[t], g_t, gow, G, wl.lr, wl.mu, wl.wd, TRUST_COEF, rr)
             assert ulps(tg[t], tr) <= 1, (t, step, tg[t], tr)
             pg, mg = to_host(params[t]), to_host(mom[t])
             if np.float32(tg[t]) == np.float32(tr):
@@ -206,8 +266,7 @@ def test_lars_full_size_resnet50_tensors():
             else:
                 close(pg, ph[t], "params[%d]" % t)
                 close(mg, mh[t], "momentum[%d]" % t)
-                ph[t][:] = pg
-                mh[t][:] = mg
+                reset_to_oracle(params[t], mom[t], ph[t], mh[t])
         log("  resnet50 step %d: %d of %d trust ratios bit-equal" % (step, exact, len(sizes)))
     plan.close()
 
@@ -239,8 +298,10 @@ def test_lars_above_the_cache_limit():
         tg = to_host(trust)
         for t, s in enumerate(sizes):
             rr = [np.zeros(s, np.float32) for _ in range(R)]
-            tr = oracle.lars_step(ph[t], mh[t], [gh[w][t] for w in range(N)], gow, G, 0.1, 0.9, 1e-4,
-                                  TRUST_COEF, rr)
+            g_t = [gh[w][t] for w in range(N)]
+            check_exact_trust(tg[t], ph[t], oracle_gbar(g_t, gow, G), 1e-4, TRUST_COEF,
+                              "tensor %d step %d" % (t, step))
+            tr = oracle.lars_step(ph[t], mh[t], g_t, gow, G, 0.1, 0.9, 1e-4, TRUST_COEF, rr)
             assert ulps(tg[t], tr) <= 1, (t, step, tg[t], tr)
             pg, mg = to_host(params[t]), to_host(mom[t])
             if np.float32(tg[t]) == np.float32(tr):
@@ -250,8 +311,7 @@ def test_lars_above_the_cache_limit():
             else:
                 close(pg, ph[t], "params[%d]" % t)
                 close(mg, mh[t], "momentum[%d]" % t)
-                ph[t][:] = pg
-                mh[t][:] = mg
+                reset_to_oracle(params[t], mom[t], ph[t], mh[t])
         log("  step %d ok" % step)
     plan.close()
 

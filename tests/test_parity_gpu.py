@@ -6,10 +6,12 @@ and the oracle use the same pairwise order and the same binary32 operations);
 the contract tolerance |gpu - ref| <= 1e-6*|ref| + 1e-6*rms(ref) is asserted
 as well. Replicas and all indexing are bit-exact.
 
-Sizes: small shapes that span several workgroups and end ragged (compared
-element by element), and the five workloads at full size in the launch
-configuration the benchmark times (sampled elements, which the oracle computes
-one by one; every element is independent of the others).
+Sizes: small shapes that span several workgroups and end ragged, shapes large
+enough that the kernels renumber their workgroups across the XCDs (every
+grid the benchmark's workloads launch is renumbered), and the five workloads at
+full size in the launch configuration the benchmark times: every element of
+the first steps, and sampled elements over the full step count (every element
+is independent of the others).
 """
 import os
 import sys
@@ -18,6 +20,7 @@ import numpy as np
 import pytest
 import torch
 
+import fullsize
 import oracle
 import workloads
 
@@ -101,6 +104,13 @@ STEP_CASES = [
     (1, 100, "f32", 777, 0, "f32", "contiguous"),
     (128, 1, "bf16", 513, 1, "f32", "shuffled"),
     (6, 7, "bf16", 2_050, 42, "bf16", "shuffled"),
+    # XCD-renumbered grids (the chunked, padded launch the workloads take):
+    # 4x4 fp32 two-unit tiles cover 2048 elements per workgroup, chunk 64, from
+    # 512 workgroups; 8x8 bf16 one-unit tiles 2048, chunk 128, from 1024; 16x8
+    # fp32 four-unit tiles 4096, chunk 32, from 256. Ragged ends in each.
+    (4, 4, "f32", 2_000_003, 16, "f32", "contiguous"),
+    (8, 8, "bf16", 4_000_003, 64, "bf16", "shuffled"),
+    (16, 8, "f32", 2_000_003, 128, "f32", "shuffled"),
 ]
 
 
@@ -401,6 +411,96 @@ def test_workload_full_size_sampled(name):
     torch.cuda.empty_cache()
 
 
+# Steps compared element by element at full size (every element of p, m and
+# of replicas 0 and R-1; all R replicas against replica 0 on the device).
+FULL_COMPARE_STEPS = {"tiny": 10, "resnet50_flat": 3, "resnet50_tensors": 3, "wide": 1, "large": 1,
+                      "resnet50_unequal": 3}
+
+
+@pytest.mark.parametrize("name", workloads.ORDER + ["resnet50_unequal"])
+def test_workload_full_size_every_element(name):
+    """Each workload at its full size, R = N replicas, in the benchmark's launch
+    configuration, against the oracle on every element: the oracle runs block
+    by block over the host threads (elements are independent, so the blocks
+    give the bits of one call over the whole vector). Inputs are regenerated
+    every step. Unequal subgroups take the paper-literal reduction."""
+    wl = workloads.WORKLOADS[name]
+    steps = FULL_COMPARE_STEPS[name]
+    N, G = wl.n_workers, wl.groups
+    T = fullsize.host_threads()
+    log("workload %s every element: n=%d N=%d %s, %d step(s), %d host threads"
+        % (name, wl.n, N, wl.grad_dtype, steps, T))
+    gow = wl.group_of_worker()
+    literal = bool(wl.group_sizes)
+    bf16_rep = wl.replica_dtype == "bf16"
+    rtd = torch.bfloat16 if bf16_rep else torch.float32
+    R = N
+    flat_p = workloads.init_params(wl, DEV)
+    if wl.tensor_sizes:
+        params = workloads.split_tensors(flat_p, wl.tensor_sizes)
+        del flat_p
+        mom = [torch.zeros_like(x) for x in params]
+        grads = [[torch.empty(s, device=DEV, dtype=wl.torch_grad_dtype) for s in wl.tensor_sizes]
+                 for _ in range(N)]
+        reps = [[torch.empty(s, device=DEV, dtype=rtd) for s in wl.tensor_sizes] for _ in range(R)]
+        plan = lsgd.Plan(params, mom, grads, gow, G, reps)
+        offs = np.cumsum([0] + list(wl.tensor_sizes))
+        flat_tmp = torch.empty(wl.n, device=DEV, dtype=wl.torch_grad_dtype)
+    else:
+        params, mom = [flat_p], [torch.zeros_like(flat_p)]
+        grads = [[torch.empty(wl.n, device=DEV, dtype=wl.torch_grad_dtype)] for _ in range(N)]
+        reps = [[torch.empty(wl.n, device=DEV, dtype=rtd)] for _ in range(R)]
+        plan = None
+    scratch = torch.empty(max(wl.tensor_sizes or (wl.n,)), device=DEV) if wl.grad_dtype == "bf16" else None
+    vp, vm = fullsize.FlatView(params), fullsize.FlatView(mom)
+    vg = [fullsize.FlatView(g) for g in grads]
+    vr0, vrl = fullsize.FlatView(reps[0]), fullsize.FlatView(reps[R - 1])
+    p_ref = vp.range(0, wl.n).copy()
+    m_ref = np.zeros(wl.n, np.float32)
+    # element blocks of at most about 2 GB of host copies
+    per_elem = N * wl.grad_bytes + 16 + 2 * (2 if bf16_rep else 4)
+    block = int(min(wl.n, max(1 << 20, (2 << 30) // per_elem)))
+    ref_step = oracle.lsgd_step_literal if literal else oracle.lsgd_step
+    rdt = oracle.BF16 if bf16_rep else oracle.F32
+    for step in range(steps):
+        for w in range(N):
+            if wl.tensor_sizes:
+                workloads.fill_worker_grad(wl, step, w, flat_tmp)
+                for t in range(len(wl.tensor_sizes)):
+                    grads[w][t].copy_(flat_tmp[offs[t]:offs[t + 1]])
+            else:
+                workloads.fill_worker_grad(wl, step, w, grads[w][0], scratch)
+        if plan is not None:
+            plan.step(wl.lr, wl.mu, wl.wd)
+        else:
+            lsgd.step(params[0], mom[0], [g[0] for g in grads], gow, G, wl.lr, wl.mu, wl.wd,
+                      [r[0] for r in reps], reduction="literal" if literal else "mean_of_means")
+        torch.cuda.synchronize()
+        for r in range(1, R):          # every replica equals replica 0, bit for bit
+            for t in range(len(reps[0])):
+                assert torch.equal(reps[r][t], reps[0][t]), "%s replica %d tensor %d step %d" % (name, r, t, step)
+        for lo in range(0, wl.n, block):
+            hi = min(wl.n, lo + block)
+            g_h = [v.range(lo, hi) for v in vg]
+            rr = np.zeros(hi - lo, np.uint16 if bf16_rep else np.float32)
+            pb, mb = p_ref[lo:hi], m_ref[lo:hi]
+
+            def run(a, b):
+                ref_step(pb[a:b], mb[a:b], [x[a:b] for x in g_h], gow, G, wl.lr, wl.mu, wl.wd, [rr[a:b]], rdt)
+            fullsize.run_blocks(run, hi - lo, T)
+            where = "%s step %d elements [%d, %d)" % (name, step, lo, hi)
+            assert_close(vp.range(lo, hi), pb, "params " + where)
+            assert_close(vm.range(lo, hi), mb, "momentum " + where)
+            assert np.array_equal(vr0.range(lo, hi), rr), "replica 0 " + where
+            assert np.array_equal(vrl.range(lo, hi), rr), "replica %d %s" % (R - 1, where)
+            del g_h
+        log("  %s step %d: all %d elements equal the oracle" % (name, step, wl.n))
+    if plan is not None:
+        plan.close()
+    del params, mom, grads, reps
+    torch.cuda.empty_cache()
+
+
 def test_results_independent_of_launch_shape():
     """Every launch shape (XCD chunking, grid-stride caps, units per lane) gives
     the same bits: each element is computed by one lane from its own inputs."""
@@ -529,6 +629,13 @@ LITERAL_CASES = [
     ([0] * 5 + [1], 2, "f32", 7, 1, True),
     (list(range(7)), 7, "f32", 3_001, 0, False),
     ([0, 0, 0, 1, 1, 2] * 20, 3, "f32", 4_099, 3, True),
+    # equal power-of-two groups: the compile-time kernels, on XCD-renumbered
+    # grids, with the replicas and the broadcast in copy passes of their own
+    ("shuffled4x4", 4, "f32", 2_000_003, 16, False),
+    ("shuffled4x4", 4, "f32", 2_000_003, 16, True),
+    ("shuffled4x4", 4, "f32", 33_333, 2, True),
+    ("contiguous8x8", 8, "bf16", 100_003, 2, False),
+    ("contiguous2x2", 2, "f32", 1_000_001, 1, True),
 ]
 
 
@@ -536,6 +643,9 @@ LITERAL_CASES = [
 def test_literal_reduction_matches_oracle(gow, G, gdt, n, R, bcast):
     if gow == "shuffled4x4":
         gow = workloads.shuffled_groups(4, 4, seed=9)
+    elif isinstance(gow, str) and gow.startswith("contiguous"):
+        g, w = (int(x) for x in gow[len("contiguous"):].split("x"))
+        gow = workloads.contiguous_groups(g, w)
     log("literal G=%d N=%d %s n=%d R=%d bcast=%s" % (G, len(gow), gdt, n, R, bcast))
     rng = np.random.default_rng(n + G)
     gh = [rand_host(rng, n, 1e-2, gdt) for _ in range(len(gow))]
@@ -555,6 +665,67 @@ def test_literal_reduction_matches_oracle(gow, G, gdt, n, R, bcast):
         assert np.array_equal(to_host(reps[r]), rr[r])
     for w in range(len(gow)):
         assert np.array_equal(to_host(grads[w]), gw[w]), w   # broadcast target (or untouched)
+
+
+def extreme_grads(rng, n, N, gdt):
+    """Gradients at the ends of the binary32 range, one regime per element for
+    all workers: small integer multiples of the smallest subnormal (where a
+    group's sum / N and the mean of means round differently), values near the
+    overflow threshold (where some sums overflow), and ordinary values."""
+    out = []
+    kind = rng.integers(0, 3, n)
+    for _ in range(N):
+        sub = (rng.integers(-6, 7, n).astype(np.float64) * 2.0 ** -149).astype(np.float32)
+        big = (rng.choice([-1.0, 1.0], n) * rng.uniform(0.6e38, 1.7e38, n)).astype(np.float32)
+        mid = (rng.standard_normal(n) * 1e-2).astype(np.float32)
+        x = np.where(kind == 0, sub, np.where(kind == 1, big, mid)).astype(np.float32)
+        out.append(oracle.f32_to_bf16(x) if gdt == "bf16" else x)
+    return out
+
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+def test_literal_power_of_two_groups_at_range_extremes(gdt):
+    """The paper-literal reduction on equal power-of-two groups (the
+    compile-time kernels, flat and plan) with subnormal and near-overflow
+    gradients: bit-exact against the oracle's literal step. With binary32
+    gradients that step differs from the mean of means on some of these
+    elements (division by N against division by W then G, where the quotient
+    is subnormal); bfloat16 subnormals are multiples of 2^-133, whose
+    quotients by 16 are exact in binary32, so there the two agree."""
+    G, W, n = 4, 4, 65_541
+    N = G * W
+    rng = np.random.default_rng(2024 + len(gdt))
+    gow = workloads.shuffled_groups(G, W, seed=11)
+    gh = extreme_grads(rng, n, N, gdt)
+    p0 = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    lit = oracle.lsgd_step_literal
+    p_lit, m_lit = p0.copy(), np.zeros(n, np.float32)
+    rr = [np.zeros(n, np.float32)]
+    lit(p_lit, m_lit, [x.copy() for x in gh], gow, G, 0.5, 0.0, 0.0, rr)
+    p_mom, m_mom = p0.copy(), np.zeros(n, np.float32)
+    oracle.lsgd_step(p_mom, m_mom, gh, gow, G, 0.5, 0.0, 0.0)
+    differ = np.count_nonzero(m_lit.view(np.uint32) != m_mom.view(np.uint32))
+    log("literal vs mean of means (%s): %d of %d mean gradients differ" % (gdt, differ, n))
+    assert differ > 0 or gdt == "bf16"
+    grads = [to_dev(x) for x in gh]
+    p, m = to_dev(p0), torch.zeros(n, device=DEV)
+    reps = [torch.empty(n, device=DEV)]
+    lsgd.step(p, m, grads, gow, G, 0.5, 0.0, 0.0, reps, reduction="literal")
+    torch.cuda.synchronize()
+    assert_close(to_host(p), p_lit, "params")
+    assert_close(to_host(m), m_lit, "momentum")
+    assert_close(to_host(reps[0]), rr[0], "replica")   # NaN where inf - inf: compared as NaN
+    # the same elements as two plan tensors
+    cut = 40_000
+    pt = [to_dev(p0[:cut]), to_dev(p0[cut:])]
+    mt = [torch.zeros(cut, device=DEV), torch.zeros(n - cut, device=DEV)]
+    gt = [[to_dev(x[:cut]), to_dev(x[cut:])] for x in gh]
+    plan = lsgd.Plan(pt, mt, gt, gow, G)
+    plan.step(0.5, 0.0, 0.0, reduction="literal")
+    torch.cuda.synchronize()
+    assert_close(np.concatenate([to_host(x) for x in pt]), p_lit, "plan params")
+    assert_close(np.concatenate([to_host(x) for x in mt]), m_lit, "plan momentum")
+    plan.close()
 
 
 @pytest.mark.parametrize("G,W", [(4, 4), (3, 5), (2, 16)])
@@ -798,6 +969,8 @@ def test_graph_with_separate_copy_out_matches_eager():
     ([2, 0, 1, 1, 0, 2, 1], 3, "bf16", 2, False),
     ([0, 0, 1, 1, 1, 2, 2, 2, 2, 2, 3, 3, 3, 3, 3, 3], 4, "f32", 1, True),
     (workloads.contiguous_groups(4, 4), 4, "f32", 16, True),
+    (workloads.shuffled_groups(4, 4, 6), 4, "f32", 2, True),
+    (workloads.shuffled_groups(2, 4, 7), 2, "bf16", 3, False),
 ])
 def test_plan_literal_reduction_and_broadcast_match_oracle(gow, G, gdt, R, bcast):
     """Plans over any partition take the paper-literal reduction, optionally
@@ -840,9 +1013,8 @@ def test_plan_literal_reduction_and_broadcast_match_oracle(gow, G, gdt, R, bcast
             assert_close(to_host(mom[t]), mh[t], "momentum[%d] step %d" % (t, step))
             for r in range(R):
                 assert np.array_equal(to_host(reps[r][t]), rr[r]), (t, r)
-            if bcast:
-                for w in (0, N - 1):
-                    assert np.array_equal(to_host(grads[w][t]), gt[w]), (t, w)
+            for w in range(N):   # the broadcast's targets, or untouched
+                assert np.array_equal(to_host(grads[w][t]), gt[w]), (t, w)
     plan.close()
 
 
