@@ -399,6 +399,32 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
                                          size_t workspace_bytes, float* trust_out,
                                          const float* lr_device, void* stream);
 
+/*
+ * lsgd_lars_step_plan without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc. The scratch that lsgd_lars_step_plan keeps in the
+ * caller's workspace (the mean gradient, the partial norms and the trust
+ * ratios) lives instead in an array owned by the library, of
+ * LSGD_NOALLOC_SCRATCH_BYTES (128 MiB) on each device, which each device the
+ * call runs on holds until the process ends. The call makes no allocation
+ * (no hipMalloc, no host heap), launches the same kernels and gives the same
+ * results, bit for bit. Plans whose lsgd_lars_workspace_size exceeds
+ * LSGD_NOALLOC_SCRATCH_BYTES (about 33 million elements; ResNet-50's 25.6
+ * million fit) are rejected with LSGD_ERR_SIZE and nothing is launched. Every
+ * call on one device uses that device's one array and leaves its contents
+ * there; no call needs them (every byte a call reads is written earlier in
+ * the same call), but calls whose kernels may overlap on one device (other
+ * streams, other host threads) race on it: order them on one stream. The
+ * first call on a device looks the array up there (hipGetSymbolAddress; a
+ * failure is LSGD_ERR_HIP). Other arguments and errors as
+ * lsgd_lars_step_plan; trust_out and lr_device may not overlap the plan's
+ * written buffers (LSGD_ERR_ALIAS).
+ */
+#define LSGD_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+LSGD_API lsgd_status lsgd_lars_step_plan_noalloc(const lsgd_plan* plan, float lr, float momentum_coef,
+                                                 float weight_decay, float trust_coef, float* trust_out,
+                                                 const float* lr_device, void* stream);
+
 /* Tensors excluded from the layer-wise rates: exclude[t] != 0 gives tensor t
  * trust 1 in every later lsgd_lars_step_plan (so its update is the plain
  * step of lsgd_step_plan); NULL clears every exclusion. Implementations

@@ -33,7 +33,8 @@ EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
            "lsgd_lars_workspace_size", "lsgd_lars_step_plan", "lsgd_set_copy_out_mode",
            "lsgd_get_copy_out_mode", "lsgd_plan_set_lars_exclude", "lsgd_copy_out",
-           "lsgd_plan_copy_out")
+           "lsgd_plan_copy_out", "lsgd_lars_step_plan_noalloc")
+NOALLOC_SCRATCH_BYTES = 128 << 20      # LSGD_NOALLOC_SCRATCH_BYTES
 
 
 class StepOptions(ctypes.Structure):
@@ -90,6 +91,7 @@ def _load():
     lib.lsgd_plan_set_lars_exclude.argtypes = [P, P]
     lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
     lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P, P]
+    lib.lsgd_lars_step_plan_noalloc.argtypes = [P, f32, f32, f32, f32, P, P, P]
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_copy_out", "lsgd_plan_copy_out",
                  "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
@@ -440,6 +442,26 @@ class Plan:
             st = lib.lsgd_lars_step_plan(self._handle, lr, momentum_coef, weight_decay, trust_coef,
                                          workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                          tp, lp, _stream(stream, self.device))
+        check(st)
+
+    def lars_step_noalloc(self, lr, momentum_coef, weight_decay, trust_coef, trust_out=None, stream=None,
+                          lr_device=None):
+        """lsgd_lars_step_plan_noalloc: lars_step with the library's own
+        per-device scratch (at most NOALLOC_SCRATCH_BYTES) instead of a
+        workspace; the call allocates nothing."""
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        tp = None
+        if trust_out is not None:
+            _dev_tensor(trust_out, "trust_out", torch.float32, len(self._keep[0]), self.device)
+            tp = trust_out.data_ptr()
+        lp = None
+        if lr_device is not None:
+            _dev_tensor(lr_device, "lr_device", torch.float32, 1, self.device)
+            lp = lr_device.data_ptr()
+        with torch.cuda.device(self.device):
+            st = lib.lsgd_lars_step_plan_noalloc(self._handle, lr, momentum_coef, weight_decay, trust_coef, tp,
+                                                 lp, _stream(stream, self.device))
         check(st)
 
     def close(self):

@@ -100,4 +100,12 @@ int device_cus();
 
 inline bool is_pow2_le16(int x) { return x == 1 || x == 2 || x == 4 || x == 8 || x == 16; }
 
+// lsgd_lars_step_plan with its scratch at `workspace` (workspace_bytes long);
+// `library_workspace`: the scratch is the library's own per-device array
+// (lsgd_lars_step_plan_noalloc), which no caller buffer can overlap, and the
+// call then makes no host allocation either.
+lsgd_status lars_step(const lsgd_plan* plan, float lr, float momentum_coef, float weight_decay, float trust_coef,
+                      void* workspace, size_t workspace_bytes, bool library_workspace, float* trust_out,
+                      const float* lr_device, void* stream);
+
 }  // namespace lsgd

@@ -222,6 +222,88 @@ void free_plan(lsgd_plan* p) {
 }
 
 }  // namespace
+
+// The LARS step of a plan with its scratch at `workspace`. A caller-owned
+// workspace is checked for size, alignment and overlap with every buffer of
+// the call; a library-owned one (`library_workspace`, the per-device array of
+// lsgd_lars_step_plan_noalloc) cannot overlap caller memory, and then the
+// call also allocates nothing on the host: trust_out and lr_device are
+// checked against the plan's ranges one by one.
+lsgd_status lars_step(const lsgd_plan* plan, float lr, float momentum_coef, float weight_decay, float trust_coef,
+                      void* workspace, size_t workspace_bytes, bool library_workspace, float* trust_out,
+                      const float* lr_device, void* stream) {
+    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
+    if (!workspace) return fail(LSGD_ERR_NULL, "workspace is NULL");
+    const LarsLayout l = lars_layout(plan);
+    if (workspace_bytes < l.total)
+        return fail(LSGD_ERR_SIZE, "workspace_bytes=%zu < %zu (lsgd_lars_workspace_size)", workspace_bytes, l.total);
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return fail(LSGD_ERR_ALIGN, "workspace is not 256-byte aligned");
+    if (trust_out && (reinterpret_cast<uintptr_t>(trust_out) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "trust_out is not 4-byte aligned");
+    if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
+        return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
+    const uintptr_t tb = reinterpret_cast<uintptr_t>(trust_out);
+    const uintptr_t te = tb + static_cast<uintptr_t>(plan->n_tensors) * sizeof(float);
+    const uintptr_t lb = reinterpret_cast<uintptr_t>(lr_device);
+    const uintptr_t le = lb + sizeof(float);
+    lsgd_status st = LSGD_OK;
+    if (library_workspace) {
+        auto overlaps = [](uintptr_t b0, uintptr_t e0, uintptr_t b1, uintptr_t e1) { return b0 < e1 && b1 < e0; };
+        if (trust_out && lr_device && overlaps(tb, te, lb, le))
+            return fail(LSGD_ERR_ALIAS, "written buffer trust_out overlaps lr_device");
+        for (const Range& r : *plan->ranges) {
+            if (trust_out && overlaps(tb, te, r.begin, r.end))
+                return fail(LSGD_ERR_ALIAS, "written buffer trust_out overlaps %s", r.what);
+            if (lr_device && r.written && overlaps(lb, le, r.begin, r.end))
+                return fail(LSGD_ERR_ALIAS, "buffer lr_device overlaps written buffer %s", r.what);
+        }
+    } else {
+        std::vector<Range> ranges(*plan->ranges);
+        const uintptr_t wb = reinterpret_cast<uintptr_t>(workspace);
+        ranges.push_back(Range{wb, wb + l.total, true, "workspace"});
+        if (trust_out) ranges.push_back(Range{tb, te, true, "trust_out"});
+        if (lr_device) ranges.push_back(Range{lb, le, false, "lr_device"});
+        if ((st = check_overlap(ranges)) != LSGD_OK) return st;
+    }
+    if (plan->W == 0) return fail(LSGD_ERR_GROUPS, "the LARS step needs equal group sizes; this plan's differ");
+    if ((st = check_device(plan)) != LSGD_OK) return st;
+
+    LarsArgs la;
+    memset(&la, 0, sizeof la);
+    LaunchShape ls;
+    la.pa = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
+    la.gbar_off = plan->d_gbar_off;
+    la.tensor_chunks = plan->d_tensor_chunks;
+    char* ws = static_cast<char*>(workspace);
+    la.gbar = reinterpret_cast<float*>(ws + l.gbar);
+    la.partials = reinterpret_cast<double*>(ws + l.partials);
+    la.trust = reinterpret_cast<float*>(ws + l.trust);
+    la.trust_out = trust_out;
+    la.exclude = plan->d_lars_exclude;
+    la.n_tensors = plan->n_tensors;
+    la.trust_coef = trust_coef;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (plan->n_buckets > 0) {
+        const LarsKernel k1 = plan->gdt == LSGD_BF16 ? pick_lars<uint16_t>(plan->W, plan->n_groups)
+                                                     : pick_lars<float>(plan->W, plan->n_groups);
+        hipLaunchKernelGGL(k1, dim3(ls.blocks), dim3(kBlock), 0, s, la);
+        if ((st = check_launch("lsgd_lars_step_plan (norms)")) != LSGD_OK) return st;
+    }
+    hipLaunchKernelGGL(lars_trust_kernel, dim3(plan->n_tensors), dim3(kBlock), 0, s, la);
+    if ((st = check_launch("lsgd_lars_step_plan (trust)")) != LSGD_OK) return st;
+    if (plan->n_buckets == 0) return LSGD_OK;
+    // the update reads and writes as lsgd_sgd_step does: the same copy-out rule
+    const bool split = separate_copy_out_update(plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,
+                                                use_cached_state(plan->n_workers, plan->total_elems));
+    if (split) la.pa.n_replicas = 0;
+    hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
+    if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK || !split) return st;
+    la.pa.n_replicas = plan->n_replicas;
+    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, la.pa, s)
+                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, la.pa, s);
+}
+
 }  // namespace lsgd
 
 using namespace lsgd;
@@ -486,66 +568,8 @@ LSGD_API lsgd_status lsgd_lars_step_plan(const lsgd_plan* plan, float lr, float 
                                          float weight_decay, float trust_coef, void* workspace,
                                          size_t workspace_bytes, float* trust_out,
                                          const float* lr_device, void* stream) {
-    if (!plan) return fail(LSGD_ERR_NULL, "plan is NULL");
-    if (!workspace) return fail(LSGD_ERR_NULL, "workspace is NULL");
-    const LarsLayout l = lars_layout(plan);
-    if (workspace_bytes < l.total)
-        return fail(LSGD_ERR_SIZE, "workspace_bytes=%zu < %zu (lsgd_lars_workspace_size)", workspace_bytes, l.total);
-    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-        return fail(LSGD_ERR_ALIGN, "workspace is not 256-byte aligned");
-    if (trust_out && (reinterpret_cast<uintptr_t>(trust_out) & 3u) != 0)
-        return fail(LSGD_ERR_ALIGN, "trust_out is not 4-byte aligned");
-    if (lr_device && (reinterpret_cast<uintptr_t>(lr_device) & 3u) != 0)
-        return fail(LSGD_ERR_ALIGN, "lr_device is not 4-byte aligned");
-    std::vector<Range> ranges(*plan->ranges);
-    const uintptr_t wb = reinterpret_cast<uintptr_t>(workspace);
-    ranges.push_back(Range{wb, wb + l.total, true, "workspace"});
-    if (trust_out) {
-        const uintptr_t tb = reinterpret_cast<uintptr_t>(trust_out);
-        ranges.push_back(Range{tb, tb + static_cast<uintptr_t>(plan->n_tensors) * sizeof(float), true, "trust_out"});
-    }
-    if (lr_device) {
-        const uintptr_t lb = reinterpret_cast<uintptr_t>(lr_device);
-        ranges.push_back(Range{lb, lb + sizeof(float), false, "lr_device"});
-    }
-    lsgd_status st = check_overlap(ranges);
-    if (st != LSGD_OK) return st;
-    if (plan->W == 0) return fail(LSGD_ERR_GROUPS, "the LARS step needs equal group sizes; this plan's differ");
-    if ((st = check_device(plan)) != LSGD_OK) return st;
-
-    LarsArgs la;
-    memset(&la, 0, sizeof la);
-    LaunchShape ls;
-    la.pa = plan_args(plan, Hyper{lr, momentum_coef, weight_decay}, lr_device, ls);
-    la.gbar_off = plan->d_gbar_off;
-    la.tensor_chunks = plan->d_tensor_chunks;
-    char* ws = static_cast<char*>(workspace);
-    la.gbar = reinterpret_cast<float*>(ws + l.gbar);
-    la.partials = reinterpret_cast<double*>(ws + l.partials);
-    la.trust = reinterpret_cast<float*>(ws + l.trust);
-    la.trust_out = trust_out;
-    la.exclude = plan->d_lars_exclude;
-    la.n_tensors = plan->n_tensors;
-    la.trust_coef = trust_coef;
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    if (plan->n_buckets > 0) {
-        const LarsKernel k1 = plan->gdt == LSGD_BF16 ? pick_lars<uint16_t>(plan->W, plan->n_groups)
-                                                     : pick_lars<float>(plan->W, plan->n_groups);
-        hipLaunchKernelGGL(k1, dim3(ls.blocks), dim3(kBlock), 0, s, la);
-        if ((st = check_launch("lsgd_lars_step_plan (norms)")) != LSGD_OK) return st;
-    }
-    hipLaunchKernelGGL(lars_trust_kernel, dim3(plan->n_tensors), dim3(kBlock), 0, s, la);
-    if ((st = check_launch("lsgd_lars_step_plan (trust)")) != LSGD_OK) return st;
-    if (plan->n_buckets == 0) return LSGD_OK;
-    // the update reads and writes as lsgd_sgd_step does: the same copy-out rule
-    const bool split = separate_copy_out_update(plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,
-                                                use_cached_state(plan->n_workers, plan->total_elems));
-    if (split) la.pa.n_replicas = 0;
-    hipLaunchKernelGGL(lars_update_kernel<2>, dim3(ls.blocks), dim3(kBlock), 0, s, la);
-    if ((st = check_launch("lsgd_lars_step_plan (update)")) != LSGD_OK || !split) return st;
-    la.pa.n_replicas = plan->n_replicas;
-    return plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, la.pa, s)
-                                  : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, la.pa, s);
+    return lsgd::lars_step(plan, lr, momentum_coef, weight_decay, trust_coef, workspace, workspace_bytes, false,
+                           trust_out, lr_device, stream);
 }
 
 LSGD_API lsgd_status lsgd_plan_set_lars_exclude(lsgd_plan* plan, const uint8_t* exclude) {

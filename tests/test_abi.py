@@ -47,7 +47,7 @@ def test_header_declares_the_boundary():
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
             "lsgd_lr_schedule_step", "lsgd_step_plan_ex", "lsgd_lars_workspace_size",
             "lsgd_lars_step_plan", "lsgd_set_copy_out_mode", "lsgd_get_copy_out_mode",
-            "lsgd_plan_set_lars_exclude"} == names
+            "lsgd_plan_set_lars_exclude", "lsgd_lars_step_plan_noalloc"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -61,6 +61,8 @@ def test_header_constants_match_binding():
     text = open(HEADER).read()
     assert int(re.search(r"#define LSGD_MAX_WORKERS (\d+)", text).group(1)) == L.MAX_WORKERS
     assert int(re.search(r"#define LSGD_MAX_REPLICAS (\d+)", text).group(1)) == L.MAX_REPLICAS
+    shift = int(re.search(r"#define LSGD_NOALLOC_SCRATCH_BYTES \(\(size_t\)128 << (\d+)\)", text).group(1))
+    assert (128 << shift) == L.NOALLOC_SCRATCH_BYTES
     for code, name in L.STATUS_NAMES.items():
         assert re.search(r"%s = %d" % (name, code), text), name
 
@@ -309,6 +311,8 @@ def test_lars_validation():
     assert lib.lsgd_lars_step_plan(None, 0.1, 0.9, 1e-4, 1e-3, A, 1 << 30, None, None, None) == NULL
     assert "plan is NULL" in lib.lsgd_last_error().decode()
     assert lib.lsgd_plan_set_lars_exclude(None, None) == NULL
+    assert lib.lsgd_lars_step_plan_noalloc(None, 0.1, 0.9, 1e-4, 1e-3, None, None, None) == NULL
+    assert "plan is NULL" in lib.lsgd_last_error().decode()
 
 
 def test_last_error_is_per_thread():
