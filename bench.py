@@ -212,19 +212,24 @@ class Setup:
             def step():
                 check(fn(*args))
             if R and separate_copy_out(wl, R, copy_out) and not lr_schedule and not broadcast_grad:
-                # the same two kernels launched one at a time: the step without
-                # replicas on the same buffers, then the copy-out pass
-                args0 = args[:11] + (None, 0) + args[13:]
-                copy_args = (self.params[0].data_ptr(), wl.n, common[11], R, common[13],
+                # the same two kernels launched one at a time, on the element
+                # ranges the library uses (library_ranges): the step without
+                # replicas on the same buffers, then the copy-out pass, range
+                # by range
+                gsz, rsz = wl.grad_bytes, (2 if rtd == torch.bfloat16 else 4)
+                self.parts = []
+                for lo, hi in library_ranges(wl.n):
+                    sargs = ((self.params[0].data_ptr() + 4 * lo, self.mom[0].data_ptr() + 4 * lo,
+                              ptr_array([g[0].data_ptr() + gsz * lo for g in self.grads])) + args[3:7]
+                             + (hi - lo,) + args[8:11] + (None, 0) + args[13:])
+                    cargs = (self.params[0].data_ptr() + 4 * lo, hi - lo,
+                             ptr_array([r[0].data_ptr() + rsz * lo for r in self.reps]), R, common[13],
                              ctypes.c_void_p(stream.cuda_stream))
-
-                def step_part():
-                    check(fn(*args0))
-
-                def copy_part():
-                    check(lib.lsgd_copy_out(*copy_args))
-                self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes()),
-                              ("copy_out_rmajor_kernel", copy_part, self._copy_bytes())]
+                    frac = (hi - lo) / wl.n
+                    self.parts.append((kernel_match(wl, reduction), lambda a=sargs: check(fn(*a)),
+                                       round(self._step_bytes() * frac)))
+                    self.parts.append(("copy_out_rmajor_kernel", lambda a=cargs: check(lib.lsgd_copy_out(*a)),
+                                       round(self._copy_bytes() * frac)))
         del scratch
         if lr_schedule:
             inner = step
@@ -735,6 +740,18 @@ def separate_copy_out(wl, R, mode="auto", bcast=False):
     return copy_bytes >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
 
 
+def library_ranges(n):
+    """The element ranges in which the library runs a flat step whose copy-out
+    is a pass of its own (the step kernel, then the copy-out, range by range):
+    one range up to 2^26 elements, else ceil(n / 2^25) ranges starting on
+    multiples of 2048 elements."""
+    if n <= 1 << 26:
+        return [(0, n)]
+    K = (n + (1 << 25) - 1) >> 25
+    edges = [(n // K * i) // 2048 * 2048 for i in range(K)] + [n]
+    return list(zip(edges[:-1], edges[1:]))
+
+
 def kernel_match(wl, reduction=None, lars=False):
     ct = (not wl.group_sizes and wl.groups in (1, 2, 4, 8, 16)
           and wl.workers_per_group in (1, 2, 4, 8, 16) and wl.n_workers <= 128)
@@ -767,12 +784,16 @@ def derive_traffic(args):
     per_alg = {kname: wl.algorithmic_bytes(0 if split else R)}
     if split:
         per_alg["copy_out"] = wl.n * (4 + R * rb)
+    # a flat step with a copy-out pass runs each kernel once per element range
+    launches = len(library_ranges(wl.n)) if split and not wl.tensor_sizes else 1
     per = {}
     for k, a in per_alg.items():
         f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", k)
         w_k, nw = _per_dispatch_kib(write_rows, "WRITE_SIZE", k)
+        f_k, w_k = f_k * launches, w_k * launches        # per step
         rbytes, wbytes = f_k * f_scale * 1024, w_k * w_scale * 1024
-        per[k] = {"fetch_kib_per_dispatch": f_k, "write_kib_per_dispatch": w_k, "dispatches": [nf, nw],
+        per[k] = {"fetch_kib_per_step": f_k, "write_kib_per_step": w_k, "dispatches": [nf, nw],
+                  "launches_per_step": launches,
                   "read_bytes": rbytes, "write_bytes": wbytes, "traffic_bytes": rbytes + wbytes,
                   "algorithmic_bytes": a, "traffic_over_algorithmic": (rbytes + wbytes) / a}
     fetch_b = sum(v["read_bytes"] for v in per.values())
@@ -947,14 +968,22 @@ def main(argv=None):
     setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
                   args.tensor_layout, args.copy_out, args.lr_schedule)
     replay = captured(setup) if args.graph else None
-    reps_ms = time_steps(setup, args.steps, args.warmup, replay)
-    ms = median(reps_ms)
     kernels = []
     if setup.parts and not args.graph:   # two kernels per step: the step again, an event between its kernels
+        # measured first: the GPU runs the first tens of steps of a process
+        # slower (the copy-out pass up to a quarter slower for about 25 steps),
+        # which the five timed loops of each kernel absorb before the headline
+        per = {}    # per kernel: summed over the ranges of a step
         for (name, _, nbytes), kms in zip(setup.parts, time_parts(setup, args.steps, args.warmup)):
+            t, b, c = per.get(name, (0.0, 0, 0))
+            per[name] = (t + kms, b + nbytes, c + 1)
+        for name, (kms, nbytes, launches) in per.items():
             kg = nbytes / (kms * 1e-3) / 1e9
             kernels.append({"kernel": name, "ms": round(kms, 6), "algorithmic_bytes": nbytes,
-                            "GBps": round(kg, 2), "frac": round(kg / PEAK_HBM_GBPS, 4)})
+                            "GBps": round(kg, 2), "frac": round(kg / PEAK_HBM_GBPS, 4),
+                            **({"launches": launches} if launches > 1 else {})})
+    reps_ms = time_steps(setup, args.steps, args.warmup, replay)
+    ms = median(reps_ms)
     alg = wl.algorithmic_bytes(R) + extra_bytes()
     gbps = alg / (ms * 1e-3) / 1e9
     traffic = stored_traffic(wl, R, args.lars)

@@ -130,3 +130,44 @@ def test_all_cores_cpu_baseline_runs_the_oracle_on_blocks(monkeypatch):
         sl = slice(k * B, min(n, (k + 1) * B))
         oracle.lsgd_step(pb[sl], mb[sl], [g[sl] for g in gs], [0, 0, 1, 1], 2, 0.1, 0.9, 1e-4, [rb[0][sl]])
     assert pa.tobytes() == pb.tobytes() and ma.tobytes() == mb.tobytes() and ra[0].tobytes() == rb[0].tobytes()
+
+
+def test_library_ranges_cover_the_vector():
+    """The element ranges of a long flat step with a copy-out pass: one range up
+    to 2^26 elements; beyond, ceil(n / 2^25) contiguous ranges that start on
+    multiples of 2048 elements and cover [0, n)."""
+    assert bench.library_ranges(1 << 26) == [(0, 1 << 26)]
+    for n in ((1 << 26) + 1, 350_000_000, (1 << 26) + (1 << 25) + 12_345):
+        r = bench.library_ranges(n)
+        assert len(r) == -(-n // (1 << 25))
+        assert r[0][0] == 0 and r[-1][1] == n
+        assert all(a % 2048 == 0 and a < b for a, b in r)
+        assert all(r[i][1] == r[i + 1][0] for i in range(len(r) - 1))
+
+
+def test_derive_traffic_counts_every_range_launch(tmp_path, monkeypatch):
+    """A step run in element ranges (the 3.5e8-element workload: 11 launches of
+    each kernel per step): the per-dispatch counters are scaled to the step."""
+    wl = workloads.WORKLOADS["large"]
+    R = wl.n_workers
+    K = len(bench.library_ranges(wl.n))
+    gib_kib = (1 << 30) / 1024
+    step = "void lsgd::step_flat_ct<unsigned short, 8, 8, 1, 0>(lsgd::StepArgs)"
+    cpy = "void lsgd::copy_out_rmajor_kernel<8, 1, 2>(lsgd::StepArgs)"
+    copy = "lsgd::stream_copy_kernel(unsigned int __vector(4)*)"
+    calib_grid = (1 << 28) // 4
+    s_read, s_write = wl.n * (64 * 2 + 8) / K, wl.n * 8 / K
+    c_read, c_write = wl.n * 4 / K, wl.n * 2 * R / K
+    fetch = [(copy, calib_grid, gib_kib / 2)] + [(step, 1, s_read / 2048), (cpy, 1, c_read / 2048)] * K
+    write = [(copy, calib_grid, gib_kib)] + [(step, 1, s_write / 1024), (cpy, 1, c_write / 1024)] * K
+    fcsv, wcsv = tmp_path / "f.csv", tmp_path / "w.csv"
+    _write_rows(fcsv, "FETCH_SIZE", fetch)
+    _write_rows(wcsv, "WRITE_SIZE", write)
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    args = bench.parse_args(["--derive-traffic", "--workload", "large", "--fetch-csv", str(fcsv),
+                             "--write-csv", str(wcsv)])
+    bench.derive_traffic(args)
+    out = json.load(open(tmp_path / ("traffic_large_R%d.json" % R)))
+    for k in ("step_flat_ct", "copy_out"):
+        assert out["kernels"][k]["launches_per_step"] == K
+        assert abs(out["kernels"][k]["traffic_over_algorithmic"] - 1.0) < 1e-9, k

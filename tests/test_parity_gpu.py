@@ -501,6 +501,56 @@ def test_workload_full_size_every_element(name):
     torch.cuda.empty_cache()
 
 
+def test_long_vectors_in_ranges_match_oracle():
+    """Vectors above 2^26 elements whose copy-out runs as a pass of its own are
+    processed range by range (the step kernel, then its copy passes, over
+    ranges of about 2^25 elements): lsgd_step with the literal reduction and
+    the gradient broadcast, and lsgd_sgd_step, against the oracle on every
+    element, on a length that leaves four ranges and a ragged end."""
+    n = (1 << 26) + (1 << 25) + 12_345
+    G, W, R = 2, 2, 2
+    T = fullsize.host_threads()
+    log("ranges: n=%d G=%d W=%d R=%d" % (n, G, W, R))
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(77)
+    grads = [torch.randn(n, device=DEV, generator=gen) * 1e-2 for _ in range(G * W)]
+    p = torch.randn(n, device=DEV, generator=gen) * 0.05
+    m = torch.randn(n, device=DEV, generator=gen) * 0.01
+    gh = [to_host(g).copy() for g in grads]
+    p0, m0 = to_host(p).copy(), to_host(m).copy()
+    gow = workloads.contiguous_groups(G, W)
+    reps = [torch.empty(n, device=DEV) for _ in range(R)]
+    lsgd.set_copy_out_mode(lsgd.COPY_OUT_SEPARATE)
+    try:
+        lsgd.step(p, m, grads, gow, G, 0.1, 0.9, 1e-4, reps, reduction="literal", broadcast_grad=True)
+        torch.cuda.synchronize()
+        p_ref, m_ref, rr = p0.copy(), m0.copy(), np.zeros(n, np.float32)
+        fullsize.run_blocks(lambda a, b: oracle.lsgd_step_literal(
+            p_ref[a:b], m_ref[a:b], [x[a:b] for x in gh], gow, G, 0.1, 0.9, 1e-4, [rr[a:b]],
+            broadcast_grad=True), n, T)
+        assert_close(to_host(p), p_ref, "params")
+        assert_close(to_host(m), m_ref, "momentum")
+        for r in range(R):
+            assert np.array_equal(to_host(reps[r]), rr), "replica %d" % r
+        for w in range(G * W):
+            assert np.array_equal(to_host(grads[w]), gh[w]), "broadcast to worker %d" % w
+        gbar = grads[0]                       # now holds the mean gradient
+        p2, m2 = torch.from_numpy(p0).to(DEV), torch.from_numpy(m0).to(DEV)
+        lsgd.sgd_step(p2, m2, gbar, 0.1, 0.9, 1e-4, reps)
+        torch.cuda.synchronize()
+        p_ref2, m_ref2, rr2 = p0.copy(), m0.copy(), np.zeros(n, np.float32)
+        fullsize.run_blocks(lambda a, b: oracle.sgd_step(p_ref2[a:b], m_ref2[a:b], gh[0][a:b], 0.1, 0.9, 1e-4,
+                                                         [rr2[a:b]]), n, T)
+        assert_close(to_host(p2), p_ref2, "sgd params")
+        assert_close(to_host(m2), m_ref2, "sgd momentum")
+        for r in range(R):
+            assert np.array_equal(to_host(reps[r]), rr2), "sgd replica %d" % r
+    finally:
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+    del grads, reps, p, m, p2, m2
+    torch.cuda.empty_cache()
+
+
 def test_results_independent_of_launch_shape():
     """Every launch shape (XCD chunking, grid-stride caps, units per lane) gives
     the same bits: each element is computed by one lane from its own inputs."""
