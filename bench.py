@@ -172,18 +172,26 @@ class Setup:
                     check(fn(h, *hyper, s))
                 if R and separate_copy_out(wl, R, copy_out):
                     # the same two kernels launched one at a time: the step over
-                    # a plan of the same tensors without replicas, then the
-                    # plan's copy-out pass
-                    self.plan0 = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, [])
-                    h0 = self.plan0._handle
+                    # a plan of the same tensors with the replicas the step
+                    # kernel writes itself (step_replicas), then the copy-out
+                    # pass of a plan holding the others
+                    k = step_replicas(wl, R)
+                    rsz = 2 if rtd == torch.bfloat16 else 4
+                    self.plan0 = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps[:k])
+                    self.plan1 = lsgd.Plan(self.params, self.mom, self.grads, self.gow, G, self.reps[k:])
+                    h0, h1 = self.plan0._handle, self.plan1._handle
+                    mode = {"auto": -1, "fused": 0, "separate": 1}[copy_out]
 
                     def step_part():
-                        check(fn(h0, *hyper, s))
+                        lib.lsgd_set_copy_out_mode(0)
+                        st = fn(h0, *hyper, s)
+                        lib.lsgd_set_copy_out_mode(mode)
+                        check(st)
 
                     def copy_part():
-                        check(lib.lsgd_plan_copy_out(h, s))
-                    self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes()),
-                                  ("copy_out_plan_rmajor", copy_part, self._copy_bytes())]
+                        check(lib.lsgd_plan_copy_out(h1, s))
+                    self.parts = [(kernel_match(wl, reduction), step_part, self._step_bytes() + wl.n * k * rsz),
+                                  ("copy_out_plan_rmajor", copy_part, self._copy_bytes() - wl.n * k * rsz)]
         else:
             self.plan = None
             self.params = [flat_p]
@@ -216,20 +224,29 @@ class Setup:
                 # ranges the library uses (library_ranges): the step without
                 # replicas on the same buffers, then the copy-out pass, range
                 # by range
+                # (the step kernel writing its share of the replicas, step_replicas)
                 gsz, rsz = wl.grad_bytes, (2 if rtd == torch.bfloat16 else 4)
+                k = step_replicas(wl, R)
                 self.parts = []
+
+                def fused(a):
+                    lib.lsgd_set_copy_out_mode(0)     # the step kernel writes its k replicas
+                    st = fn(*a)
+                    lib.lsgd_set_copy_out_mode({"auto": -1, "fused": 0, "separate": 1}[copy_out])
+                    check(st)
                 for lo, hi in library_ranges(wl.n):
                     sargs = ((self.params[0].data_ptr() + 4 * lo, self.mom[0].data_ptr() + 4 * lo,
                               ptr_array([g[0].data_ptr() + gsz * lo for g in self.grads])) + args[3:7]
-                             + (hi - lo,) + args[8:11] + (None, 0) + args[13:])
+                             + (hi - lo,) + args[8:11]
+                             + (ptr_array([r[0].data_ptr() + rsz * lo for r in self.reps[:k]]), k) + args[13:])
                     cargs = (self.params[0].data_ptr() + 4 * lo, hi - lo,
-                             ptr_array([r[0].data_ptr() + rsz * lo for r in self.reps]), R, common[13],
+                             ptr_array([r[0].data_ptr() + rsz * lo for r in self.reps[k:]]), R - k, common[13],
                              ctypes.c_void_p(stream.cuda_stream))
                     frac = (hi - lo) / wl.n
-                    self.parts.append((kernel_match(wl, reduction), lambda a=sargs: check(fn(*a)),
-                                       round(self._step_bytes() * frac)))
+                    self.parts.append((kernel_match(wl, reduction), lambda a=sargs: fused(a),
+                                       round((self._step_bytes() + wl.n * k * rsz) * frac)))
                     self.parts.append(("copy_out_rmajor_kernel", lambda a=cargs: check(lib.lsgd_copy_out(*a)),
-                                       round(self._copy_bytes() * frac)))
+                                       round((self._copy_bytes() - wl.n * k * rsz) * frac)))
         del scratch
         if lr_schedule:
             inner = step
@@ -252,12 +269,12 @@ class Setup:
 
     parts = None     # [(kernel, callable, algorithmic bytes)] when the step is two kernels
     plan0 = None
+    plan1 = None
 
     def close(self):
-        if self.plan is not None:
-            self.plan.close()
-        if self.plan0 is not None:
-            self.plan0.close()
+        for pl in (self.plan, self.plan0, self.plan1):
+            if pl is not None:
+                pl.close()
 
 
 REPEATS = 5        # timed repeats of the K-step loop; the line reports their median
@@ -740,6 +757,15 @@ def separate_copy_out(wl, R, mode="auto", bcast=False):
     return copy_bytes >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
 
 
+def step_replicas(wl, R):
+    """The library's automatic share of the replicas that the step kernel still
+    writes when the copy-out is a pass of its own (lsgd_set_step_replicas):
+    16 bytes per element where parameters and momentum go through the caches."""
+    rb = 2 if wl.replica_dtype == "bf16" else 4
+    cached = wl.n_workers <= 16 and 8 * wl.n <= (288 << 20)
+    return min(R, 16 // rb) if cached else 0
+
+
 def library_ranges(n):
     """The element ranges in which the library runs a flat step whose copy-out
     is a pass of its own (the step kernel, then the copy-out, range by range):
@@ -781,9 +807,10 @@ def derive_traffic(args):
     kname = kernel_match(wl)
     rb = 2 if wl.replica_dtype == "bf16" else 4
     split = any("copy_out" in r.get("Kernel_Name", "") for r in fetch_rows)   # the step's copy-out pass
-    per_alg = {kname: wl.algorithmic_bytes(0 if split else R)}
+    k = step_replicas(wl, R) if split else R       # replicas the step kernel writes itself
+    per_alg = {kname: wl.algorithmic_bytes(k)}
     if split:
-        per_alg["copy_out"] = wl.n * (4 + R * rb)
+        per_alg["copy_out"] = wl.n * (4 + (R - k) * rb)
     # a flat step with a copy-out pass runs each kernel once per element range
     launches = len(library_ranges(wl.n)) if split and not wl.tensor_sizes else 1
     per = {}

@@ -152,6 +152,19 @@ LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_p
 LSGD_API lsgd_status lsgd_set_copy_out_mode(int32_t mode);
 LSGD_API int32_t lsgd_get_copy_out_mode(void);
 
+/* Where the fused steps (lsgd_step, lsgd_step_ex, lsgd_step_plan*) take the
+ * separate copy-out form: the step kernel still writes the first `replicas`
+ * replicas itself (fewer if the step has fewer) and the copy-out pass writes
+ * the rest. -1 (the default) is the automatic choice: 16 bytes of replicas per
+ * element (4 binary32 or 8 bfloat16 replicas) for steps with at most 16
+ * workers whose parameters and momentum fit in 288 MB, none otherwise (the
+ * step kernel's mostly-read stream mix takes a few write streams at little
+ * cost; measured fastest). Results are identical for every value.
+ * Process-wide, for launches after the call returns. Errors: LSGD_ERR_SIZE
+ * (outside [-1, LSGD_MAX_REPLICAS]). A tuning and measurement knob. */
+LSGD_API lsgd_status lsgd_set_step_replicas(int32_t replicas);
+LSGD_API int32_t lsgd_get_step_replicas(void);
+
 /*
  * The local layer alone (Alg. 3, Reduce to the communicator and divide):
  *   group_means[j][i] = PW over the W members of group j of grads[w][i], / W.

@@ -33,7 +33,8 @@ EXPORTS = ("lsgd_status_string", "lsgd_last_error", "lsgd_set_launch_shape",
            "lsgd_step_plan", "lsgd_step_plan_ex", "lsgd_plan_destroy", "lsgd_stream_copy",
            "lsgd_lars_workspace_size", "lsgd_lars_step_plan", "lsgd_set_copy_out_mode",
            "lsgd_get_copy_out_mode", "lsgd_plan_set_lars_exclude", "lsgd_copy_out",
-           "lsgd_plan_copy_out", "lsgd_lars_step_plan_noalloc")
+           "lsgd_plan_copy_out", "lsgd_lars_step_plan_noalloc", "lsgd_set_step_replicas",
+           "lsgd_get_step_replicas")
 NOALLOC_SCRATCH_BYTES = 128 << 20      # LSGD_NOALLOC_SCRATCH_BYTES
 
 
@@ -92,6 +93,8 @@ def _load():
     lib.lsgd_get_copy_out_mode.argtypes, lib.lsgd_get_copy_out_mode.restype = [], i32
     lib.lsgd_lars_step_plan.argtypes = [P, f32, f32, f32, f32, P, ctypes.c_size_t, P, P, P]
     lib.lsgd_lars_step_plan_noalloc.argtypes = [P, f32, f32, f32, f32, P, P, P]
+    lib.lsgd_set_step_replicas.argtypes = [i32]
+    lib.lsgd_get_step_replicas.argtypes, lib.lsgd_get_step_replicas.restype = [], i32
     for name in ("lsgd_group_mean", "lsgd_global_mean", "lsgd_sgd_step", "lsgd_copy_out", "lsgd_plan_copy_out",
                  "lsgd_step",
                  "lsgd_plan_create", "lsgd_step_plan", "lsgd_set_launch_shape",
@@ -487,3 +490,13 @@ def set_copy_out_mode(mode):
 
 def get_copy_out_mode():
     return lib.lsgd_get_copy_out_mode()
+
+
+def set_step_replicas(replicas):
+    """lsgd_set_step_replicas: with the separate copy-out, the step kernel
+    still writes the first `replicas` replicas (-1: the automatic choice)."""
+    check(lib.lsgd_set_step_replicas(int(replicas)))
+
+
+def get_step_replicas():
+    return lib.lsgd_get_step_replicas()

@@ -24,6 +24,7 @@ std::atomic<int32_t> g_xcd_chunk{kDefaultXcdChunk};
 std::atomic<int32_t> g_blocks_per_cu{kDefaultBlocksPerCu};
 std::atomic<int32_t> g_units_per_lane{kDefaultUnitsPerLane};
 std::atomic<int32_t> g_copy_out_mode{LSGD_COPY_OUT_AUTO};
+std::atomic<int32_t> g_step_replicas{-1};   // lsgd_set_step_replicas (-1: automatic)
 }  // namespace
 
 lsgd_status fail(lsgd_status st, const char* fmt, ...) {
@@ -176,6 +177,26 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
     return separate_copy_out_bytes(n_workers, gsz, static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz), n);
 }
 
+// With the separate copy-out the step kernel still writes the first k replicas
+// itself: its stream mix is mostly reads, and a few write streams added to it
+// cost less time than the copy-out pass saves by writing them. Measured on the
+// ResNet-50-sized 4x4 binary32 step with 16 replicas, same process (k
+// replicas in the step kernel, 16 - k in the pass): k = 0 6479 GB/s, 1 6508,
+// 2 6489, 3 6641, 4 6690, 5 6706, 6 6647, 8 6553, 10 6476, 12 6381, 16 (the
+// fused step) 6337; the 161-tensor plan k = 0 6285, 4 6402; 32 replicas k = 0
+// 6621, 4 6775; 64 replicas k = 0 6746, 4 6840; 2x2 with 16 replicas even;
+// with 128 binary32 gradients or 64 bfloat16 ones (nontemporal parameter and
+// momentum accesses) every k > 0 lost (128: k = 2 -1.4%, 4 -2.2%; 64 bfloat16:
+// k = 4 -2%, 16 -3.8%). The rule: 16 bytes of replicas per element in the
+// step kernel where parameters and momentum go through the caches, none
+// otherwise.
+int32_t replicas_in_step(int32_t n_workers, int32_t n_replicas, size_t rsz, int64_t n) {
+    const int32_t forced = g_step_replicas.load(std::memory_order_relaxed);
+    if (forced >= 0) return std::min(forced, n_replicas);
+    if (!use_cached_state(n_workers, n)) return 0;
+    return std::min<int32_t>(n_replicas, static_cast<int32_t>(16 / rsz));
+}
+
 // 8 MB of p per window: 1 MB in each of the eight XCD L2 caches (4 MB each),
 // re-read there for every replica. Windows of 4-20 MB measured alike; from
 // 24 MB the window no longer stays in L2 and the pass slows by a third.
@@ -268,6 +289,15 @@ LSGD_API lsgd_status lsgd_set_copy_out_mode(int32_t mode) {
 }
 
 LSGD_API int32_t lsgd_get_copy_out_mode(void) { return lsgd::g_copy_out_mode.load(std::memory_order_relaxed); }
+
+LSGD_API lsgd_status lsgd_set_step_replicas(int32_t replicas) {
+    if (replicas < -1 || replicas > LSGD_MAX_REPLICAS)
+        return lsgd::fail(LSGD_ERR_SIZE, "step replicas %d outside [-1, %d]", replicas, LSGD_MAX_REPLICAS);
+    lsgd::g_step_replicas.store(replicas, std::memory_order_relaxed);
+    return LSGD_OK;
+}
+
+LSGD_API int32_t lsgd_get_step_replicas(void) { return lsgd::g_step_replicas.load(std::memory_order_relaxed); }
 
 LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_per_cu,
                                            int32_t* units_per_lane) {

@@ -308,7 +308,9 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const bool split = separate_copy_out_bytes(
         n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n);
     a.bcast_grad = bcast ? (split ? 1 : n_workers) : 0;
-    if (split) a.n_replicas = 0;
+    // split: the step kernel writes the first k replicas, the copy-out pass the rest
+    const int32_t k_step = split ? replicas_in_step(n_workers, n_replicas, dtype_size(rdt), n) : n_replicas;
+    a.n_replicas = k_step;
     const char* what = literal ? "lsgd_step_ex" : "lsgd_step";
     const int64_t K = split ? split_ranges(n) : 1;
     for (int64_t i = 0; i < K; ++i) {
@@ -319,8 +321,9 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
         ra.upl = ls.upl;
         hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), ra);
         if ((st = check_launch(what)) != LSGD_OK || !split) return st;
-        if (n_replicas > 0) {
-            ra.n_replicas = n_replicas;
+        if (n_replicas > k_step) {
+            for (int32_t r = k_step; r < n_replicas; ++r) ra.replicas[r - k_step] = ra.replicas[r];
+            ra.n_replicas = n_replicas - k_step;
             if ((st = launch_copy_out(ra, stream)) != LSGD_OK) return st;
         }
         if (bcast_copies > 0) {

@@ -75,6 +75,10 @@ bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t
 // The same rule for `copy_bytes` bytes per element of copies (replicas, and
 // the gradient broadcast's copies of the mean gradient to the other members).
 bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n);
+// With the separate copy-out: how many of the n_replicas replicas (rsz bytes
+// each) the step kernel still writes itself; the copy-out pass writes the
+// rest (lsgd_set_step_replicas).
+int32_t replicas_in_step(int32_t n_workers, int32_t n_replicas, size_t rsz, int64_t n);
 // The same for lsgd_sgd_step and the LARS update; `cached`: their parameter
 // and momentum accesses go through the caches.
 bool separate_copy_out_update(int32_t n_replicas, size_t rsz, bool cached);

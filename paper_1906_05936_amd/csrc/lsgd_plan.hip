@@ -520,12 +520,17 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
         static_cast<int64_t>(plan->n_replicas) * (plan->rdt == LSGD_BF16 ? 2 : 4) + 4 * bcast_copies,
         plan->total_elems);
     a.bcast_grad = bcast ? (split ? 1 : plan->n_workers) : 0;
-    if (split) a.n_replicas = 0;
+    // split: the step kernel writes the first k replicas, the copy-out pass the rest
+    const int32_t k_step = split ? replicas_in_step(plan->n_workers, plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,
+                                                    plan->total_elems)
+                                 : plan->n_replicas;
+    a.n_replicas = k_step;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(k, dim3(ls.blocks), dim3(kBlock), 0, s, a);
     if ((st = check_launch("lsgd_step_plan")) != LSGD_OK || !split) return st;
-    if (plan->n_replicas > 0) {
-        a.n_replicas = plan->n_replicas;
+    if (plan->n_replicas > k_step) {
+        a.copy_dst = 2 + plan->n_workers + k_step;
+        a.n_replicas = plan->n_replicas - k_step;
         st = plan->rdt == LSGD_BF16 ? launch_plan_copy_out<8, kPlanCopyRKBF16>(plan, a, s)
                                     : launch_plan_copy_out<4, kPlanCopyRKF32>(plan, a, s);
         if (st != LSGD_OK) return st;

@@ -47,7 +47,8 @@ def test_header_declares_the_boundary():
             "lsgd_get_launch_shape", "lsgd_stream_copy", "lsgd_step_ex", "lsgd_lr_at",
             "lsgd_lr_schedule_step", "lsgd_step_plan_ex", "lsgd_lars_workspace_size",
             "lsgd_lars_step_plan", "lsgd_set_copy_out_mode", "lsgd_get_copy_out_mode",
-            "lsgd_plan_set_lars_exclude", "lsgd_lars_step_plan_noalloc"} == names
+            "lsgd_plan_set_lars_exclude", "lsgd_lars_step_plan_noalloc", "lsgd_set_step_replicas",
+            "lsgd_get_step_replicas"} == names
     assert set(L.EXPORTS) == names
 
 
@@ -303,6 +304,16 @@ def test_copy_out_mode_setter():
     assert lib.lsgd_set_copy_out_mode(2) == SIZE
     assert lib.lsgd_set_copy_out_mode(-2) == SIZE
     assert lib.lsgd_get_copy_out_mode() == -1
+
+
+def test_step_replicas_setter():
+    assert lib.lsgd_get_step_replicas() == -1
+    for k in (0, 4, 128, -1):
+        assert lib.lsgd_set_step_replicas(k) == OK
+        assert lib.lsgd_get_step_replicas() == k
+    assert lib.lsgd_set_step_replicas(129) == SIZE
+    assert lib.lsgd_set_step_replicas(-2) == SIZE
+    assert lib.lsgd_get_step_replicas() == -1
 
 
 def test_lars_validation():

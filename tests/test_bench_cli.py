@@ -65,18 +65,21 @@ def test_derive_traffic_scales_by_the_calibration_copy(tmp_path, monkeypatch):
 
 
 def test_derive_traffic_per_kernel_with_a_copy_out_pass(tmp_path, monkeypatch):
-    """A step split into the step kernel (no replicas) and the copy-out pass:
-    each kernel's traffic against its own algorithmic bytes, the step's total,
-    and the per-kernel lookup the benchmark's roofline uses."""
+    """A step split into the step kernel (writing its share of the replicas,
+    4 of 16 binary32 ones here) and the copy-out pass (the other 12): each
+    kernel's traffic against its own algorithmic bytes, the step's total, and
+    the per-kernel lookup the benchmark's roofline uses."""
     wl = workloads.WORKLOADS["resnet50_flat"]
     R = 16
+    k_step = bench.step_replicas(wl, R)
+    assert k_step == 4
     gib_kib = (1 << 30) / 1024
     step = "void lsgd::step_flat_ct<float, 4, 4, 2>(lsgd::StepArgs)"
     cpy = "void lsgd::copy_out_rmajor_kernel<4, 2, 1>(lsgd::StepArgs)"
     copy = "lsgd::stream_copy_kernel(unsigned int __vector(4)*)"
     calib_grid = (1 << 28) // 4
-    s_read, s_write = wl.n * (16 * 4 + 8), wl.n * 8
-    c_read, c_write = wl.n * 4 * 1.5, wl.n * 4 * R      # the pass reads p 1.5 times here
+    s_read, s_write = wl.n * (16 * 4 + 8), wl.n * (8 + 4 * k_step)
+    c_read, c_write = wl.n * 4 * 1.5, wl.n * 4 * (R - k_step)      # the pass reads p 1.5 times here
     fetch = [(copy, calib_grid, gib_kib / 2), (step, 1, s_read / 2048), (cpy, 1, c_read / 2048),
              (step, 1, s_read / 2048), (cpy, 1, c_read / 2048)]
     write = [(copy, calib_grid, gib_kib), (step, 1, s_write / 1024), (cpy, 1, c_write / 1024)]
@@ -90,9 +93,9 @@ def test_derive_traffic_per_kernel_with_a_copy_out_pass(tmp_path, monkeypatch):
     out = json.load(open(tmp_path / "traffic_resnet50_flat_R16.json"))
     k = out["kernels"]
     assert set(k) == {"step_flat_ct", "copy_out"}
-    assert k["step_flat_ct"]["algorithmic_bytes"] == wl.algorithmic_bytes(0)
+    assert k["step_flat_ct"]["algorithmic_bytes"] == wl.algorithmic_bytes(k_step)
     assert abs(k["step_flat_ct"]["traffic_over_algorithmic"] - 1.0) < 1e-9
-    assert k["copy_out"]["algorithmic_bytes"] == wl.n * (4 + 4 * R)
+    assert k["copy_out"]["algorithmic_bytes"] == wl.n * (4 + 4 * (R - k_step))
     assert abs(k["copy_out"]["traffic_bytes"] - (c_read + c_write)) < 1.0
     assert abs(out["traffic_bytes"] - (s_read + s_write + c_read + c_write)) < 1.0
     assert bench.stored_traffic(wl, R, False, "copy_out_rmajor_kernel") == k["copy_out"]["traffic_bytes"]

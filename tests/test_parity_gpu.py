@@ -884,10 +884,11 @@ def test_graph_captured_whole_step_follows_the_schedule():
                                              (8, 8, "f32", 3, "f32", 65_539), (3, 5, "f32", 20, "bf16", 4_099),
                                              (2, 2, "f32", 5, "f32", 4_500_007), (2, 1, "bf16", 7, "bf16", 4_500_011)])
 def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
-    """The replicas written in the step kernel, in a copy-out pass of their own,
-    and by the automatic choice: all bitwise equal to the oracle, flat and
-    through a plan (ragged sizes; the last two cases span three 8 MB windows of
-    the copy-out pass, the last one partial, and replica counts that the
+    """The replicas written in the step kernel, in a copy-out pass of their own
+    (with the step kernel writing none, some or all of them first), and by the
+    automatic choice: all bitwise equal to the oracle, flat and through a plan
+    (ragged sizes; the last two cases span three 8 MB windows of the copy-out
+    pass, the last one partial, and replica counts that the
     replicas-per-workgroup grouping does not divide)."""
     log("copy-out modes G=%d W=%d %s R=%d %s n=%d" % (G, W, gdt, R, rdt, n))
     rng = np.random.default_rng(n)
@@ -903,10 +904,17 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
     sizes = [n // 3, 1, n - n // 3 - 1]
     default_shape = lsgd.get_launch_shape()
     try:
-        # the last pass: the copy-out pass on a grid of one workgroup per CU, striding
-        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO, "strided"):
+        # then the separate pass after a step kernel that writes the first 1, 3
+        # and R replicas itself; the last pass: the copy-out pass on a grid of
+        # one workgroup per CU, striding
+        for mode in (lsgd.COPY_OUT_FUSED, lsgd.COPY_OUT_SEPARATE, lsgd.COPY_OUT_AUTO, "k1", "k3", "kR",
+                     "strided"):
+            lsgd.set_step_replicas(-1)
             if mode == "strided":
                 lsgd.set_launch_shape(default_shape[0], 1, default_shape[2])
+                mode = lsgd.COPY_OUT_SEPARATE
+            elif isinstance(mode, str):
+                lsgd.set_step_replicas(R if mode == "kR" else int(mode[1:]))
                 mode = lsgd.COPY_OUT_SEPARATE
             lsgd.set_copy_out_mode(mode)
             p, m = to_dev(p0), torch.zeros(n, device=DEV)
@@ -941,6 +949,7 @@ def test_copy_out_pass_matches_oracle_in_every_mode(G, W, gdt, R, rdt, n):
             plan.close()
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+        lsgd.set_step_replicas(-1)
         lsgd.set_launch_shape(*default_shape)
 
 
