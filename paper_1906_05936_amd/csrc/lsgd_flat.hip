@@ -19,14 +19,15 @@ struct FlatPick {
     int tile;
 };
 
-// Compile-time (W, G) kernels for power-of-two counts up to 16 each (and
-// N <= 128); every other grouping takes the segmented runtime-layout kernel.
-// Both give the same bits.
+// Compile-time (W, G) kernels for power-of-two counts with N = W*G <= 128
+// (groups of up to 16 workers, or 32 to 128 workers in up to 4 groups, or 32
+// to 128 groups of up to 4 workers); every other grouping takes the segmented
+// runtime-layout kernel. Both give the same bits.
 // The compile-time kernel for (W, G), with parameters and momentum through
 // the caches when `cached` (instantiated only where cached_state_for holds).
 template <typename GT, int W, int G>
 FlatKernel flat_ct(bool cached) {
-    constexpr int U = tile_units<GT>(W * G);
+    constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
         if (cached) return step_flat_ct<GT, W, G, U, 1>;
     return step_flat_ct<GT, W, G, U, 0>;
@@ -42,6 +43,30 @@ FlatKernel pick_flat_g(int G, bool cached) {
         case 16:
             if constexpr (W * 16 <= kMaxWorkers) return flat_ct<GT, W, 16>(cached);
             else return nullptr;
+        case 32:
+            if constexpr (W <= 4) return flat_ct<GT, W, 32>(cached);
+            else return nullptr;
+        case 64:
+            if constexpr (W <= 2) return flat_ct<GT, W, 64>(cached);
+            else return nullptr;
+        case 128:
+            if constexpr (W == 1) return flat_ct<GT, W, 128>(cached);
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+// Groups of 32 to 128 workers, in up to 4 groups.
+template <typename GT, int W>
+FlatKernel pick_flat_big_w(int G, bool cached) {
+    switch (G) {
+        case 1: return flat_ct<GT, W, 1>(cached);
+        case 2:
+            if constexpr (W * 2 <= kMaxWorkers) return flat_ct<GT, W, 2>(cached);
+            else return nullptr;
+        case 4:
+            if constexpr (W * 4 <= kMaxWorkers) return flat_ct<GT, W, 4>(cached);
+            else return nullptr;
     }
     return nullptr;
 }
@@ -55,8 +80,11 @@ FlatPick pick_flat(int W, int G, bool cached) {
         case 4: k = pick_flat_g<GT, 4>(G, cached); break;
         case 8: k = pick_flat_g<GT, 8>(G, cached); break;
         case 16: k = pick_flat_g<GT, 16>(G, cached); break;
+        case 32: k = pick_flat_big_w<GT, 32>(G, cached); break;
+        case 64: k = pick_flat_big_w<GT, 64>(G, cached); break;
+        case 128: k = pick_flat_big_w<GT, 128>(G, cached); break;
     }
-    if (k) return FlatPick{k, tile_units<GT>(W * G)};
+    if (k) return FlatPick{k, tile_units<GT>(W * G, G)};
     return FlatPick{nullptr, 1};
 }
 

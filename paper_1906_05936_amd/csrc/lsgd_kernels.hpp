@@ -529,9 +529,12 @@ constexpr int kStreamFloats = 128;
 // stay at one unit: two units measured -1% at 4x4, +0.6% / -0.2% on the
 // 3.5e8-element 8x8 workload (step kernel alone / whole step), +1.6% at 8x8
 // and +4% at 16x8 on 2.6e7 elements.
+// With 32 or more groups the pairwise accumulator over groups holds
+// log2(G) + 1 partial sums of the tile, and four-unit tiles spilled to
+// scratch (2.3 KB per lane at 4x32 and 2x32): those kernels take two units.
 template <typename GT>
-constexpr int tile_units(int n_workers) {
-    return sizeof(GT) == 4 ? (n_workers * 2 * Unit<GT>::VEC <= kUnrollFloats ? 2 : 4) : 1;
+constexpr int tile_units(int n_workers, int n_groups = 1) {
+    return sizeof(GT) == 4 ? (n_workers * 2 * Unit<GT>::VEC <= kUnrollFloats || n_groups >= 32 ? 2 : 4) : 1;
 }
 
 // Pairwise sum of K leaves (compile-time K, a power of two) of T floats each:
@@ -696,7 +699,8 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
             for (int q = 0; q < U; ++q) load_grad<GT, TAIL>(g, e0[q], cnt, slice<VEC, T>(x, q));
         };
         float sum[T];
-        pw_tree<0, W, T>(member_leaf, sum);
+        if constexpr (W <= 16) pw_tree<0, W, T>(member_leaf, sum);
+        else pw_leaves<W, T, T>(member_leaf, sum);   // larger groups: members streamed through an accumulator
 #pragma unroll
         for (int v = 0; v < T; ++v) gm[v] = sum[v] * group_scale;
     };

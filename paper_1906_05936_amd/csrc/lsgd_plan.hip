@@ -73,7 +73,7 @@ PlanKernel plan_seg(int max_count, bool cached) {
 
 template <typename GT, int W, int G>
 PlanKernel plan_ct(bool cached) {
-    constexpr int U = tile_units<GT>(W * G);
+    constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
         if (cached) return step_plan_kernel<GT, W, G, U, 1>;
     return step_plan_kernel<GT, W, G, U, 0>;
@@ -89,12 +89,37 @@ PlanKernel pick_plan_g(int G, bool cached) {
         case 16:
             if constexpr (W * 16 <= kMaxWorkers) return plan_ct<GT, W, 16>(cached);
             else return nullptr;
+        case 32:
+            if constexpr (W <= 4) return plan_ct<GT, W, 32>(cached);
+            else return nullptr;
+        case 64:
+            if constexpr (W <= 2) return plan_ct<GT, W, 64>(cached);
+            else return nullptr;
+        case 128:
+            if constexpr (W == 1) return plan_ct<GT, W, 128>(cached);
+            else return nullptr;
     }
     return nullptr;
 }
 
-// The plan kernel for (W, G): compile-time for powers of two up to 16, with
-// parameters and momentum through the caches when `cached`; else segmented.
+// Groups of 32 to 128 workers, in up to 4 groups.
+template <typename GT, int W>
+PlanKernel pick_plan_big_w(int G, bool cached) {
+    switch (G) {
+        case 1: return plan_ct<GT, W, 1>(cached);
+        case 2:
+            if constexpr (W * 2 <= kMaxWorkers) return plan_ct<GT, W, 2>(cached);
+            else return nullptr;
+        case 4:
+            if constexpr (W * 4 <= kMaxWorkers) return plan_ct<GT, W, 4>(cached);
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+// The plan kernel for (W, G): compile-time for the power-of-two groupings of
+// pick_flat (lsgd_flat.hip), with parameters and momentum through the caches
+// when `cached`; else segmented.
 template <typename GT>
 PlanPick pick_plan(int W, int G, bool cached = false) {
     PlanKernel k = nullptr;
@@ -104,8 +129,11 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
         case 4: k = pick_plan_g<GT, 4>(G, cached); break;
         case 8: k = pick_plan_g<GT, 8>(G, cached); break;
         case 16: k = pick_plan_g<GT, 16>(G, cached); break;
+        case 32: k = pick_plan_big_w<GT, 32>(G, cached); break;
+        case 64: k = pick_plan_big_w<GT, 64>(G, cached); break;
+        case 128: k = pick_plan_big_w<GT, 128>(G, cached); break;
     }
-    if (k) return PlanPick{k, tile_units<GT>(W * G)};
+    if (k) return PlanPick{k, tile_units<GT>(W * G, G)};
     return PlanPick{plan_seg<GT>(W > G ? W : G, cached), SegTileUnits<GT>::U};
 }
 
@@ -166,12 +194,35 @@ lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t
 template <typename GT, int W>
 LarsKernel pick_lars_g(int G) {
     switch (G) {
-        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W)>;
-        case 2: return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2)>;
-        case 4: return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4)>;
-        case 8: return lars_norms_kernel<GT, W, 8, tile_units<GT>(W * 8)>;
+        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W, 1)>;
+        case 2: return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2, 2)>;
+        case 4: return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4, 4)>;
+        case 8: return lars_norms_kernel<GT, W, 8, tile_units<GT>(W * 8, 8)>;
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, tile_units<GT>(W * 16)>;
+            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, tile_units<GT>(W * 16, 16)>;
+            else return nullptr;
+        case 32:
+            if constexpr (W <= 4) return lars_norms_kernel<GT, W, 32, tile_units<GT>(W * 32, 32)>;
+            else return nullptr;
+        case 64:
+            if constexpr (W <= 2) return lars_norms_kernel<GT, W, 64, tile_units<GT>(W * 64, 64)>;
+            else return nullptr;
+        case 128:
+            if constexpr (W == 1) return lars_norms_kernel<GT, W, 128, tile_units<GT>(W * 128, 128)>;
+            else return nullptr;
+    }
+    return nullptr;
+}
+
+template <typename GT, int W>
+LarsKernel pick_lars_big_w(int G) {
+    switch (G) {
+        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W, 1)>;
+        case 2:
+            if constexpr (W * 2 <= kMaxWorkers) return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2, 2)>;
+            else return nullptr;
+        case 4:
+            if constexpr (W * 4 <= kMaxWorkers) return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4, 4)>;
             else return nullptr;
     }
     return nullptr;
@@ -186,6 +237,9 @@ LarsKernel pick_lars(int W, int G) {
         case 4: k = pick_lars_g<GT, 4>(G); break;
         case 8: k = pick_lars_g<GT, 8>(G); break;
         case 16: k = pick_lars_g<GT, 16>(G); break;
+        case 32: k = pick_lars_big_w<GT, 32>(G); break;
+        case 64: k = pick_lars_big_w<GT, 64>(G); break;
+        case 128: k = pick_lars_big_w<GT, 128>(G); break;
     }
     if (k) return k;
     return seg_levels(W > G ? W : G) == 5 ? lars_norms_seg<GT, 5> : lars_norms_seg<GT, 8>;

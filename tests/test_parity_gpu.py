@@ -111,6 +111,16 @@ STEP_CASES = [
     (4, 4, "f32", 2_000_003, 16, "f32", "contiguous"),
     (8, 8, "bf16", 4_000_003, 64, "bf16", "shuffled"),
     (16, 8, "f32", 2_000_003, 128, "f32", "shuffled"),
+    # compile-time kernels for 32 to 128 groups of few workers, and for groups
+    # of 32 to 128 workers (members streamed through an accumulator)
+    (32, 4, "f32", 300_007, 8, "f32", "shuffled"),
+    (32, 4, "bf16", 70_001, 2, "bf16", "shuffled"),
+    (64, 2, "f32", 50_001, 0, "f32", "shuffled"),
+    (128, 1, "f32", 9_999, 1, "f32", "shuffled"),
+    (4, 32, "f32", 60_003, 3, "f32", "shuffled"),
+    (2, 64, "bf16", 40_009, 1, "f32", "shuffled"),
+    (1, 128, "f32", 20_011, 2, "bf16", "contiguous"),
+    (1, 32, "bf16", 33_335, 1, "bf16", "contiguous"),
 ]
 
 
@@ -238,7 +248,8 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
 
 @pytest.mark.parametrize("G,W,gdt,R,rdt", [(4, 4, "f32", 16, "f32"), (2, 2, "f32", 0, "f32"),
                                            (8, 8, "bf16", 3, "bf16"), (3, 5, "f32", 1, "bf16"),
-                                           (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32")])
+                                           (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32"),
+                                           (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
