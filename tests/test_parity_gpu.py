@@ -121,6 +121,14 @@ STEP_CASES = [
     (2, 64, "bf16", 40_009, 1, "f32", "shuffled"),
     (1, 128, "f32", 20_011, 2, "bf16", "contiguous"),
     (1, 32, "bf16", 33_335, 1, "bf16", "contiguous"),
+    # non-power-of-two group counts with power-of-two groups, and groups of 3,
+    # 5 or 6 (the segmented kernel)
+    (3, 8, "f32", 100_003, 24, "f32", "shuffled"),
+    (6, 4, "bf16", 50_001, 2, "bf16", "shuffled"),
+    (12, 8, "f32", 30_007, 1, "f32", "shuffled"),
+    (4, 6, "f32", 65_537, 24, "f32", "shuffled"),
+    (9, 1, "bf16", 5_555, 0, "f32", "contiguous"),
+    (3, 2, "f32", 4_101, 6, "f32", "shuffled"),
 ]
 
 
