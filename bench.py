@@ -768,13 +768,13 @@ def step_replicas(wl, R):
 
 def library_ranges(n):
     """The element ranges in which the library runs a flat step whose copy-out
-    is a pass of its own (the step kernel, then the copy-out, range by range):
-    one range up to 2^26 elements, else ceil(n / 2^25) ranges starting on
-    multiples of 2048 elements."""
+    is a pass of its own, or which writes no replicas (the step kernel, then
+    the copy-out, range by range): one range up to 2^26 elements, else
+    ceil(n / 2^24) ranges starting on multiples of 2^20 elements."""
     if n <= 1 << 26:
         return [(0, n)]
-    K = (n + (1 << 25) - 1) >> 25
-    edges = [(n // K * i) // 2048 * 2048 for i in range(K)] + [n]
+    K = (n + (1 << 24) - 1) >> 24
+    edges = [(n // K * i) >> 20 << 20 for i in range(K)] + [n]
     return list(zip(edges[:-1], edges[1:]))
 
 
@@ -813,8 +813,9 @@ def derive_traffic(args):
     per_alg = {kname: wl.algorithmic_bytes(k)}
     if split:
         per_alg["copy_out"] = wl.n * (4 + (R - k) * rb)
-    # a flat step with a copy-out pass runs each kernel once per element range
-    launches = len(library_ranges(wl.n)) if split and not wl.tensor_sizes else 1
+    # a flat step with a copy-out pass, or without replicas, runs each kernel
+    # once per element range
+    launches = len(library_ranges(wl.n)) if (split or R == 0) and not wl.tensor_sizes else 1
     per = {}
     for k, a in per_alg.items():
         f_k, nf = _per_dispatch_kib(fetch_rows, "FETCH_SIZE", k)

@@ -166,24 +166,34 @@ lsgd_status launch_copy_out(StepArgs& a, void* stream) {
     return launch_copy_out_rmajor<4, kCopyUF32, kCopyRKF32>(a, s);
 }
 
-// With the copy-out as a pass of its own, long vectors are processed range by
-// range: the step kernel over one range of elements, then its copy passes over
-// that range, then the next range. The copy-out pass then reads the new
+// Long vectors are processed range by range, unless one pass writes the
+// replicas too: the step kernel over one range of elements (then, with the
+// copy-out as a pass of its own, its copy passes over that range), then the
+// next range. The copy-out pass then reads the new
 // parameters of a range soon after the step kernel wrote them (a range of
-// kRangeElems holds 128 MB of parameters, which the 256 MB Infinity Cache
-// still holds) instead of after the whole vector. Measured on the 3.5e8-element
-// 8x8 bfloat16 step with 64 replicas, same process: 2, 4, 8, 16 and 32 ranges
-// against one +0.5%, +1.4%, +3.3%, +3.2% and +0.9%; on the 2.6e7-element
-// 4x4 step two ranges lost 0.6%, so vectors up to kRangeSplitMin stay whole.
+// kRangeElems holds 64 MB of parameters, which the 256 MB Infinity Cache
+// still holds) instead of after the whole vector, and the step kernel alone
+// runs faster over ranges than over the whole vector in one launch. Measured
+// on the 3.5e8-element 8x8 bfloat16 step, same process: with no replicas,
+// ranges of 2^23, 2^24 and 2^26 elements +3.1%, +3.3% and +2.6% against one
+// launch; with 64 replicas and the copy-out pass, +1.5%, +1.9% and +1.8%
+// against ranges of 2^25 whose edges were not 2 MB apart (such ranges were no
+// faster than one launch without replicas). On the 2.6e7-element 4x4 step two
+// ranges lost 0.6%, so vectors up to kRangeSplitMin stay whole.
 // Results are the same bits (every element is computed on its own).
-constexpr int64_t kRangeElems = int64_t{1} << 25;
+constexpr int64_t kRangeElems = int64_t{1} << 24;
 constexpr int64_t kRangeSplitMin = int64_t{1} << 26;
+// Range edges fall on multiples of kRangeAlign elements: 2 MB or more in every
+// buffer, so buffers that start at the same offset modulo 2 MB (as separate
+// large allocations do) keep doing so within every range.
+constexpr int64_t kRangeAlign = int64_t{1} << 20;
 
 int64_t split_ranges(int64_t n) { return n > kRangeSplitMin ? (n + kRangeElems - 1) / kRangeElems : 1; }
 
-// Start of range i of K over n elements (range K ends at n); starts are
-// multiples of 2048 elements, so every buffer of a range stays 16-byte aligned.
-int64_t range_edge(int64_t n, int64_t K, int64_t i) { return i >= K ? n : (n / K * i) / 2048 * 2048; }
+// Start of range i of K over n elements (range K ends at n). With K > 1 the
+// vector is longer than 4 * kRangeElems, so every range holds at least
+// kRangeElems / 2 elements.
+int64_t range_edge(int64_t n, int64_t K, int64_t i) { return i >= K ? n : (n / K * i) / kRangeAlign * kRangeAlign; }
 
 // The arguments of a step restricted to elements [lo, hi): every per-element
 // pointer advanced by lo elements (R replica pointers of rsz bytes).
@@ -331,7 +341,7 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     // Copies per element besides parameters and momentum: the replicas, and
     // with the broadcast the mean gradient to the other N - 1 members. Split
     // off, the step kernel writes the mean gradient to the first member only
-    // and copy passes of their own write the rest, range by range (split_ranges).
+    // and copy passes of their own write the rest (range by range: split_ranges).
     const int32_t bcast_copies = bcast ? n_workers - 1 : 0;
     const bool split = separate_copy_out_bytes(
         n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n);
@@ -340,7 +350,9 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const int32_t k_step = split ? replicas_in_step(n_workers, n_replicas, dtype_size(rdt), n) : n_replicas;
     a.n_replicas = k_step;
     const char* what = literal ? "lsgd_step_ex" : "lsgd_step";
-    const int64_t K = split ? split_ranges(n) : 1;
+    // a fused pass that writes replicas or broadcast copies stays one launch
+    // (ranges measured 0.8% slower there: 3.5e8-element 8x8 bfloat16 step, 64 replicas)
+    const int64_t K = split || (n_replicas == 0 && !bcast) ? split_ranges(n) : 1;
     for (int64_t i = 0; i < K; ++i) {
         const int64_t lo = range_edge(n, K, i), hi = range_edge(n, K, i + 1);
         StepArgs ra = K == 1 ? a : offset_args(a, lo, hi, dtype_size(gdt), dtype_size(rdt), n_replicas);
@@ -348,7 +360,8 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
         ra.xcd_chunk = ls.xcd_chunk;
         ra.upl = ls.upl;
         hipLaunchKernelGGL(k.kernel, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), ra);
-        if ((st = check_launch(what)) != LSGD_OK || !split) return st;
+        if ((st = check_launch(what)) != LSGD_OK) return st;
+        if (!split) continue;
         if (n_replicas > k_step) {
             for (int32_t r = k_step; r < n_replicas; ++r) ra.replicas[r - k_step] = ra.replicas[r];
             ra.n_replicas = n_replicas - k_step;
@@ -474,7 +487,7 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
     const bool split = separate_copy_out_update(n_replicas, dtype_size(rdt), use_cached_state(1, n));
     if (split) a.n_replicas = 0;
     const FlatKernel sk = use_cached_state(1, n) ? sgd_kernel<kSgdTile, 1> : sgd_kernel<kSgdTile, 0>;
-    const int64_t K = split ? split_ranges(n) : 1;   // range by range, as lsgd_step
+    const int64_t K = split || n_replicas == 0 ? split_ranges(n) : 1;   // range by range, as lsgd_step
     for (int64_t i = 0; i < K; ++i) {
         const int64_t lo = range_edge(n, K, i), hi = range_edge(n, K, i + 1);
         StepArgs ra = K == 1 ? a : offset_args(a, lo, hi, 4, dtype_size(rdt), n_replicas);
@@ -482,7 +495,8 @@ LSGD_API lsgd_status lsgd_sgd_step(float* params, float* momentum, const float* 
         ra.xcd_chunk = ls.xcd_chunk;
         ra.upl = ls.upl;
         hipLaunchKernelGGL(sk, dim3(ls.blocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), ra);
-        if ((st = check_launch("lsgd_sgd_step")) != LSGD_OK || !split) return st;
+        if ((st = check_launch("lsgd_sgd_step")) != LSGD_OK) return st;
+        if (!split) continue;
         ra.n_replicas = n_replicas;
         if ((st = launch_copy_out(ra, stream)) != LSGD_OK) return st;
     }

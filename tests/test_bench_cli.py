@@ -136,20 +136,21 @@ def test_all_cores_cpu_baseline_runs_the_oracle_on_blocks(monkeypatch):
 
 
 def test_library_ranges_cover_the_vector():
-    """The element ranges of a long flat step with a copy-out pass: one range up
-    to 2^26 elements; beyond, ceil(n / 2^25) contiguous ranges that start on
-    multiples of 2048 elements and cover [0, n)."""
+    """The element ranges of a long flat step with a copy-out pass (or without
+    replicas): one range up to 2^26 elements; beyond, ceil(n / 2^24) contiguous
+    ranges of at least 2^23 elements that start on multiples of 2^20 elements
+    (2 MB in a buffer of 2-byte elements) and cover [0, n)."""
     assert bench.library_ranges(1 << 26) == [(0, 1 << 26)]
-    for n in ((1 << 26) + 1, 350_000_000, (1 << 26) + (1 << 25) + 12_345):
+    for n in ((1 << 26) + 1, 350_000_000, 352_321_536, (1 << 26) + (1 << 25) + 12_345, (1 << 31) + 7):
         r = bench.library_ranges(n)
-        assert len(r) == -(-n // (1 << 25))
+        assert len(r) == -(-n // (1 << 24))
         assert r[0][0] == 0 and r[-1][1] == n
-        assert all(a % 2048 == 0 and a < b for a, b in r)
+        assert all(a % (1 << 20) == 0 and b - a >= 1 << 23 for a, b in r)
         assert all(r[i][1] == r[i + 1][0] for i in range(len(r) - 1))
 
 
 def test_derive_traffic_counts_every_range_launch(tmp_path, monkeypatch):
-    """A step run in element ranges (the 3.5e8-element workload: 11 launches of
+    """A step run in element ranges (the 3.5e8-element workload: 21 launches of
     each kernel per step): the per-dispatch counters are scaled to the step."""
     wl = workloads.WORKLOADS["large"]
     R = wl.n_workers

@@ -521,11 +521,12 @@ def test_workload_full_size_every_element(name):
 
 
 def test_long_vectors_in_ranges_match_oracle():
-    """Vectors above 2^26 elements whose copy-out runs as a pass of its own are
-    processed range by range (the step kernel, then its copy passes, over
-    ranges of about 2^25 elements): lsgd_step with the literal reduction and
-    the gradient broadcast, and lsgd_sgd_step, against the oracle on every
-    element, on a length that leaves four ranges and a ragged end."""
+    """Vectors above 2^26 elements whose copy-out runs as a pass of its own, or
+    which have no replicas, are processed range by range (the step kernel, then
+    its copy passes, over ranges of about 2^24 elements): lsgd_step with the
+    literal reduction and the gradient broadcast, lsgd_step without replicas,
+    and lsgd_sgd_step with and without replicas, against the oracle on every
+    element, on a length that leaves seven ranges and a ragged end."""
     n = (1 << 26) + (1 << 25) + 12_345
     G, W, R = 2, 2, 2
     T = fullsize.host_threads()
@@ -564,9 +565,24 @@ def test_long_vectors_in_ranges_match_oracle():
         assert_close(to_host(m2), m_ref2, "sgd momentum")
         for r in range(R):
             assert np.array_equal(to_host(reps[r]), rr2), "sgd replica %d" % r
+        # no replicas: the step kernel alone, range by range (automatic mode)
+        lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
+        p3, m3 = torch.from_numpy(p0).to(DEV), torch.from_numpy(m0).to(DEV)
+        lsgd.step(p3, m3, grads, gow, G, 0.1, 0.9, 1e-4, [])
+        lsgd.sgd_step(p2, m2, gbar, 0.1, 0.9, 1e-4, [])
+        torch.cuda.synchronize()
+        p_ref3, m_ref3 = p0.copy(), m0.copy()        # gh: the broadcast gradients, as on the device
+        fullsize.run_blocks(lambda a, b: oracle.lsgd_step(p_ref3[a:b], m_ref3[a:b], [x[a:b] for x in gh], gow, G,
+                                                          0.1, 0.9, 1e-4, []), n, T)
+        assert_close(to_host(p3), p_ref3, "params (no replicas)")
+        assert_close(to_host(m3), m_ref3, "momentum (no replicas)")
+        fullsize.run_blocks(lambda a, b: oracle.sgd_step(p_ref2[a:b], m_ref2[a:b], gh[0][a:b], 0.1, 0.9, 1e-4, []),
+                            n, T)
+        assert_close(to_host(p2), p_ref2, "sgd params (no replicas)")
+        assert_close(to_host(m2), m_ref2, "sgd momentum (no replicas)")
     finally:
         lsgd.set_copy_out_mode(lsgd.COPY_OUT_AUTO)
-    del grads, reps, p, m, p2, m2
+    del grads, reps, p, m, p2, m2, p3, m3
     torch.cuda.empty_cache()
 
 
