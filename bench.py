@@ -754,7 +754,9 @@ def separate_copy_out(wl, R, mode="auto", bcast=False):
     if mode == "separate":
         return True
     cached = wl.n_workers <= 16 and 8 * wl.n <= (288 << 20)   # parameters and momentum through the caches
-    return copy_bytes >= (64 if cached else 32) or wl.n_workers * wl.grad_bytes >= 256
+    segmented = kernel_match(wl).endswith("_seg")             # runtime group layouts
+    crossing = (48 if segmented else 64) if cached else 32
+    return copy_bytes >= crossing or wl.n_workers * wl.grad_bytes >= 256
 
 
 def step_replicas(wl, R):

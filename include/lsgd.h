@@ -139,9 +139,10 @@ LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_p
  * mostly from cache) and writes the replicas one window of the vector at a
  * time. Results are identical either way. LSGD_COPY_OUT_AUTO (the default)
  * takes the separate pass where it measured faster: for the fused steps when
- * the replica bytes R*s_r per element are at least 32 (64 for at most 16
+ * the replica bytes R*s_r per element are at least 32 (for at most 16
  * workers with parameters and momentum within 288 MB, whose step kernels
- * access them through the caches) or the gradient bytes N*s_g at least 256;
+ * access them through the caches: 64 with power-of-two groups and group
+ * counts, 48 for other group layouts) or the gradient bytes N*s_g at least 256;
  * for lsgd_sgd_step and the LARS update when R*s_r >= 16 (parameters and
  * momentum within 288 MB; beyond, binary32 replicas and R >= 4).
  * Process-wide, for launches after the call returns. Errors: LSGD_ERR_SIZE

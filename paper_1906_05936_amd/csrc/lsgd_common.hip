@@ -163,18 +163,18 @@ int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_ord
 // (use_cached_state) the fused pass gains more, and the crossing moves to 64
 // bytes: at 32 the fused pass won by 2-4% (4x4 R = 8, 2x2 R = 8, 4x4
 // bfloat16 R = 16), at 64 the separate one by 3-12% (4x4 R = 16, 2x2 R = 16,
-// the ResNet-50 plan), at 256 by 28%.
-bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n) {
+// the ResNet-50 plan), at 256 by 28%. The segmented kernels (runtime group
+// layouts) cross earlier there: the separate pass won by 5-8% at 56 and 60
+// replica bytes (2x7, 3x5, 5x3 binary32) and lost by 3-8% at 24 and 36 (2x3,
+// 3x2, 1x9), so their crossing is 48 bytes.
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool segmented) {
     if (copy_bytes <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
     const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
-    return copy_bytes >= (use_cached_state(n_workers, n) ? 64 : 32) || grad_bytes >= 256;
-}
-
-bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n) {
-    return separate_copy_out_bytes(n_workers, gsz, static_cast<int64_t>(n_replicas) * static_cast<int64_t>(rsz), n);
+    const int64_t crossing = !use_cached_state(n_workers, n) ? 32 : segmented ? 48 : 64;
+    return copy_bytes >= crossing || grad_bytes >= 256;
 }
 
 // With the separate copy-out the step kernel still writes the first k replicas

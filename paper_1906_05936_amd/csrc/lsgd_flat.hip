@@ -89,11 +89,16 @@ FlatPick pick_flat(int W, int G, bool cached) {
 }
 
 // Runtime group layouts: accumulator levels for the largest count.
+// (the cached forms exist for counts up to 31, the only ones they can have)
 template <typename GT>
 FlatPick pick_flat_seg(int max_count, bool cached) {
     constexpr int U = SegTileUnits<GT>::U;
-    if (seg_levels(max_count) != 5) return FlatPick{step_flat_seg<GT, 8, U, 0>, U};
-    return FlatPick{cached ? step_flat_seg<GT, 5, U, 1> : step_flat_seg<GT, 5, U, 0>, U};
+    switch (seg_levels(max_count)) {
+        case 3: return FlatPick{cached ? step_flat_seg<GT, 3, U, 1> : step_flat_seg<GT, 3, U, 0>, U};
+        case 4: return FlatPick{cached ? step_flat_seg<GT, 4, U, 1> : step_flat_seg<GT, 4, U, 0>, U};
+        case 5: return FlatPick{cached ? step_flat_seg<GT, 5, U, 1> : step_flat_seg<GT, 5, U, 0>, U};
+    }
+    return FlatPick{step_flat_seg<GT, 8, U, 0>, U};
 }
 
 using MeanKernel = void (*)(MeanArgs);
@@ -114,7 +119,12 @@ MeanPick pick_group_mean(int W) {
         case 8: return MeanPick{group_mean_kernel_ct<GT, 8, U>, U};
         case 16: return MeanPick{group_mean_kernel_ct<GT, 16, U>, U};
     }
-    return MeanPick{seg_levels(W) == 5 ? group_mean_kernel<GT, 5> : group_mean_kernel<GT, 8>, 1};
+    switch (seg_levels(W)) {
+        case 3: return MeanPick{group_mean_kernel<GT, 3>, 1};
+        case 4: return MeanPick{group_mean_kernel<GT, 4>, 1};
+        case 5: return MeanPick{group_mean_kernel<GT, 5>, 1};
+    }
+    return MeanPick{group_mean_kernel<GT, 8>, 1};
 }
 
 // Global mean: compile-time G for powers of two up to 128, else runtime G.
@@ -129,7 +139,12 @@ MeanPick pick_global_mean(int G) {
         case 64: return MeanPick{global_mean_kernel_ct<64, 2>, 2};
         case 128: return MeanPick{global_mean_kernel_ct<128, 2>, 2};
     }
-    return MeanPick{seg_levels(G) == 5 ? global_mean_kernel<5> : global_mean_kernel<8>, 1};
+    switch (seg_levels(G)) {
+        case 3: return MeanPick{global_mean_kernel<3>, 1};
+        case 4: return MeanPick{global_mean_kernel<4>, 1};
+        case 5: return MeanPick{global_mean_kernel<5>, 1};
+    }
+    return MeanPick{global_mean_kernel<8>, 1};
 }
 
 size_t dtype_size(lsgd_dtype d) { return d == LSGD_BF16 ? 2 : 4; }
@@ -328,7 +343,8 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const bool cached = use_cached_state(n_workers, n);
     if (W > 0)
         k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(W, n_groups, cached) : pick_flat<float>(W, n_groups, cached);
-    if (!k.kernel) {
+    const bool segmented = !k.kernel;
+    if (segmented) {
         // runtime layout: group j is members [start[j], start[j+1]) of the member order
         int32_t max_count = n_groups;
         for (int32_t j = 0; j <= n_groups; ++j) {
@@ -344,7 +360,8 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     // and copy passes of their own write the rest (range by range: split_ranges).
     const int32_t bcast_copies = bcast ? n_workers - 1 : 0;
     const bool split = separate_copy_out_bytes(
-        n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n);
+        n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n,
+        segmented);
     a.bcast_grad = bcast ? (split ? 1 : n_workers) : 0;
     // split: the step kernel writes the first k replicas, the copy-out pass the rest
     const int32_t k_step = split ? replicas_in_step(n_workers, n_replicas, dtype_size(rdt), n) : n_replicas;

@@ -68,13 +68,12 @@ LaunchShape launch_shape(int64_t units, int tile = 1);
 // The launch shape's passes per workgroup (units_per_lane).
 int32_t launch_passes_per_block();
 
-// Whether a step with N gradients of gsz bytes, R replicas of rsz bytes and n
-// elements writes its replicas in a copy-out pass of its own
-// (lsgd_set_copy_out_mode).
-bool separate_copy_out(int32_t n_workers, size_t gsz, int32_t n_replicas, size_t rsz, int64_t n);
-// The same rule for `copy_bytes` bytes per element of copies (replicas, and
-// the gradient broadcast's copies of the mean gradient to the other members).
-bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n);
+// Whether a step with N gradients of gsz bytes, n elements and `copy_bytes`
+// bytes per element of copies (replicas, and the gradient broadcast's copies
+// of the mean gradient to the other members) writes them in copy passes of
+// their own (lsgd_set_copy_out_mode); `segmented`: the step runs a
+// runtime-layout (segmented) kernel.
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool segmented);
 // With the separate copy-out: how many of the n_replicas replicas (rsz bytes
 // each) the step kernel still writes itself; the copy-out pass writes the
 // rest (lsgd_set_step_replicas).

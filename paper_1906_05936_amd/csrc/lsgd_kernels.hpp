@@ -438,8 +438,17 @@ __device__ __forceinline__ void pw_segments(int N, int G, const Ptr& ptr, const 
 }
 
 // Accumulator levels for runtime counts up to `max_count` (host side): the
-// segmented kernels are built for 5 levels (counts up to 31) and 8 (255).
-__host__ __device__ constexpr int seg_levels(int max_count) { return max_count <= 31 ? 5 : 8; }
+// segmented kernels are built for 3, 4, 5 and 8 levels (counts up to 7, 15,
+// 31 and 255). Every level holds a tile of partial sums in registers, so the
+// smallest sufficient form runs more waves per SIMD (binary32 step kernel:
+// 200 VGPRs at 5 levels, 168 at 3). Measured on the ResNet-50 size against
+// 5 levels for everything up to 31, same process: unequal groups 2, 3, 5, 6
+// +6.9% (R = 16), 6x4 +6.9%, 2x3 +5.8%, 4x6 +3.3% with 3 levels; 12x8 +2.1%
+// and 4x10 +1.2% with 4; without replicas +3.5% to +20%; one loss, 3x5 with
+// its 15 replicas written by the step kernel, -2.5%.
+__host__ __device__ constexpr int seg_levels(int max_count) {
+    return max_count <= 7 ? 3 : max_count <= 15 ? 4 : max_count <= 31 ? 5 : 8;
+}
 
 // ------------------------------------------------------------- the update
 

@@ -51,10 +51,12 @@ using LarsKernel = void (*)(LarsArgs);
 // 64-float (256-byte) boundary.
 constexpr int64_t kGbarAlign = 64;
 
-// A kernel and the units per lane tile it processes.
+// A kernel, the units per lane tile it processes, and whether it is the
+// segmented (runtime-layout) form.
 struct PlanPick {
     PlanKernel kernel;
     int tile;
+    bool segmented;
 };
 
 // Elements per piece and per bucket: one tile pass of the plan's kernel.
@@ -67,8 +69,12 @@ static_assert(piece_elems<float>(1) % 8 == 0 && piece_elems<uint16_t>(1) % 8 == 
 // (the cached form exists for counts up to 31, the only ones it can have).
 template <typename GT>
 PlanKernel plan_seg(int max_count, bool cached) {
-    if (seg_levels(max_count) != 5) return step_plan_seg<GT, 8, 0>;
-    return cached ? step_plan_seg<GT, 5, 1> : step_plan_seg<GT, 5, 0>;
+    switch (seg_levels(max_count)) {
+        case 3: return cached ? step_plan_seg<GT, 3, 1> : step_plan_seg<GT, 3, 0>;
+        case 4: return cached ? step_plan_seg<GT, 4, 1> : step_plan_seg<GT, 4, 0>;
+        case 5: return cached ? step_plan_seg<GT, 5, 1> : step_plan_seg<GT, 5, 0>;
+    }
+    return step_plan_seg<GT, 8, 0>;
 }
 
 template <typename GT, int W, int G>
@@ -133,8 +139,8 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
         case 64: k = pick_plan_big_w<GT, 64>(G, cached); break;
         case 128: k = pick_plan_big_w<GT, 128>(G, cached); break;
     }
-    if (k) return PlanPick{k, tile_units<GT>(W * G, G)};
-    return PlanPick{plan_seg<GT>(W > G ? W : G, cached), SegTileUnits<GT>::U};
+    if (k) return PlanPick{k, tile_units<GT>(W * G, G), false};
+    return PlanPick{plan_seg<GT>(W > G ? W : G, cached), SegTileUnits<GT>::U, true};
 }
 
 lsgd_status check_device(const lsgd_plan* plan) {
@@ -242,7 +248,12 @@ LarsKernel pick_lars(int W, int G) {
         case 128: k = pick_lars_big_w<GT, 128>(G); break;
     }
     if (k) return k;
-    return seg_levels(W > G ? W : G) == 5 ? lars_norms_seg<GT, 5> : lars_norms_seg<GT, 8>;
+    switch (seg_levels(W > G ? W : G)) {
+        case 3: return lars_norms_seg<GT, 3>;
+        case 4: return lars_norms_seg<GT, 4>;
+        case 5: return lars_norms_seg<GT, 5>;
+    }
+    return lars_norms_seg<GT, 8>;
 }
 
 // LARS workspace layout: [gbar scratch | per-chunk partials | trust ratios],
@@ -557,10 +568,12 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     // equal groups (W > 0): the compile-time kernels for powers of two, for
     // either reduction; the segmented kernel otherwise
     PlanKernel k = nullptr;
+    bool segmented = true;
     if (plan->W > 0) {
         const PlanPick pk = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached)
                                                    : pick_plan<float>(plan->W, plan->n_groups, cached);
         k = pk.kernel;
+        segmented = pk.segmented;
     } else {
         const int32_t max_count = std::max(plan->max_group, plan->n_groups);
         k = plan->gdt == LSGD_BF16 ? plan_seg<uint16_t>(max_count, cached) : plan_seg<float>(max_count, cached);
@@ -572,7 +585,7 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     const bool split = separate_copy_out_bytes(
         plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4,
         static_cast<int64_t>(plan->n_replicas) * (plan->rdt == LSGD_BF16 ? 2 : 4) + 4 * bcast_copies,
-        plan->total_elems);
+        plan->total_elems, segmented);
     a.bcast_grad = bcast ? (split ? 1 : plan->n_workers) : 0;
     // split: the step kernel writes the first k replicas, the copy-out pass the rest
     const int32_t k_step = split ? replicas_in_step(plan->n_workers, plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,

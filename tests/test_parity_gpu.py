@@ -129,6 +129,11 @@ STEP_CASES = [
     (4, 6, "f32", 65_537, 24, "f32", "shuffled"),
     (9, 1, "bf16", 5_555, 0, "f32", "contiguous"),
     (3, 2, "f32", 4_101, 6, "f32", "shuffled"),
+    # the segmented kernel's accumulator forms: counts up to 7 take 3 levels
+    # (above), up to 15 four, up to 31 five, larger eight (1 x 100 above)
+    (1, 9, "f32", 6_007, 3, "f32", "contiguous"),
+    (20, 3, "f32", 7_001, 2, "f32", "shuffled"),
+    (3, 20, "bf16", 5_003, 1, "bf16", "shuffled"),
 ]
 
 
@@ -206,7 +211,10 @@ def test_fixed_point_on_gpu():
 @pytest.mark.parametrize("G,W,gdt,n,R,rdt", [(4, 4, "f32", 100_003, 2, "f32"),
                                              (8, 8, "bf16", 20_001, 1, "bf16"),
                                              (3, 5, "f32", 7_777, 0, "f32"),
-                                             (1, 1, "bf16", 5, 1, "f32")])
+                                             (1, 1, "bf16", 5, 1, "f32"),
+                                             (12, 8, "f32", 9_001, 1, "f32"),
+                                             (2, 12, "bf16", 3_001, 0, "f32"),
+                                             (20, 3, "f32", 4_003, 0, "f32")])
 def test_unfused_calls_match_oracle_and_fused(G, W, gdt, n, R, rdt):
     log("unfused G=%d W=%d %s n=%d" % (G, W, gdt, n))
     rng = np.random.default_rng(n)
@@ -257,7 +265,8 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
 @pytest.mark.parametrize("G,W,gdt,R,rdt", [(4, 4, "f32", 16, "f32"), (2, 2, "f32", 0, "f32"),
                                            (8, 8, "bf16", 3, "bf16"), (3, 5, "f32", 1, "bf16"),
                                            (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32"),
-                                           (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16")])
+                                           (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16"),
+                                           (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
