@@ -29,14 +29,40 @@ CFLAGS = [
 ]
 
 
+# Every kernel keeps its working set in registers: one that spills to scratch
+# memory runs far below the bandwidth bound (a four-unit 16x4 step kernel
+# spilled 2.3 KB per lane and ran at half speed). The compiler's per-kernel
+# resource remarks are read back and a spilling kernel fails the build.
+RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage"]
+
+
+def spilling_kernels(remarks: str):
+    """(kernel, scratch bytes per lane) for every kernel whose resource-usage
+    remark reports scratch memory."""
+    import re
+    out, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and int(m.group(1)) > 0:
+            out.append((name, int(m.group(1))))
+    return out
+
+
 def _compile(src, verbose):
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + CFLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + CFLAGS + RESOURCE_REMARKS + ["-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, r.stdout, r.stderr))
+    spills = spilling_kernels(r.stderr)
+    if spills:
+        raise RuntimeError("kernels of %s spill to scratch memory (bytes per lane): %s"
+                           % (src, ", ".join("%s %d" % k for k in spills)))
     return obj
 
 

@@ -111,6 +111,7 @@ STEP_CASES = [
     (4, 4, "f32", 2_000_003, 16, "f32", "contiguous"),
     (8, 8, "bf16", 4_000_003, 64, "bf16", "shuffled"),
     (16, 8, "f32", 2_000_003, 128, "f32", "shuffled"),
+    (16, 4, "f32", 2_000_003, 8, "f32", "shuffled"),    # 16 groups of 4: two-unit tiles
     # compile-time kernels for 32 to 128 groups of few workers, and for groups
     # of 32 to 128 workers (members streamed through an accumulator)
     (32, 4, "f32", 300_007, 8, "f32", "shuffled"),
@@ -266,7 +267,8 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
                                            (8, 8, "bf16", 3, "bf16"), (3, 5, "f32", 1, "bf16"),
                                            (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32"),
                                            (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16"),
-                                           (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32")])
+                                           (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
+                                           (16, 4, "f32", 2, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
