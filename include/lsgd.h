@@ -226,11 +226,16 @@ LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* 
  * and writes parameters and momentum once; the group means and the mean
  * gradient stay in registers. The replicas are written either by that kernel
  * or, where lsgd_set_copy_out_mode's rule takes the separate form (the
- * default at 64 or more replica bytes per element with up to 16 workers), by
- * a copy-out pass launched right after it, which reads the new parameters
- * once more. Arguments as for the three calls above. The results are
+ * default with up to 16 workers at 64 or more replica bytes per element for
+ * power-of-two groups and counts, 48 for other group layouts), by a copy-out
+ * pass launched right after it, which reads the new parameters once more
+ * (the step kernel then still writes the first lsgd_set_step_replicas
+ * replicas). Vectors longer than 2^26 elements are processed range by range
+ * (about 2^24 elements each, edges on multiples of 2^20 elements: the step
+ * kernel, then its copy-out pass) unless the step kernel writes every
+ * replica itself. Arguments as for the three calls above. The results are
  * bit-identical to lsgd_group_mean, then lsgd_global_mean, then
- * lsgd_sgd_step, in either form.
+ * lsgd_sgd_step, in every form.
  */
 LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
                                lsgd_dtype gdt, int32_t n_workers,
@@ -323,7 +328,8 @@ LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int
  * launch. The plan copies a chunk table and a pointer table to device memory
  * once; lsgd_step_plan then launches one kernel. Tensors are cut into pieces
  * of 2048 elements (4096 for binary32 gradients with more than 16 workers in
- * power-of-two groups; times the launch shape's units_per_lane at creation);
+ * power-of-two groups, except 32 or more groups and 16 groups of 4; times the
+ * launch shape's units_per_lane at creation);
  * small tensors are bucketed so that one workgroup covers several of them.
  *   numel     [n_tensors] host int64, elements of each tensor (>= 0).
  *   params, momentum [n_tensors] device pointers (binary32).
