@@ -371,14 +371,24 @@ __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x
 // Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
 
-// Member gradient loads a lane holds in one register batch of the segmented sum.
-constexpr int kSegBatch = 8;
+// Member gradient loads a lane holds in one register batch of the segmented
+// sum: 8 for binary32 gradients, 4 for bfloat16. The consume code is unrolled
+// over a batch, once per batch register set, and with it every group's
+// finishing code: at 8 loads the bfloat16 kernels took 78-156 KB of code
+// (binary32 64-129 KB, the compile-time kernels 11-36 KB), more than the
+// instruction cache that two CUs share. Halving the bfloat16 batch (42-80 KB)
+// measured on the ResNet-50 size, same process: 2x3 +9% (R = N) / +14%
+// (R = 0), 6x4 +6% / +10%, 3x32 +19% / +85%, 12x1 and 5x16 within 1%. For
+// binary32 the same change was mixed (12x1 +8%, 2x3 +1%, 12x8 -1% / -2%, 3x32
+// -2%), so it keeps 8.
+template <typename GT>
+constexpr int seg_batch() { return sizeof(GT) == 2 ? 4 : 8; }
 
 // Pairwise sums of consecutive runs of the N member-ordered gradients of one
 // lane tile (U units, stream-major), for group layouts known only at run time:
 // group j holds members [gs(j), gs(j+1)), j < G, and done(j, sum) receives PW
 // over them for every element of the tile. Loads run ahead of the additions
-// in two alternating register batches of kSegBatch loads (kSegBatch / U
+// in two alternating register batches of seg_batch loads (seg_batch / U
 // members) that ignore group boundaries, so a lane keeps between one and two
 // batches of 128-bit loads in flight whatever the group sizes. Each group is
 // folded through a binary-counter accumulator (LV levels: sizes below 2^LV).
@@ -388,8 +398,8 @@ __device__ __forceinline__ void pw_segments(int N, int G, const Ptr& ptr, const 
                                             int cnt, const Done& done) {
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
-    constexpr int B = kSegBatch / U;
-    static_assert(B >= 1 && B * U == kSegBatch, "the batch holds whole members");
+    constexpr int B = seg_batch<GT>() / U;
+    static_assert(B >= 1 && B * U == seg_batch<GT>(), "the batch holds whole members");
     u32x4 xa[B][U], xb[B][U];
     PwAcc<T, LV> acc;
     int j = 0;
