@@ -768,15 +768,22 @@ def step_replicas(wl, R):
     return min(R, 16 // rb) if cached else 0
 
 
+# The library's range rule for long flat steps (kRangeSplitMin, kRangeElems and
+# kRangeAlign of lsgd_flat.hip, which a CPU test compares with these).
+RANGE_SPLIT_MIN = 1 << 26
+RANGE_ELEMS = 1 << 24
+RANGE_ALIGN = 1 << 20
+
+
 def library_ranges(n):
     """The element ranges in which the library runs a flat step whose copy-out
     is a pass of its own, or which writes no replicas (the step kernel, then
-    the copy-out, range by range): one range up to 2^26 elements, else
-    ceil(n / 2^24) ranges starting on multiples of 2^20 elements."""
-    if n <= 1 << 26:
+    the copy-out, range by range): one range up to RANGE_SPLIT_MIN elements,
+    else ceil(n / RANGE_ELEMS) ranges starting on multiples of RANGE_ALIGN."""
+    if n <= RANGE_SPLIT_MIN:
         return [(0, n)]
-    K = (n + (1 << 24) - 1) >> 24
-    edges = [(n // K * i) >> 20 << 20 for i in range(K)] + [n]
+    K = (n + RANGE_ELEMS - 1) // RANGE_ELEMS
+    edges = [(n // K * i) // RANGE_ALIGN * RANGE_ALIGN for i in range(K)] + [n]
     return list(zip(edges[:-1], edges[1:]))
 
 

@@ -149,6 +149,21 @@ def test_library_ranges_cover_the_vector():
         assert all(r[i][1] == r[i + 1][0] for i in range(len(r) - 1))
 
 
+def test_range_rule_matches_the_library_source():
+    """bench.py's copy of the library's range constants equals the values in
+    the C++ source (kRangeSplitMin, kRangeElems, kRangeAlign)."""
+    import re
+    src = open(os.path.join(ROOT, "paper_1906_05936_amd", "csrc", "lsgd_flat.hip")).read()
+
+    def const(name):
+        m = re.search(r"constexpr int64_t %s = int64_t\{1\} << (\d+);" % name, src)
+        assert m, name
+        return 1 << int(m.group(1))
+    assert const("kRangeSplitMin") == bench.RANGE_SPLIT_MIN
+    assert const("kRangeElems") == bench.RANGE_ELEMS
+    assert const("kRangeAlign") == bench.RANGE_ALIGN
+
+
 def test_derive_traffic_counts_every_range_launch(tmp_path, monkeypatch):
     """A step run in element ranges (the 3.5e8-element workload: 21 launches of
     each kernel per step): the per-dispatch counters are scaled to the step."""
