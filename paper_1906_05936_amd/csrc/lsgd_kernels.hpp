@@ -372,15 +372,14 @@ __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
 
 // Member gradient loads a lane holds in one register batch of the segmented
-// sum: 8 for binary32 gradients, 4 for bfloat16. The consume code is unrolled
-// over a batch, once per batch register set, and with it every group's
-// finishing code: at 8 loads the bfloat16 kernels took 78-156 KB of code
-// (binary32 64-129 KB, the compile-time kernels 11-36 KB), more than the
-// instruction cache that two CUs share. Halving the bfloat16 batch (42-80 KB)
-// measured on the ResNet-50 size, same process: 2x3 +9% (R = N) / +14%
-// (R = 0), 6x4 +6% / +10%, 3x32 +19% / +85%, 12x1 and 5x16 within 1%. For
-// binary32 the same change was mixed (12x1 +8%, 2x3 +1%, 12x8 -1% / -2%, 3x32
-// -2%), so it keeps 8.
+// sum: 8 for binary32 gradients, 4 for bfloat16. Halving the bfloat16 batch
+// cut its kernels from 186-256 VGPRs to 154-234 (3 waves per SIMD instead of
+// 2 for counts up to 7) and their code by half; measured on the ResNet-50
+// size, same process: 2x3 +9% (R = N) / +14% (R = 0), 6x4 +6% / +10%, 3x32
+// +19% / +85%, 12x1 and 5x16 within 1%. The instruction cache was not the
+// limit (0.01% misses with either batch, as for the compile-time kernels).
+// For binary32 the same change was mixed (12x1 +8%, 2x3 +1%, 12x8 -1% / -2%,
+// 3x32 -2%), so it keeps 8.
 template <typename GT>
 constexpr int seg_batch() { return sizeof(GT) == 2 ? 4 : 8; }
 
