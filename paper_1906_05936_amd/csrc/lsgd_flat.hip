@@ -325,12 +325,17 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     if (literal)
         for (int32_t j = 0; j < n_groups; ++j)
             if (gstart[j + 1] - gstart[j] != gstart[1] - gstart[0]) W = 0;
+    int32_t G = n_groups;
+    if (one_group_form(W, G, literal)) {
+        W = n_workers;
+        G = 1;
+    }
     a.p = params;
     a.m = momentum;
     a.n = n;
     a.h = Hyper{lr, momentum_coef, weight_decay};
     a.n_workers = n_workers;
-    a.n_groups = n_groups;
+    a.n_groups = G;
     a.W = W;
     a.n_replicas = n_replicas;
     a.rdt = static_cast<int32_t>(rdt);
@@ -342,12 +347,12 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     FlatPick k{nullptr, 1};
     const bool cached = use_cached_state(n_workers, n);
     if (W > 0)
-        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(W, n_groups, cached) : pick_flat<float>(W, n_groups, cached);
+        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(W, G, cached) : pick_flat<float>(W, G, cached);
     const bool segmented = !k.kernel;
     if (segmented) {
         // runtime layout: group j is members [start[j], start[j+1]) of the member order
-        int32_t max_count = n_groups;
-        for (int32_t j = 0; j <= n_groups; ++j) {
+        int32_t max_count = G;
+        for (int32_t j = 0; j <= G; ++j) {
             const int32_t b = literal ? gstart[j] : j * W;
             a.group_start[j] = static_cast<uint8_t>(b);
             if (j > 0) max_count = std::max(max_count, b - static_cast<int32_t>(a.group_start[j - 1]));

@@ -350,8 +350,16 @@ lsgd_status lars_step(const lsgd_plan* plan, float lr, float momentum_coef, floa
     la.trust_coef = trust_coef;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->n_buckets > 0) {
-        const LarsKernel k1 = plan->gdt == LSGD_BF16 ? pick_lars<uint16_t>(plan->W, plan->n_groups)
-                                                     : pick_lars<float>(plan->W, plan->n_groups);
+        int32_t W = plan->W, G = plan->n_groups;
+        if (one_group_form(W, G, false)) {
+            W = plan->n_workers;
+            G = 1;
+            la.pa.W = W;
+            la.pa.n_groups = 1;
+            la.pa.group_start[0] = 0;
+            la.pa.group_start[1] = static_cast<uint8_t>(W);
+        }
+        const LarsKernel k1 = plan->gdt == LSGD_BF16 ? pick_lars<uint16_t>(W, G) : pick_lars<float>(W, G);
         hipLaunchKernelGGL(k1, dim3(ls.blocks), dim3(kBlock), 0, s, la);
         if ((st = check_launch("lsgd_lars_step_plan (norms)")) != LSGD_OK) return st;
     }
@@ -569,9 +577,18 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     // either reduction; the segmented kernel otherwise
     PlanKernel k = nullptr;
     bool segmented = true;
-    if (plan->W > 0) {
-        const PlanPick pk = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(plan->W, plan->n_groups, cached)
-                                                   : pick_plan<float>(plan->W, plan->n_groups, cached);
+    int32_t W = plan->W, G = plan->n_groups;
+    if (one_group_form(W, G, literal)) {
+        W = plan->n_workers;
+        G = 1;
+        a.W = W;
+        a.n_groups = 1;
+        a.group_start[0] = 0;
+        a.group_start[1] = static_cast<uint8_t>(W);
+    }
+    if (W > 0) {
+        const PlanPick pk = plan->gdt == LSGD_BF16 ? pick_plan<uint16_t>(W, G, cached)
+                                                   : pick_plan<float>(W, G, cached);
         k = pk.kernel;
         segmented = pk.segmented;
     } else {

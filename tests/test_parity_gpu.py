@@ -135,6 +135,12 @@ STEP_CASES = [
     (1, 9, "f32", 6_007, 3, "f32", "contiguous"),
     (20, 3, "f32", 7_001, 2, "f32", "shuffled"),
     (3, 20, "bf16", 5_003, 1, "bf16", "shuffled"),
+    # one worker per group in a non-power-of-two count: run as one group of
+    # all N workers in the member order (shuffled: that order is not the
+    # workers' ids)
+    (12, 1, "f32", 33_333, 3, "f32", "shuffled"),
+    (6, 1, "bf16", 20_005, 2, "bf16", "shuffled"),
+    (12, 1, "f32", 2_000_003, 12, "f32", "shuffled"),
 ]
 
 
@@ -268,7 +274,7 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
                                            (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32"),
                                            (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16"),
                                            (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
-                                           (16, 4, "f32", 2, "f32")])
+                                           (16, 4, "f32", 2, "f32"), (6, 1, "f32", 2, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
