@@ -14,7 +14,11 @@ timed region (HIP events on the stream the kernel runs on). The roofline peak
 is MI355X's published 8 TB/s. `cpu_baseline` times the CPU oracle on a bounded
 sample of the same workload on this host (one thread).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+Timing: the step runs untimed for --settle seconds (0.5), then W warmup steps,
+then five timed loops of exactly K steps, each bracketed by a device
+synchronize; ms_per_step is their median.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--settle S] [--workload NAME]
                        [--replicas R] [--no-cpu-baseline]
        python bench.py --derive-traffic --fetch-csv F --write-csv W [--workload NAME]
 """
@@ -41,6 +45,8 @@ def parse_args(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle", type=float, default=0.5, metavar="SECONDS",
+                    help="untimed steps for this long before the first timed loop (0: none)")
     ap.add_argument("--workload", default="resnet50_flat")
     ap.add_argument("--grouping", default=None, metavar="GxW",
                     help="override the workload's grouping with G equal groups of W workers")
@@ -302,6 +308,29 @@ def time_steps(setup, steps, warmup, fn=None, repeats=REPEATS):
         torch.cuda.synchronize()
         out.append(t0.elapsed_time(t1) / steps)
     return out
+
+
+def settle(setup, seconds, fn=None):
+    """Runs the step back to back, untimed, for `seconds` of wall time (in
+    bursts of 10 steps with a synchronize after each), and returns the number
+    of steps run. After an idle period the GPU runs the first tens to hundreds
+    of steps slower (its clocks and power state ramp up: five 20-step loops
+    straight after start-up measured 0.562, 0.563, 0.563, 0.558 and 0.553 ms
+    at the ResNet-50 size, a 200-step loop 0.551), so the timed loops that
+    follow start from the steady state a training loop runs in."""
+    import time
+    import torch
+    fn = fn or setup.step
+    if seconds <= 0:
+        return 0
+    n, t_end = 0, time.perf_counter() + seconds
+    while True:
+        for _ in range(10):
+            fn()
+        n += 10
+        torch.cuda.synchronize()
+        if time.perf_counter() >= t_end:
+            return n
 
 
 def median(xs):
@@ -958,6 +987,7 @@ def main(argv=None):
                             "separate": lsgd.COPY_OUT_SEPARATE}[args.copy_out])
     if args.path == "unfused":
         setup = UnfusedSetup(wl, R, dev)
+        settled = settle(setup, args.settle)
         reps_ms = time_steps(setup, args.steps, args.warmup)
         ms = median(reps_ms)
         per_call = setup.time_calls(args.steps, args.warmup)
@@ -971,6 +1001,7 @@ def main(argv=None):
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
             "data": "synthetic",
             "repeats_ms_per_step": [round(x, 6) for x in reps_ms],
+            "settle": {"seconds": args.settle, "steps": settled},
             "config": {"workload": wl.name, "path": "unfused", "n": wl.n, "groups": wl.groups,
                        "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                        "replicas": R},
@@ -1007,6 +1038,7 @@ def main(argv=None):
     setup = Setup(wl, R, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
                   args.tensor_layout, args.copy_out, args.lr_schedule)
     replay = captured(setup) if args.graph else None
+    settled = settle(setup, args.settle, replay)
     kernels = []
     if setup.parts and not args.graph:   # two kernels per step: the step again, an event between its kernels
         # measured first: the GPU runs the first tens of steps of a process
@@ -1033,6 +1065,7 @@ def main(argv=None):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "repeats_ms_per_step": [round(x, 6) for x in reps_ms],
+        "settle": {"seconds": args.settle, "steps": settled},
         "config": {"workload": wl.name, "n": wl.n, "groups": wl.groups,
                    "workers_per_group": wl.workers_per_group, "grad_dtype": wl.grad_dtype,
                    "replicas": R, "replica_dtype": wl.replica_dtype,
@@ -1085,7 +1118,9 @@ def main(argv=None):
         torch.cuda.empty_cache()
         setup = Setup(wl, 0, dev, args.reduction, args.broadcast_grad, args.lars, args.trust_coef, lars_excl,
                       args.tensor_layout, args.copy_out, args.lr_schedule)
-        ms0 = median(time_steps(setup, args.steps, args.warmup, captured(setup) if args.graph else None))
+        replay0 = captured(setup) if args.graph else None
+        settle(setup, args.settle, replay0)
+        ms0 = median(time_steps(setup, args.steps, args.warmup, replay0))
         alg0 = wl.algorithmic_bytes(0) + extra_bytes()
         result["r0"] = {"replicas": 0, "ms_per_step": round(ms0, 6),
                         "GBps": round(alg0 / (ms0 * 1e-3) / 1e9, 2), "steps_per_s": round(1e3 / ms0, 2),

@@ -34,6 +34,8 @@ def check_common(b):
     assert abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-3
     reps = b["repeats_ms_per_step"]     # five timed loops of K steps; the line reports their median
     assert len(reps) == 5 and abs(b["ms_per_step"] - sorted(reps)[2]) < 1e-6
+    st = b["settle"]                    # untimed steps before the first timed loop
+    assert st["seconds"] >= 0 and st["steps"] >= (10 if st["seconds"] > 0 else 0)
 
 
 def test_bench_default_line():
