@@ -221,7 +221,8 @@ def test_fixed_point_on_gpu():
                                              (1, 1, "bf16", 5, 1, "f32"),
                                              (12, 8, "f32", 9_001, 1, "f32"),
                                              (2, 12, "bf16", 3_001, 0, "f32"),
-                                             (20, 3, "f32", 4_003, 0, "f32")])
+                                             (20, 3, "f32", 4_003, 0, "f32"),
+                                             (6, 1, "f32", 4_001, 1, "f32")])
 def test_unfused_calls_match_oracle_and_fused(G, W, gdt, n, R, rdt):
     log("unfused G=%d W=%d %s n=%d" % (G, W, gdt, n))
     rng = np.random.default_rng(n)
@@ -730,6 +731,7 @@ LITERAL_CASES = [
     ("shuffled4x4", 4, "f32", 65_541, 0, True),
     ([0] * 5 + [1], 2, "f32", 7, 1, True),
     (list(range(7)), 7, "f32", 3_001, 0, False),
+    ([3, 0, 6, 1, 5, 2, 4], 7, "f32", 3_001, 1, False),   # one worker per group, shuffled: divides per group
     ([0, 0, 0, 1, 1, 2] * 20, 3, "f32", 4_099, 3, True),
     # equal power-of-two groups: the compile-time kernels, on XCD-renumbered
     # grids, with the replicas and the broadcast in copy passes of their own
