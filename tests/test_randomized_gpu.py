@@ -3,6 +3,7 @@
 replica dtypes, replica count, copy-out mode, flat vector or plan (a random
 split into tensors), and the LARS step where it applies. Every case is
 checked against the oracle bit for bit; each draw is logged before it runs."""
+import os
 import sys
 
 import numpy as np
@@ -20,7 +21,9 @@ else:  # collected but skipped on machines without a GPU
     lsgd = None
 
 DEV = torch.device("cuda:0")
-N_CASES = 96
+# cases drawn; LSGD_RANDOM_CASES raises it for longer runs (the first 96 are
+# always the same draws)
+N_CASES = int(os.environ.get("LSGD_RANDOM_CASES", "96"))
 
 
 def log(msg):
@@ -45,7 +48,7 @@ def draw(k):
     rng = np.random.default_rng(workloads.stream_seed(77, k))
     equal = rng.random() < 0.6
     if equal:
-        G = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+        G = int(rng.choice([1, 2, 3, 4, 5, 6, 8, 12, 16]))
         W = int(rng.choice([1, 2, 3, 4, 6, 8]))
         while G * W > 128:
             W = max(1, W // 2)
