@@ -819,7 +819,7 @@ def library_ranges(n):
 def kernel_match(wl, reduction=None, lars=False):
     pow2 = (1, 2, 4, 8, 16, 32, 64, 128)
     G, W = wl.groups, wl.workers_per_group
-    ct = (not wl.group_sizes and G in pow2 and W in pow2 and G * W <= 128
+    ct = (not wl.group_sizes and G in pow2 and (W in pow2 or W in (3, 5, 6, 7)) and G * W <= 128
           and (W <= 16 and G <= 16 or W <= 4 or G <= 4))
     if lars:
         return "lars_norms_kernel" if ct else "lars_norms_seg"

@@ -19,10 +19,11 @@ struct FlatPick {
     int tile;
 };
 
-// Compile-time (W, G) kernels for power-of-two counts with N = W*G <= 128
-// (groups of up to 16 workers, or 32 to 128 workers in up to 4 groups, or 32
-// to 128 groups of up to 4 workers); every other grouping takes the segmented
-// runtime-layout kernel. Both give the same bits.
+// Compile-time (W, G) kernels for power-of-two group counts G with N = W*G
+// <= 128: groups of up to 16 workers (W a power of two, or 3, 5, 6 or 7), or
+// 32 to 128 workers in up to 4 groups, or 32 to 128 groups of up to 4
+// workers; every other grouping takes the segmented runtime-layout kernel.
+// Both give the same bits.
 // The compile-time kernel for (W, G), with parameters and momentum through
 // the caches when `cached` (instantiated only where cached_state_for holds).
 template <typename GT, int W, int G>
@@ -77,7 +78,11 @@ FlatPick pick_flat(int W, int G, bool cached) {
     switch (W) {
         case 1: k = pick_flat_g<GT, 1>(G, cached); break;
         case 2: k = pick_flat_g<GT, 2>(G, cached); break;
+        case 3: k = pick_flat_g<GT, 3>(G, cached); break;
         case 4: k = pick_flat_g<GT, 4>(G, cached); break;
+        case 5: k = pick_flat_g<GT, 5>(G, cached); break;
+        case 6: k = pick_flat_g<GT, 6>(G, cached); break;
+        case 7: k = pick_flat_g<GT, 7>(G, cached); break;
         case 8: k = pick_flat_g<GT, 8>(G, cached); break;
         case 16: k = pick_flat_g<GT, 16>(G, cached); break;
         case 32: k = pick_flat_big_w<GT, 32>(G, cached); break;

@@ -368,6 +368,9 @@ struct PwAcc {
 
 __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
+// Largest power of two <= x (x >= 1).
+__host__ __device__ constexpr int pow2_floor(int x) { return x <= 1 ? 1 : 2 * pow2_floor(x / 2); }
+
 // Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
 
@@ -550,14 +553,14 @@ constexpr int kStreamFloats = 128;
 // With 32 or more groups the pairwise accumulator over groups holds
 // log2(G) + 1 partial sums of the tile, and four-unit tiles spilled to
 // scratch (2.3 KB per lane at 4x32 and 2x32): those kernels take two units.
-// So does the flat 16x4 kernel (16 groups of 4 workers), which spilled 2.3 KB
-// per lane with four units; with two (158 VGPRs, no scratch) the ResNet-50-
-// sized step ran 49% faster with 64 replicas, 87% without, the plan step 5%
-// and the LARS step 11% faster.
+// So do 16 groups of 4 (and of 3), whose four-unit kernels spilled 2.3 KB
+// per lane; with two (158 VGPRs, no scratch) the ResNet-50-sized 16x4 step
+// ran 49% faster with 64 replicas, 87% without, the plan step 5% and the
+// LARS step 11% faster.
 template <typename GT>
 constexpr int tile_units(int n_workers, int n_groups = 1) {
     return sizeof(GT) == 4 ? (n_workers * 2 * Unit<GT>::VEC <= kUnrollFloats || n_groups >= 32 ||
-                                      (n_groups == 16 && n_workers == 64)
+                                      (n_groups == 16 && (n_workers == 48 || n_workers == 64))
                                   ? 2
                                   : 4)
                            : 1;
@@ -573,8 +576,12 @@ __device__ __forceinline__ void pw_leaves(const Leaf& leaf, float (&out)[T]) {
     if constexpr (K * LW <= kUnrollFloats) {
         pw_tree<0, K, T>(leaf, out);
     } else {
+        // batches of a power of two of leaves (K is one), so that they cover
+        // the K leaves exactly: a batch of kStreamFloats / LW leaves that does
+        // not divide K would call leaf() past K
         constexpr int B0 = kStreamFloats / LW;
-        constexpr int B = B0 < 1 ? 1 : (B0 > K ? K : B0);
+        constexpr int B = pow2_floor(B0 < 1 ? 1 : (B0 > K ? K : B0));
+        static_assert((K & (K - 1)) == 0 && K % B == 0, "leaf batches cover the K leaves exactly");
         PwAcc<T, ilog2(K) + 1> acc;
 #pragma unroll 1
         for (int j0 = 0; j0 < K; j0 += B) {
@@ -716,7 +723,12 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
     const bool lit = s.literal() != 0;
-    const float group_scale = lit ? 1.0f / static_cast<float>(W * G) : 1.0f / static_cast<float>(W);
+    // G is a power of two; so is W in most kernels, and then the divisions are
+    // exact multiplications by 1/W (or 1/N); for W = 3, 5, 6 or 7 they are
+    // divisions
+    constexpr bool kPow2W = (W & (W - 1)) == 0;
+    const float group_div = lit ? static_cast<float>(W * G) : static_cast<float>(W);
+    const float group_scale = 1.0f / group_div;
     const float total_scale = lit ? 1.0f : 1.0f / static_cast<float>(G);
     auto group_leaf = [&](int j, float (&gm)[T]) {
         auto member_leaf = [&](int k, float (&x)[T]) {
@@ -728,7 +740,7 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
         if constexpr (W <= 16) pw_tree<0, W, T>(member_leaf, sum);
         else pw_leaves<W, T, T>(member_leaf, sum);   // larger groups: members streamed through an accumulator
 #pragma unroll
-        for (int v = 0; v < T; ++v) gm[v] = sum[v] * group_scale;
+        for (int v = 0; v < T; ++v) gm[v] = kPow2W ? sum[v] * group_scale : sum[v] / group_div;
     };
     float tot[T];
     pw_leaves<G, T, W * T>(group_leaf, tot);

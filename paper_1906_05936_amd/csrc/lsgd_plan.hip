@@ -132,7 +132,11 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
     switch (W) {
         case 1: k = pick_plan_g<GT, 1>(G, cached); break;
         case 2: k = pick_plan_g<GT, 2>(G, cached); break;
+        case 3: k = pick_plan_g<GT, 3>(G, cached); break;
         case 4: k = pick_plan_g<GT, 4>(G, cached); break;
+        case 5: k = pick_plan_g<GT, 5>(G, cached); break;
+        case 6: k = pick_plan_g<GT, 6>(G, cached); break;
+        case 7: k = pick_plan_g<GT, 7>(G, cached); break;
         case 8: k = pick_plan_g<GT, 8>(G, cached); break;
         case 16: k = pick_plan_g<GT, 16>(G, cached); break;
         case 32: k = pick_plan_big_w<GT, 32>(G, cached); break;
@@ -240,7 +244,11 @@ LarsKernel pick_lars(int W, int G) {
     switch (W) {
         case 1: k = pick_lars_g<GT, 1>(G); break;
         case 2: k = pick_lars_g<GT, 2>(G); break;
+        case 3: k = pick_lars_g<GT, 3>(G); break;
         case 4: k = pick_lars_g<GT, 4>(G); break;
+        case 5: k = pick_lars_g<GT, 5>(G); break;
+        case 6: k = pick_lars_g<GT, 6>(G); break;
+        case 7: k = pick_lars_g<GT, 7>(G); break;
         case 8: k = pick_lars_g<GT, 8>(G); break;
         case 16: k = pick_lars_g<GT, 16>(G); break;
         case 32: k = pick_lars_big_w<GT, 32>(G); break;

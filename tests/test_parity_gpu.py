@@ -141,6 +141,18 @@ STEP_CASES = [
     (12, 1, "f32", 33_333, 3, "f32", "shuffled"),
     (6, 1, "bf16", 20_005, 2, "bf16", "shuffled"),
     (12, 1, "f32", 2_000_003, 12, "f32", "shuffled"),
+    # compile-time kernels for groups of 3, 5, 6 or 7 in a power-of-two count
+    # (the group mean a true division); 16 and 32 groups of 3 stream their
+    # groups in power-of-two batches
+    (8, 3, "f32", 100_003, 24, "f32", "shuffled"),
+    (16, 3, "f32", 2_000_003, 4, "f32", "shuffled"),
+    (32, 3, "f32", 10_007, 2, "f32", "shuffled"),
+    (8, 3, "bf16", 50_001, 3, "bf16", "shuffled"),
+    (4, 5, "bf16", 40_009, 2, "bf16", "shuffled"),
+    (8, 5, "bf16", 9_001, 0, "f32", "shuffled"),
+    (2, 7, "f32", 30_011, 14, "f32", "contiguous"),
+    (4, 7, "bf16", 7_003, 1, "f32", "contiguous"),
+    (16, 6, "f32", 20_003, 1, "f32", "shuffled"),
 ]
 
 
@@ -275,7 +287,8 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
                                            (16, 8, "f32", 2, "f32"), (5, 3, "bf16", 0, "f32"),
                                            (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16"),
                                            (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
-                                           (16, 4, "f32", 2, "f32"), (6, 1, "f32", 2, "f32")])
+                                           (16, 4, "f32", 2, "f32"), (6, 1, "f32", 2, "f32"),
+                                           (8, 3, "bf16", 1, "f32"), (4, 6, "f32", 2, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
@@ -740,6 +753,9 @@ LITERAL_CASES = [
     ("shuffled4x4", 4, "f32", 33_333, 2, True),
     ("contiguous8x8", 8, "bf16", 100_003, 2, False),
     ("contiguous2x2", 2, "f32", 1_000_001, 1, True),
+    # equal groups of 3 in a power-of-two count: the compile-time kernel, each
+    # group's sum divided by N = 24
+    (workloads.shuffled_groups(8, 3, 5), 8, "f32", 40_003, 3, True),
 ]
 
 
