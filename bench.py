@@ -783,8 +783,12 @@ def separate_copy_out(wl, R, mode="auto", bcast=False):
     if mode == "separate":
         return True
     cached = wl.n_workers <= 16 and 8 * wl.n <= (288 << 20)   # parameters and momentum through the caches
-    segmented = kernel_match(wl).endswith("_seg")             # runtime group layouts
-    crossing = (48 if segmented else 64) if cached else 32
+    G, W = wl.groups, wl.workers_per_group
+    if W == 1 and G & (G - 1) and not ct_grouping(1, G) and not wl.group_sizes:
+        G, W = 1, wl.n_workers                                  # run as one group of all workers
+    pow2_grouping = (not kernel_match(wl).endswith("_seg") and not wl.group_sizes
+                     and W & (W - 1) == 0 and G & (G - 1) == 0)
+    crossing = (64 if pow2_grouping else 48) if cached else 32
     return copy_bytes >= crossing or wl.n_workers * wl.grad_bytes >= 256
 
 
@@ -816,11 +820,21 @@ def library_ranges(n):
     return list(zip(edges[:-1], edges[1:]))
 
 
-def kernel_match(wl, reduction=None, lars=False):
+def ct_grouping(W, G):
+    """Whether the library has a compile-time kernel for G groups of W."""
     pow2 = (1, 2, 4, 8, 16, 32, 64, 128)
+    if W * G > 128:
+        return False
+    if G in pow2:
+        return (W in pow2 or W in (3, 5, 6, 7)) and (W <= 16 and G <= 16 or W <= 4 or G <= 4)
+    return G in (3, 5, 6, 7, 12) and (W <= 8 or W == 16)
+
+
+def kernel_match(wl, reduction=None, lars=False):
     G, W = wl.groups, wl.workers_per_group
-    ct = (not wl.group_sizes and G in pow2 and (W in pow2 or W in (3, 5, 6, 7)) and G * W <= 128
-          and (W <= 16 and G <= 16 or W <= 4 or G <= 4))
+    ct = not wl.group_sizes and ct_grouping(W, G)
+    if (not ct and not wl.group_sizes and W == 1 and G & (G - 1) and reduction != "literal"):
+        ct = ct_grouping(G, 1)   # one worker per group: run as one group of all workers
     if lars:
         return "lars_norms_kernel" if ct else "lars_norms_seg"
     if wl.tensor_sizes:

@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblsgd.so")
-SOURCES = ["lsgd_common.hip", "lsgd_flat.hip", "lsgd_plan.hip", "lsgd_bench.hip", "lsgd_noalloc.hip"]
+SOURCES = ["lsgd_common.hip", "lsgd_flat.hip", "lsgd_flat_np2.hip", "lsgd_plan.hip", "lsgd_plan_np2.hip",
+           "lsgd_bench.hip", "lsgd_noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

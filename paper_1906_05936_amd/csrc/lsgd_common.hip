@@ -163,17 +163,20 @@ int32_t launch_passes_per_block() { return g_units_per_lane.load(std::memory_ord
 // (use_cached_state) the fused pass gains more, and the crossing moves to 64
 // bytes: at 32 the fused pass won by 2-4% (4x4 R = 8, 2x2 R = 8, 4x4
 // bfloat16 R = 16), at 64 the separate one by 3-12% (4x4 R = 16, 2x2 R = 16,
-// the ResNet-50 plan), at 256 by 28%. The segmented kernels (runtime group
-// layouts) cross earlier there: the separate pass won by 5-8% at 56 and 60
-// replica bytes (2x7, 3x5, 5x3 binary32) and lost by 3-8% at 24 and 36 (2x3,
-// 3x2, 1x9), so their crossing is 48 bytes.
-bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool segmented) {
+// the ResNet-50 plan), at 256 by 28%. Groupings other than power-of-two
+// groups in a power-of-two count cross earlier there: with the segmented
+// kernels the separate pass won by 5-8% at 56 and 60 replica bytes (2x7,
+// 3x5, 5x3 binary32) and lost by 3-8% at 24 and 36 (2x3, 3x2, 1x9); with
+// their compile-time kernels the fused form lost 4% at 3x5 and 11% at 3x5
+// with bfloat16 gradients (60 bytes) and 13% at 12x1 bfloat16 (48 bytes).
+// Their crossing is 48 bytes (`other_layout`).
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool other_layout) {
     if (copy_bytes <= 0) return false;
     const int32_t mode = g_copy_out_mode.load(std::memory_order_relaxed);
     if (mode == LSGD_COPY_OUT_FUSED) return false;
     if (mode == LSGD_COPY_OUT_SEPARATE) return true;
     const int64_t grad_bytes = static_cast<int64_t>(n_workers) * static_cast<int64_t>(gsz);
-    const int64_t crossing = !use_cached_state(n_workers, n) ? 32 : segmented ? 48 : 64;
+    const int64_t crossing = !use_cached_state(n_workers, n) ? 32 : other_layout ? 48 : 64;
     return copy_bytes >= crossing || grad_bytes >= 256;
 }
 

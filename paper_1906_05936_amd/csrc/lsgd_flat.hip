@@ -6,6 +6,7 @@
 
 #include "lsgd_host.hpp"
 #include "lsgd_kernels.hpp"
+#include "lsgd_np2.hpp"
 #include "lsgd_schedule.hpp"
 
 namespace lsgd {
@@ -330,10 +331,24 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     if (literal)
         for (int32_t j = 0; j < n_groups; ++j)
             if (gstart[j + 1] - gstart[j] != gstart[1] - gstart[0]) W = 0;
+    const bool cached = use_cached_state(n_workers, n);
+    // a compile-time kernel for (W, G): power-of-two group counts, then 3, 5,
+    // 6, 7 and 12 (lsgd_np2.hpp)
+    auto pick_ct = [&](int32_t w, int32_t g) {
+        FlatPick p = gdt == LSGD_BF16 ? pick_flat<uint16_t>(w, g, cached) : pick_flat<float>(w, g, cached);
+        if (!p.kernel && np2_group_count(g)) {
+            const Np2FlatPick q = pick_flat_np2(w, g, cached, gdt == LSGD_BF16);
+            p = FlatPick{q.kernel, q.tile};
+        }
+        return p;
+    };
     int32_t G = n_groups;
-    if (one_group_form(W, G, literal)) {
+    FlatPick k{nullptr, 1};
+    if (W > 0) k = pick_ct(W, G);
+    if (!k.kernel && one_group_form(W, G, literal)) {
         W = n_workers;
         G = 1;
+        k = pick_ct(W, G);
     }
     a.p = params;
     a.m = momentum;
@@ -349,11 +364,8 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     for (int32_t r = 0; r < n_replicas; ++r) a.replicas[r] = replicas[r];
 
     const int64_t vec = gdt == LSGD_BF16 ? Unit<uint16_t>::VEC : Unit<float>::VEC;
-    FlatPick k{nullptr, 1};
-    const bool cached = use_cached_state(n_workers, n);
-    if (W > 0)
-        k = gdt == LSGD_BF16 ? pick_flat<uint16_t>(W, G, cached) : pick_flat<float>(W, G, cached);
     const bool segmented = !k.kernel;
+    const bool pow2_grouping = !segmented && (W & (W - 1)) == 0 && (G & (G - 1)) == 0;
     if (segmented) {
         // runtime layout: group j is members [start[j], start[j+1]) of the member order
         int32_t max_count = G;
@@ -371,7 +383,7 @@ LSGD_API lsgd_status lsgd_step_ex(float* params, float* momentum, void* const* g
     const int32_t bcast_copies = bcast ? n_workers - 1 : 0;
     const bool split = separate_copy_out_bytes(
         n_workers, dtype_size(gdt), static_cast<int64_t>(n_replicas) * dtype_size(rdt) + 4 * bcast_copies, n,
-        segmented);
+        !pow2_grouping);
     a.bcast_grad = bcast ? (split ? 1 : n_workers) : 0;
     // split: the step kernel writes the first k replicas, the copy-out pass the rest
     const int32_t k_step = split ? replicas_in_step(n_workers, n_replicas, dtype_size(rdt), n) : n_replicas;

@@ -71,11 +71,11 @@ int32_t launch_passes_per_block();
 // Whether a step with N gradients of gsz bytes, n elements and `copy_bytes`
 // bytes per element of copies (replicas, and the gradient broadcast's copies
 // of the mean gradient to the other members) writes them in copy passes of
-// their own (lsgd_set_copy_out_mode); `segmented`: the step runs a
-// runtime-layout (segmented) kernel.
-bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool segmented);
+// their own (lsgd_set_copy_out_mode); `other_layout`: the step's grouping is
+// not power-of-two groups in a power-of-two count.
+bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, int64_t n, bool other_layout);
 // One worker per group, in a group count with no compile-time kernel (not a
-// power of two), under the mean of means: the result equals that of one group
+// power of two, nor 3, 5, 6, 7 or 12), under the mean of means: the result equals that of one group
 // of all N workers in the same member order (the same pairwise sum over the
 // same sequence of values, then one division by N = G; the group means are
 // the members themselves), which the segmented kernels compute with one
@@ -83,8 +83,12 @@ bool separate_copy_out_bytes(int32_t n_workers, size_t gsz, int64_t copy_bytes, 
 // that form (W = N, G = 1). Measured on the ResNet-50 size, same process:
 // 12x1 binary32 62% -> 82% of 8 TB/s (R = N) and 51% -> 80% (R = 0), 6x1
 // 79% -> 88%, 12x1 bfloat16 50% -> 76% and 34% -> 66%.
+// Group counts other than powers of two that have compile-time kernels too
+// (lsgd_np2.hpp).
+inline bool np2_group_count(int G) { return G == 3 || G == 5 || G == 6 || G == 7 || G == 12; }
+
 inline bool one_group_form(int32_t W, int32_t G, bool literal) {
-    return !literal && W == 1 && G > 1 && (G & (G - 1)) != 0;
+    return !literal && W == 1 && G > 1 && (G & (G - 1)) != 0 && !np2_group_count(G);
 }
 // With the separate copy-out: how many of the n_replicas replicas (rsz bytes
 // each) the step kernel still writes itself; the copy-out pass writes the

@@ -368,8 +368,11 @@ struct PwAcc {
 
 __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
-// Largest power of two <= x (x >= 1).
-__host__ __device__ constexpr int pow2_floor(int x) { return x <= 1 ? 1 : 2 * pow2_floor(x / 2); }
+// Largest divisor of k that is <= b (k, b >= 1); for a power of two k, the
+// largest power of two <= b.
+__host__ __device__ constexpr int largest_divisor_le(int k, int b) {
+    return b <= 1 ? 1 : (k % b == 0 ? b : largest_divisor_le(k, b - 1));
+}
 
 // Levels a PwAcc needs for `cnt` pushes (uniform runtime value).
 __device__ __forceinline__ int acc_levels(int cnt) { return 32 - __builtin_clz(static_cast<unsigned>(cnt)); }
@@ -566,22 +569,22 @@ constexpr int tile_units(int n_workers, int n_groups = 1) {
                            : 1;
 }
 
-// Pairwise sum of K leaves (compile-time K, a power of two) of T floats each:
-// unrolled while K * LW floats (LW = floats a leaf loads) stay within
-// kUnrollFloats, so that every load is issued up front; otherwise streamed in
-// batches of about kStreamFloats through a compile-time-sized pairwise
-// accumulator. Both give PW over the K leaves in order.
+// Pairwise sum of K leaves (compile-time K) of T floats each: unrolled while
+// K * LW floats (LW = floats a leaf loads) stay within kUnrollFloats, so that
+// every load is issued up front; otherwise streamed in batches of about
+// kStreamFloats through a compile-time-sized pairwise accumulator. Both give
+// PW over the K leaves in order.
 template <int K, int T, int LW, typename Leaf>
 __device__ __forceinline__ void pw_leaves(const Leaf& leaf, float (&out)[T]) {
     if constexpr (K * LW <= kUnrollFloats) {
         pw_tree<0, K, T>(leaf, out);
     } else {
-        // batches of a power of two of leaves (K is one), so that they cover
-        // the K leaves exactly: a batch of kStreamFloats / LW leaves that does
-        // not divide K would call leaf() past K
+        // batches of a divisor of K leaves (a power of two where K is one), so
+        // that they cover the K leaves exactly: a batch of kStreamFloats / LW
+        // leaves that does not divide K would call leaf() past K
         constexpr int B0 = kStreamFloats / LW;
-        constexpr int B = pow2_floor(B0 < 1 ? 1 : (B0 > K ? K : B0));
-        static_assert((K & (K - 1)) == 0 && K % B == 0, "leaf batches cover the K leaves exactly");
+        constexpr int B = largest_divisor_le(K, B0 < 1 ? 1 : (B0 > K ? K : B0));
+        static_assert(K % B == 0, "leaf batches cover the K leaves exactly");
         PwAcc<T, ilog2(K) + 1> acc;
 #pragma unroll 1
         for (int j0 = 0; j0 < K; j0 += B) {
@@ -723,10 +726,12 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
     constexpr int VEC = Unit<GT>::VEC;
     constexpr int T = U * VEC;
     const bool lit = s.literal() != 0;
-    // G is a power of two; so is W in most kernels, and then the divisions are
-    // exact multiplications by 1/W (or 1/N); for W = 3, 5, 6 or 7 they are
-    // divisions
+    // Divisions by powers of two are the exact multiplications by 1/W, 1/N or
+    // 1/G; the others (W = 3, 5, 6 or 7; G = 3, 5, 6, 7 or 12; N of either)
+    // are divisions. The mean of means divides each group's sum by W and the
+    // total by G; the literal reduction each group's sum by N, the total by 1.
     constexpr bool kPow2W = (W & (W - 1)) == 0;
+    constexpr bool kPow2G = (G & (G - 1)) == 0;
     const float group_div = lit ? static_cast<float>(W * G) : static_cast<float>(W);
     const float group_scale = 1.0f / group_div;
     const float total_scale = lit ? 1.0f : 1.0f / static_cast<float>(G);
@@ -739,13 +744,32 @@ __device__ __forceinline__ void mean_tile_ct(const Src& s, const int64_t (&e0)[U
         float sum[T];
         if constexpr (W <= 16) pw_tree<0, W, T>(member_leaf, sum);
         else pw_leaves<W, T, T>(member_leaf, sum);   // larger groups: members streamed through an accumulator
+        if constexpr (kPow2W && kPow2G) {
 #pragma unroll
-        for (int v = 0; v < T; ++v) gm[v] = kPow2W ? sum[v] * group_scale : sum[v] / group_div;
+            for (int v = 0; v < T; ++v) gm[v] = sum[v] * group_scale;
+        } else if constexpr (!kPow2W) {
+#pragma unroll
+            for (int v = 0; v < T; ++v) gm[v] = sum[v] / group_div;
+        } else if (lit) {   // W a power of two, N not
+#pragma unroll
+            for (int v = 0; v < T; ++v) gm[v] = sum[v] / group_div;
+        } else {
+#pragma unroll
+            for (int v = 0; v < T; ++v) gm[v] = sum[v] * group_scale;
+        }
     };
     float tot[T];
     pw_leaves<G, T, W * T>(group_leaf, tot);
+    if constexpr (kPow2G) {
 #pragma unroll
-    for (int v = 0; v < T; ++v) gbar[v] = tot[v] * total_scale;
+        for (int v = 0; v < T; ++v) gbar[v] = tot[v] * total_scale;
+    } else if (lit) {
+#pragma unroll
+        for (int v = 0; v < T; ++v) gbar[v] = tot[v];
+    } else {
+#pragma unroll
+        for (int v = 0; v < T; ++v) gbar[v] = tot[v] / static_cast<float>(G);
+    }
 }
 
 template <typename GT, int W, int G, int U, bool TAIL, typename Src>

@@ -15,6 +15,7 @@
 #include <algorithm>
 
 #include "lsgd_host.hpp"
+#include "lsgd_np2.hpp"
 #include "lsgd_plan_kernels.hpp"
 
 struct lsgd_plan {
@@ -144,6 +145,10 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
         case 128: k = pick_plan_big_w<GT, 128>(G, cached); break;
     }
     if (k) return PlanPick{k, tile_units<GT>(W * G, G), false};
+    if (np2_group_count(G)) {   // group counts 3, 5, 6, 7 and 12 (lsgd_np2.hpp)
+        const Np2PlanPick q = pick_plan_np2(W, G, cached, sizeof(GT) == 2);
+        if (q.kernel) return PlanPick{q.kernel, q.tile, false};
+    }
     return PlanPick{plan_seg<GT>(W > G ? W : G, cached), SegTileUnits<GT>::U, true};
 }
 
@@ -256,6 +261,8 @@ LarsKernel pick_lars(int W, int G) {
         case 128: k = pick_lars_big_w<GT, 128>(G); break;
     }
     if (k) return k;
+    if (np2_group_count(G))
+        if (const Np2LarsKernel q = pick_lars_np2(W, G, sizeof(GT) == 2)) return q;
     switch (seg_levels(W > G ? W : G)) {
         case 3: return lars_norms_seg<GT, 3>;
         case 4: return lars_norms_seg<GT, 4>;
@@ -610,7 +617,7 @@ LSGD_API lsgd_status lsgd_step_plan_ex(const lsgd_plan* plan, float lr, float mo
     const bool split = separate_copy_out_bytes(
         plan->n_workers, plan->gdt == LSGD_BF16 ? 2 : 4,
         static_cast<int64_t>(plan->n_replicas) * (plan->rdt == LSGD_BF16 ? 2 : 4) + 4 * bcast_copies,
-        plan->total_elems, segmented);
+        plan->total_elems, segmented || (W & (W - 1)) != 0 || (G & (G - 1)) != 0);
     a.bcast_grad = bcast ? (split ? 1 : plan->n_workers) : 0;
     // split: the step kernel writes the first k replicas, the copy-out pass the rest
     const int32_t k_step = split ? replicas_in_step(plan->n_workers, plan->n_replicas, plan->rdt == LSGD_BF16 ? 2 : 4,

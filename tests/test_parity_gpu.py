@@ -153,6 +153,15 @@ STEP_CASES = [
     (2, 7, "f32", 30_011, 14, "f32", "contiguous"),
     (4, 7, "bf16", 7_003, 1, "f32", "contiguous"),
     (16, 6, "f32", 20_003, 1, "f32", "shuffled"),
+    # compile-time kernels for 3, 5, 6, 7 or 12 groups (the total a true
+    # division; 12 groups stream through the accumulator in batches of a
+    # divisor of 12)
+    (12, 4, "f32", 2_000_003, 12, "f32", "shuffled"),
+    (12, 8, "bf16", 30_001, 2, "bf16", "shuffled"),
+    (7, 16, "bf16", 9_999, 1, "f32", "shuffled"),
+    (5, 16, "f32", 8_011, 3, "f32", "contiguous"),
+    (6, 3, "f32", 60_013, 18, "f32", "shuffled"),
+    (12, 1, "bf16", 11_111, 2, "bf16", "shuffled"),
 ]
 
 
