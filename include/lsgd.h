@@ -141,9 +141,9 @@ LSGD_API lsgd_status lsgd_get_launch_shape(int32_t* xcd_chunk, int32_t* blocks_p
  * takes the separate pass where it measured faster: for the fused steps when
  * the replica bytes R*s_r per element are at least 32 (for at most 16
  * workers with parameters and momentum within 288 MB, whose step kernels
- * access them through the caches: 64 for power-of-two group counts with
- * groups of a power of two or of 3, 5, 6 or 7 workers, 48 for other group
- * layouts) or the gradient bytes N*s_g at least 256;
+ * access them through the caches: 64 for power-of-two groups in a
+ * power-of-two count, 48 for every other group layout) or the gradient bytes
+ * N*s_g at least 256;
  * for lsgd_sgd_step and the LARS update when R*s_r >= 16 (parameters and
  * momentum within 288 MB; beyond, binary32 replicas and R >= 4).
  * Process-wide, for launches after the call returns. Errors: LSGD_ERR_SIZE
@@ -228,16 +228,20 @@ LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* 
  * gradient stay in registers. The replicas are written either by that kernel
  * or, where lsgd_set_copy_out_mode's rule takes the separate form (the
  * default with up to 16 workers at 64 or more replica bytes per element for
- * the compile-time groupings (power-of-two group counts, groups of a power of
- * two or of 3, 5, 6 or 7), 48 for other group layouts), by a copy-out
+ * power-of-two groups in a power-of-two count, 48 for every other group
+ * layout), by a copy-out
  * pass launched right after it, which reads the new parameters once more
  * (the step kernel then still writes the first lsgd_set_step_replicas
  * replicas). Vectors longer than 2^26 elements are processed range by range
  * (about 2^24 elements each, edges on multiples of 2^20 elements: the step
  * kernel, then its copy-out pass) unless the step kernel writes every
- * replica itself. Arguments as for the three calls above. The results are
- * bit-identical to lsgd_group_mean, then lsgd_global_mean, then
- * lsgd_sgd_step, in every form.
+ * replica itself. Compile-time kernels (the pairwise trees unrolled) serve
+ * power-of-two group counts with groups of 1 to 16 workers (a power of two,
+ * or 3, 5, 6 or 7), 32 to 128 workers in up to 4 groups, 32 to 128 groups
+ * of up to 4 workers, and 3, 5, 6, 7 or 12 groups of 1 to 8 or 16 workers;
+ * every other grouping takes a runtime-layout kernel. Arguments as for the
+ * three calls above. The results are bit-identical to lsgd_group_mean, then
+ * lsgd_global_mean, then lsgd_sgd_step, in every form.
  */
 LSGD_API lsgd_status lsgd_step(float* params, float* momentum, const void* const* grads,
                                lsgd_dtype gdt, int32_t n_workers,
@@ -330,9 +334,9 @@ LSGD_API lsgd_status lsgd_lr_schedule_step(const lsgd_lr_schedule* schedule, int
  * launch. The plan copies a chunk table and a pointer table to device memory
  * once; lsgd_step_plan then launches one kernel. Tensors are cut into pieces
  * of 2048 elements (4096 for binary32 gradients with more than 16 workers in
- * a power-of-two count of groups of a power of two or of 3, 5, 6 or 7
- * workers, except 32 or more groups and 16 groups of 3 or 4; times the
- * launch shape's units_per_lane at creation);
+ * a grouping with a compile-time kernel, as listed for lsgd_step, except 32
+ * or more groups and 16 groups of 3 or 4; times the launch shape's
+ * units_per_lane at creation);
  * small tensors are bucketed so that one workgroup covers several of them.
  *   numel     [n_tensors] host int64, elements of each tensor (>= 0).
  *   params, momentum [n_tensors] device pointers (binary32).
