@@ -826,8 +826,8 @@ def ct_grouping(W, G):
     if W * G > 128:
         return False
     if G in pow2:
-        return (W in pow2 or W in (3, 5, 6, 7)) and (W <= 16 and G <= 16 or W <= 4 or G <= 4)
-    return G in (3, 5, 6, 7, 12) and (W <= 8 or W == 16)
+        return (W in pow2 or W in (3, 5, 6, 7, 12)) and (W <= 16 and G <= 16 or W <= 4 or G <= 4)
+    return G in (3, 5, 6, 7, 12) and (W <= 8 or W in (12, 16, 32))
 
 
 def kernel_match(wl, reduction=None, lars=False):

@@ -237,8 +237,9 @@ LSGD_API lsgd_status lsgd_copy_out(const float* params, int64_t n, void* const* 
  * kernel, then its copy-out pass) unless the step kernel writes every
  * replica itself. Compile-time kernels (the pairwise trees unrolled) serve
  * power-of-two group counts with groups of 1 to 16 workers (a power of two,
- * or 3, 5, 6 or 7), 32 to 128 workers in up to 4 groups, 32 to 128 groups
- * of up to 4 workers, and 3, 5, 6, 7 or 12 groups of 1 to 8 or 16 workers;
+ * or 3, 5, 6, 7 or 12), 32 to 128 workers in up to 4 groups, 32 to 128
+ * groups of up to 4 workers, and 3, 5, 6, 7 or 12 groups of 1 to 8, 12, 16
+ * or 32 workers (N at most 128);
  * every other grouping takes a runtime-layout kernel. Arguments as for the
  * three calls above. The results are bit-identical to lsgd_group_mean, then
  * lsgd_global_mean, then lsgd_sgd_step, in every form.

@@ -21,7 +21,7 @@ struct FlatPick {
 };
 
 // Compile-time (W, G) kernels for power-of-two group counts G with N = W*G
-// <= 128: groups of up to 16 workers (W a power of two, or 3, 5, 6 or 7), or
+// <= 128: groups of up to 16 workers (W a power of two, or 3, 5, 6, 7 or 12), or
 // 32 to 128 workers in up to 4 groups, or 32 to 128 groups of up to 4
 // workers; every other grouping takes the segmented runtime-layout kernel.
 // Both give the same bits.
@@ -85,6 +85,7 @@ FlatPick pick_flat(int W, int G, bool cached) {
         case 6: k = pick_flat_g<GT, 6>(G, cached); break;
         case 7: k = pick_flat_g<GT, 7>(G, cached); break;
         case 8: k = pick_flat_g<GT, 8>(G, cached); break;
+        case 12: k = pick_flat_g<GT, 12>(G, cached); break;
         case 16: k = pick_flat_g<GT, 16>(G, cached); break;
         case 32: k = pick_flat_big_w<GT, 32>(G, cached); break;
         case 64: k = pick_flat_big_w<GT, 64>(G, cached); break;

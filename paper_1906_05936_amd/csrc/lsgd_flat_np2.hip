@@ -27,8 +27,14 @@ FlatKernel np2_flat_w(int W, bool cached) {
         case 6: return np2_flat<GT, 6, G>(cached);
         case 7: return np2_flat<GT, 7, G>(cached);
         case 8: return np2_flat<GT, 8, G>(cached);
+        case 12:
+            if constexpr (12 * G <= kMaxWorkers) return np2_flat<GT, 12, G>(cached);
+            else return nullptr;
         case 16:
             if constexpr (16 * G <= kMaxWorkers) return np2_flat<GT, 16, G>(cached);
+            else return nullptr;
+        case 32:
+            if constexpr (32 * G <= kMaxWorkers) return np2_flat<GT, 32, G>(cached);
             else return nullptr;
     }
     return nullptr;

@@ -1,5 +1,5 @@
 // Compile-time (W, G) kernels for group counts G = 3, 5, 6, 7 and 12 (groups
-// of 1 to 8 or 16 workers, N = W*G <= 128): the same kernels as for
+// of 1 to 8, 12, 16 or 32 workers, N = W*G <= 128): the same kernels as for
 // power-of-two counts (the group tree unrolled or streamed through the
 // pairwise accumulator, the division by G a true division), instantiated in
 // translation units of their own so that they compile in parallel with the

@@ -139,6 +139,7 @@ PlanPick pick_plan(int W, int G, bool cached = false) {
         case 6: k = pick_plan_g<GT, 6>(G, cached); break;
         case 7: k = pick_plan_g<GT, 7>(G, cached); break;
         case 8: k = pick_plan_g<GT, 8>(G, cached); break;
+        case 12: k = pick_plan_g<GT, 12>(G, cached); break;
         case 16: k = pick_plan_g<GT, 16>(G, cached); break;
         case 32: k = pick_plan_big_w<GT, 32>(G, cached); break;
         case 64: k = pick_plan_big_w<GT, 64>(G, cached); break;
@@ -255,6 +256,7 @@ LarsKernel pick_lars(int W, int G) {
         case 6: k = pick_lars_g<GT, 6>(G); break;
         case 7: k = pick_lars_g<GT, 7>(G); break;
         case 8: k = pick_lars_g<GT, 8>(G); break;
+        case 12: k = pick_lars_g<GT, 12>(G); break;
         case 16: k = pick_lars_g<GT, 16>(G); break;
         case 32: k = pick_lars_big_w<GT, 32>(G); break;
         case 64: k = pick_lars_big_w<GT, 64>(G); break;

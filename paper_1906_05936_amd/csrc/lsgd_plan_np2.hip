@@ -28,8 +28,14 @@ PlanKernel np2_plan_w(int W, bool cached) {
         case 6: return np2_plan<GT, 6, G>(cached);
         case 7: return np2_plan<GT, 7, G>(cached);
         case 8: return np2_plan<GT, 8, G>(cached);
+        case 12:
+            if constexpr (12 * G <= kMaxWorkers) return np2_plan<GT, 12, G>(cached);
+            else return nullptr;
         case 16:
             if constexpr (16 * G <= kMaxWorkers) return np2_plan<GT, 16, G>(cached);
+            else return nullptr;
+        case 32:
+            if constexpr (32 * G <= kMaxWorkers) return np2_plan<GT, 32, G>(cached);
             else return nullptr;
     }
     return nullptr;
@@ -51,8 +57,14 @@ Np2LarsKernel np2_lars_w(int W) {
         case 6: return np2_lars<GT, 6, G>();
         case 7: return np2_lars<GT, 7, G>();
         case 8: return np2_lars<GT, 8, G>();
+        case 12:
+            if constexpr (12 * G <= kMaxWorkers) return np2_lars<GT, 12, G>();
+            else return nullptr;
         case 16:
             if constexpr (16 * G <= kMaxWorkers) return np2_lars<GT, 16, G>();
+            else return nullptr;
+        case 32:
+            if constexpr (32 * G <= kMaxWorkers) return np2_lars<GT, 32, G>();
             else return nullptr;
     }
     return nullptr;

@@ -154,7 +154,8 @@ class Case:
                                            (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
                                            (16, 4, "f32", 2, "f32"), (5, 1, "bf16", 1, "f32"),
                                            (4, 3, "f32", 1, "f32"), (2, 5, "bf16", 0, "f32"),
-                                           (6, 2, "f32", 1, "f32"), (12, 4, "bf16", 0, "f32")])
+                                           (6, 2, "f32", 1, "f32"), (12, 4, "bf16", 0, "f32"),
+                                           (4, 12, "bf16", 1, "f32"), (3, 32, "f32", 0, "f32")])
 def test_lars_plan_matches_oracle(G, W, gdt, R, rdt):
     log("lars plan G=%d W=%d %s R=%d %s" % (G, W, gdt, R, rdt))
     c = Case(G, W, gdt, R, rdt, seed=G * 10 + W)

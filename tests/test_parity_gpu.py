@@ -162,6 +162,16 @@ STEP_CASES = [
     (5, 16, "f32", 8_011, 3, "f32", "contiguous"),
     (6, 3, "f32", 60_013, 18, "f32", "shuffled"),
     (12, 1, "bf16", 11_111, 2, "bf16", "shuffled"),
+    # groups of 12 workers: compile-time kernels for power-of-two counts and
+    # for 3, 5, 6 and 7 groups
+    (4, 12, "f32", 100_003, 12, "f32", "shuffled"),
+    (8, 12, "bf16", 30_007, 2, "bf16", "shuffled"),
+    (3, 12, "f32", 20_011, 3, "f32", "shuffled"),
+    (7, 12, "bf16", 9_001, 0, "f32", "shuffled"),
+    (1, 12, "f32", 8_191, 1, "f32", "contiguous"),
+    # 3 groups of 32: members streamed through the accumulator, G a division
+    (3, 32, "f32", 20_011, 2, "f32", "shuffled"),
+    (3, 32, "bf16", 9_001, 0, "f32", "contiguous"),
 ]
 
 
@@ -297,7 +307,8 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
                                            (32, 4, "f32", 2, "f32"), (2, 64, "bf16", 1, "bf16"),
                                            (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
                                            (16, 4, "f32", 2, "f32"), (6, 1, "f32", 2, "f32"),
-                                           (8, 3, "bf16", 1, "f32"), (4, 6, "f32", 2, "f32")])
+                                           (8, 3, "bf16", 1, "f32"), (4, 6, "f32", 2, "f32"),
+                                           (2, 12, "f32", 2, "f32"), (3, 32, "bf16", 1, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
