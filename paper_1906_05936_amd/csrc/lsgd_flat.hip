@@ -31,8 +31,8 @@ template <typename GT, int W, int G>
 FlatKernel flat_ct(bool cached) {
     constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
-        if (cached) return step_flat_ct<GT, W, G, U, 1>;
-    return step_flat_ct<GT, W, G, U, 0>;
+        if (cached) return flat_step_kernel<GT, W, G, U, 1>();
+    return flat_step_kernel<GT, W, G, U, 0>();
 }
 
 template <typename GT, int W>

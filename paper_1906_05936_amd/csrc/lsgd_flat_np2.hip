@@ -12,8 +12,8 @@ template <typename GT, int W, int G>
 FlatKernel np2_flat(bool cached) {
     constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
-        if (cached) return step_flat_ct<GT, W, G, U, 1>;
-    return step_flat_ct<GT, W, G, U, 0>;
+        if (cached) return flat_step_kernel<GT, W, G, U, 1>();
+    return flat_step_kernel<GT, W, G, U, 0>();
 }
 
 template <typename GT, int G>

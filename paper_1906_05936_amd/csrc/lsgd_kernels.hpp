@@ -869,7 +869,7 @@ struct FlatSrcT {
 // only when that is nonzero): the lane whose partial tile holds it runs it
 // through the TAIL form of the unit body.
 template <typename GT, int W, int G, int U, int CACHED>
-__global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
+__device__ __forceinline__ void step_flat_ct_body(const StepArgs& a) {
     constexpr int VEC = Unit<GT>::VEC;
     const FlatSrcT<CACHED> s{a, resolve_hyper(a.h, a.lr_ptr)};
     const int64_t full = a.n / VEC;
@@ -881,6 +881,62 @@ __global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
             if (u < full) fused_unit_ct<GT, W, G, false>(s, u * VEC, VEC);
             else fused_unit_ct<GT, W, G, true>(s, u * VEC, rem);
         });
+}
+
+template <typename GT, int W, int G, int U, int CACHED>
+__global__ __launch_bounds__(kBlock) void step_flat_ct(StepArgs a) {
+    step_flat_ct_body<GT, W, G, U, CACHED>(a);
+}
+
+// The same kernel with at most CAP waves per SIMD. Left to itself, the
+// compiler schedules for the highest occupancy the registers allow, and
+// for some groupings it gets there by holding fewer loads in flight: the
+// bfloat16 kernels for groups of 3 in 8 or more groups sink each gradient
+// load to its use and wait for it (one 16-byte load in flight per wave), and
+// the small binary32 groupings run four or more waves with short load
+// batches. Under a cap of 2 or 3 the scheduler keeps a batch of loads in
+// flight instead.
+template <typename GT, int W, int G, int U, int CACHED, int CAP>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(1, CAP))) void step_flat_ct_cap(StepArgs a) {
+    step_flat_ct_body<GT, W, G, U, CACHED>(a);
+}
+
+// The wave cap of the compile-time flat step kernel for G groups of W
+// workers, 0 for none: measured, each grouping against the uncapped kernel
+// at the ResNet-50 size (25.6M elements, same process, replicas R = N and
+// R = 0). A grouping is listed where a cap gains at least one point of the
+// 8 TB/s peak on the mean of the two and loses at most one in either.
+struct WaveCapEntry {
+    short W, G, cap;
+};
+constexpr WaveCapEntry kWaveCapF32[] = {
+    {1, 8, 2},  {1, 16, 2}, {1, 128, 2}, {2, 4, 2},  {2, 8, 2},  {2, 12, 2}, {3, 3, 2},  {3, 4, 2},
+    {3, 5, 2},  {4, 2, 2},  {4, 4, 2},   {4, 6, 2},  {5, 2, 2},  {5, 3, 2},  {6, 2, 2},  {8, 1, 2},
+    {12, 1, 2}, {12, 5, 2}, {16, 1, 2},  {16, 2, 2}, {16, 4, 2}, {16, 8, 2}, {1, 2, 3},  {1, 3, 3},
+    {1, 4, 3},  {1, 5, 3},  {1, 6, 3},   {2, 1, 3},  {2, 2, 3},  {3, 1, 3},  {3, 2, 3},  {3, 8, 3},
+    {3, 12, 3}, {3, 16, 3}, {4, 1, 3},   {4, 3, 3},  {5, 1, 3},  {6, 1, 3},  {8, 6, 3},  {12, 3, 3},
+};
+constexpr WaveCapEntry kWaveCapBF16[] = {
+    {1, 2, 2}, {1, 4, 2},  {2, 1, 2},  {2, 2, 2}, {3, 1, 2}, {3, 8, 2}, {3, 12, 2},
+    {3, 16, 2}, {3, 32, 2}, {4, 1, 2}, {5, 16, 2}, {8, 1, 2}, {8, 6, 2}, {8, 12, 2},
+    {1, 8, 3}, {1, 16, 3}, {2, 4, 3}, {4, 2, 3}, {5, 1, 3}, {6, 1, 3},
+};
+template <typename GT>
+constexpr int flat_wave_cap(int W, int G) {
+    constexpr bool kBF16 = sizeof(GT) == 2;
+    const WaveCapEntry* t = kBF16 ? kWaveCapBF16 : kWaveCapF32;
+    const int n = kBF16 ? sizeof(kWaveCapBF16) / sizeof(WaveCapEntry) : sizeof(kWaveCapF32) / sizeof(WaveCapEntry);
+    for (int i = 0; i < n; ++i)
+        if (t[i].W == W && t[i].G == G) return t[i].cap;
+    return 0;
+}
+
+// The flat step kernel for (W, G): capped where the table says so.
+template <typename GT, int W, int G, int U, int CACHED>
+constexpr auto flat_step_kernel() {
+    constexpr int cap = flat_wave_cap<GT>(W, G);
+    if constexpr (cap != 0) return step_flat_ct_cap<GT, W, G, U, CACHED, cap>;
+    else return step_flat_ct<GT, W, G, U, CACHED>;
 }
 
 // Runtime group layouts (non-power-of-two or large counts, and the
