@@ -82,8 +82,8 @@ template <typename GT, int W, int G>
 PlanKernel plan_ct(bool cached) {
     constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
-        if (cached) return step_plan_kernel<GT, W, G, U, 1>;
-    return step_plan_kernel<GT, W, G, U, 0>;
+        if (cached) return plan_step_kernel<GT, W, G, U, 1>();
+    return plan_step_kernel<GT, W, G, U, 0>();
 }
 
 template <typename GT, int W>
@@ -210,21 +210,21 @@ lsgd_status launch_plan_copy_out(const lsgd_plan* plan, PlanArgs& a, hipStream_t
 template <typename GT, int W>
 LarsKernel pick_lars_g(int G) {
     switch (G) {
-        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W, 1)>;
-        case 2: return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2, 2)>;
-        case 4: return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4, 4)>;
-        case 8: return lars_norms_kernel<GT, W, 8, tile_units<GT>(W * 8, 8)>;
+        case 1: return lars_kernel_for<GT, W, 1>();
+        case 2: return lars_kernel_for<GT, W, 2>();
+        case 4: return lars_kernel_for<GT, W, 4>();
+        case 8: return lars_kernel_for<GT, W, 8>();
         case 16:
-            if constexpr (W * 16 <= kMaxWorkers) return lars_norms_kernel<GT, W, 16, tile_units<GT>(W * 16, 16)>;
+            if constexpr (W * 16 <= kMaxWorkers) return lars_kernel_for<GT, W, 16>();
             else return nullptr;
         case 32:
-            if constexpr (W <= 4) return lars_norms_kernel<GT, W, 32, tile_units<GT>(W * 32, 32)>;
+            if constexpr (W <= 4) return lars_kernel_for<GT, W, 32>();
             else return nullptr;
         case 64:
-            if constexpr (W <= 2) return lars_norms_kernel<GT, W, 64, tile_units<GT>(W * 64, 64)>;
+            if constexpr (W <= 2) return lars_kernel_for<GT, W, 64>();
             else return nullptr;
         case 128:
-            if constexpr (W == 1) return lars_norms_kernel<GT, W, 128, tile_units<GT>(W * 128, 128)>;
+            if constexpr (W == 1) return lars_kernel_for<GT, W, 128>();
             else return nullptr;
     }
     return nullptr;
@@ -233,12 +233,12 @@ LarsKernel pick_lars_g(int G) {
 template <typename GT, int W>
 LarsKernel pick_lars_big_w(int G) {
     switch (G) {
-        case 1: return lars_norms_kernel<GT, W, 1, tile_units<GT>(W, 1)>;
+        case 1: return lars_kernel_for<GT, W, 1>();
         case 2:
-            if constexpr (W * 2 <= kMaxWorkers) return lars_norms_kernel<GT, W, 2, tile_units<GT>(W * 2, 2)>;
+            if constexpr (W * 2 <= kMaxWorkers) return lars_kernel_for<GT, W, 2>();
             else return nullptr;
         case 4:
-            if constexpr (W * 4 <= kMaxWorkers) return lars_norms_kernel<GT, W, 4, tile_units<GT>(W * 4, 4)>;
+            if constexpr (W * 4 <= kMaxWorkers) return lars_kernel_for<GT, W, 4>();
             else return nullptr;
     }
     return nullptr;

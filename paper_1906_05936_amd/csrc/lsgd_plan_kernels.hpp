@@ -94,7 +94,7 @@ __device__ __forceinline__ void for_plan_chunks(const PlanArgs& a, const ChunkFn
 // Compile-time (W, G): tiles of U units kBlock apart, then the units of a
 // partial last tile, then the ragged end (thread 0).
 template <typename GT, int W, int G, int U, int CACHED>
-__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
+__device__ __forceinline__ void step_plan_body(const PlanArgs& a) {
     constexpr int VEC = Unit<GT>::VEC;
     for_plan_chunks<CACHED>(a, [&](const auto& s, const PlanChunk& ch, int32_t) {
         const int64_t full = ch.len / VEC;
@@ -112,6 +112,40 @@ __global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
         const int rem = static_cast<int>(ch.len - full * VEC);
         if (rem != 0 && threadIdx.x == 0) fused_unit_ct<GT, W, G, true>(s, ch.start + full * VEC, rem);
     });
+}
+
+template <typename GT, int W, int G, int U, int CACHED>
+__global__ __launch_bounds__(kBlock) void step_plan_kernel(PlanArgs a) {
+    step_plan_body<GT, W, G, U, CACHED>(a);
+}
+
+// The same kernel with at most CAP waves per SIMD (see step_flat_ct_cap).
+template <typename GT, int W, int G, int U, int CACHED, int CAP>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(1, CAP))) void step_plan_kernel_cap(PlanArgs a) {
+    step_plan_body<GT, W, G, U, CACHED>(a);
+}
+
+// Wave caps of the compile-time plan step kernel, measured as for the flat
+// one: the 161 ResNet-50 tensors, R = N, each grouping against the uncapped
+// kernel; a grouping is listed where a cap gains at least one point of the
+// 8 TB/s peak and no cap loses.
+constexpr WaveCapEntry kPlanWaveCapF32[] = {{2, 2, 2}, {2, 12, 2}, {3, 16, 3}};
+constexpr WaveCapEntry kPlanWaveCapBF16[] = {{2, 2, 2}, {3, 8, 2}, {3, 16, 2}};
+// The LARS norms kernel (pass 1), same measurement of the whole LARS step.
+constexpr WaveCapEntry kLarsWaveCapBF16[] = {{4, 4, 2}, {3, 8, 2}, {8, 8, 2}, {3, 16, 2}};
+
+template <size_t K>
+constexpr int wave_cap_in(const WaveCapEntry (&t)[K], int W, int G) {
+    for (size_t i = 0; i < K; ++i)
+        if (t[i].W == W && t[i].G == G) return t[i].cap;
+    return 0;
+}
+
+template <typename GT, int W, int G, int U, int CACHED>
+constexpr auto plan_step_kernel() {
+    constexpr int cap = sizeof(GT) == 2 ? wave_cap_in(kPlanWaveCapBF16, W, G) : wave_cap_in(kPlanWaveCapF32, W, G);
+    if constexpr (cap != 0) return step_plan_kernel_cap<GT, W, G, U, CACHED, cap>;
+    else return step_plan_kernel<GT, W, G, U, CACHED>;
 }
 
 // Runtime group layouts (non-power-of-two or large counts, and the
@@ -330,9 +364,8 @@ __device__ __forceinline__ void lars_tile_out(const PlanSrc& s, float* gb, const
 
 // Pass 1, compile-time (W, G).
 template <typename GT, int W, int G, int U>
-__global__ __launch_bounds__(kBlock) void lars_norms_kernel(LarsArgs la) {
+__device__ __forceinline__ void lars_norms_body(const LarsArgs& la, double (&lds)[kBlock / 64][2]) {
     constexpr int VEC = Unit<GT>::VEC;
-    __shared__ double lds[kBlock / 64][2];
     for_plan_chunks(la.pa, [&](const PlanSrc& s, const PlanChunk& ch, int32_t c) {
         float* gb = la.gbar + read_table(&la.gbar_off[ch.tensor]);
         double sp = 0.0, sg = 0.0;
@@ -367,6 +400,27 @@ __global__ __launch_bounds__(kBlock) void lars_norms_kernel(LarsArgs la) {
             la.partials[2 * static_cast<int64_t>(c) + 1] = sg;
         }
     });
+}
+
+template <typename GT, int W, int G, int U>
+__global__ __launch_bounds__(kBlock) void lars_norms_kernel(LarsArgs la) {
+    __shared__ double lds[kBlock / 64][2];
+    lars_norms_body<GT, W, G, U>(la, lds);
+}
+
+template <typename GT, int W, int G, int U, int CAP>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(1, CAP))) void lars_norms_kernel_cap(LarsArgs la) {
+    __shared__ double lds[kBlock / 64][2];
+    lars_norms_body<GT, W, G, U>(la, lds);
+}
+
+// The LARS norms kernel for (W, G), capped where kLarsWaveCapBF16 lists it.
+template <typename GT, int W, int G>
+constexpr auto lars_kernel_for() {
+    constexpr int U = tile_units<GT>(W * G, G);
+    constexpr int cap = sizeof(GT) == 2 ? wave_cap_in(kLarsWaveCapBF16, W, G) : 0;
+    if constexpr (cap != 0) return lars_norms_kernel_cap<GT, W, G, U, cap>;
+    else return lars_norms_kernel<GT, W, G, U>;
 }
 
 // Pass 1, runtime W and G (equal groups): one unit per lane.

@@ -13,8 +13,8 @@ template <typename GT, int W, int G>
 PlanKernel np2_plan(bool cached) {
     constexpr int U = tile_units<GT>(W * G, G);
     if constexpr (cached_state_for(W * G))
-        if (cached) return step_plan_kernel<GT, W, G, U, 1>;
-    return step_plan_kernel<GT, W, G, U, 0>;
+        if (cached) return plan_step_kernel<GT, W, G, U, 1>();
+    return plan_step_kernel<GT, W, G, U, 0>();
 }
 
 template <typename GT, int G>
@@ -43,7 +43,7 @@ PlanKernel np2_plan_w(int W, bool cached) {
 
 template <typename GT, int W, int G>
 Np2LarsKernel np2_lars() {
-    return lars_norms_kernel<GT, W, G, tile_units<GT>(W * G, G)>;
+    return lars_kernel_for<GT, W, G>();
 }
 
 template <typename GT, int G>
