@@ -49,7 +49,7 @@ def draw(k):
     equal = rng.random() < 0.6
     if equal:
         G = int(rng.choice([1, 2, 3, 4, 5, 6, 8, 12, 16]))
-        W = int(rng.choice([1, 2, 3, 4, 6, 8]))
+        W = int(rng.choice([1, 2, 3, 4, 5, 6, 7, 8, 12, 32]))
         while G * W > 128:
             W = max(1, W // 2)
         gow = workloads.shuffled_groups(G, W, int(rng.integers(1 << 30)))
