@@ -112,6 +112,13 @@ STEP_CASES = [
     (8, 8, "bf16", 4_000_003, 64, "bf16", "shuffled"),
     (16, 8, "f32", 2_000_003, 128, "f32", "shuffled"),
     (16, 4, "f32", 2_000_003, 8, "f32", "shuffled"),    # 16 groups of 4: two-unit tiles
+    # kernels with a wave cap, on the chunked grid: 8 bf16 groups of 3 (cap 2),
+    # 2 fp32 groups of 5 and 2 bf16 groups of 2 with cached state (cap 2), one
+    # fp32 group of 3 (cap 3)
+    (8, 3, "bf16", 4_000_003, 0, "f32", "shuffled"),
+    (2, 5, "f32", 2_000_003, 10, "f32", "shuffled"),
+    (2, 2, "bf16", 4_000_003, 4, "f32", "contiguous"),
+    (1, 3, "f32", 2_000_003, 3, "f32", "contiguous"),
     # compile-time kernels for 32 to 128 groups of few workers, and for groups
     # of 32 to 128 workers (members streamed through an accumulator)
     (32, 4, "f32", 300_007, 8, "f32", "shuffled"),
@@ -308,7 +315,9 @@ PLAN_SIZES = [1, 3, 64, 1000, 8191, 8192, 8193, 20_000, 5, 64, 4096, 9408, 16_38
                                            (12, 8, "f32", 1, "f32"), (20, 3, "bf16", 0, "f32"),
                                            (16, 4, "f32", 2, "f32"), (6, 1, "f32", 2, "f32"),
                                            (8, 3, "bf16", 1, "f32"), (4, 6, "f32", 2, "f32"),
-                                           (2, 12, "f32", 2, "f32"), (3, 32, "bf16", 1, "f32")])
+                                           (2, 12, "f32", 2, "f32"), (3, 32, "bf16", 1, "f32"),
+                                           (2, 2, "bf16", 2, "f32"), (32, 3, "bf16", 1, "f32"),
+                                           (1, 3, "f32", 3, "f32")])
 def test_plan_matches_oracle(G, W, gdt, R, rdt):
     log("plan G=%d W=%d %s R=%d" % (G, W, gdt, R))
     rng = np.random.default_rng(G * 100 + W)
